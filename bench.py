@@ -1,0 +1,318 @@
+#!/usr/bin/env python3
+"""Benchmark of the unified AI-query pipeline on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload reviews]
+
+A step is one aiq_run of the whole query over device-resident inputs: WHERE
++ stable selection, varlen pack, decoder prefill, label head + decision,
+kept ids + COUNT, on one HIP stream.  The default workload is the
+reviews-shaped binary filter: 16,384 synthetic rows (seed 1), a 4-layer d512
+bf16 SwiGLU decoder.
+
+Printed (one JSON line): rows/s (table rows / end-to-end step time) as the
+value, tokens/s, a per-stage breakdown, the roofline of the dominant kernel
+(the gate/up SwiGLU GEMM) measured with HIP events around its launches, the
+CPU oracle timed on a bounded sample of the same workload, and a
+split-execution baseline (host selection + pack, H2D copy of survivors in
+micro-batches of 128 rows, the same device prefill with full-vocabulary
+logits copied back, host decision and COUNT).
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes as C
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "AI-query rows/s and prefill tokens/s on 1 MI355X; MFMA % peak, HBM GB/s"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3
+PEAK_HBM_GBPS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+# ------------------------------------------------------------------ HIP events (raw handles for the C ABI)
+class HipEvents:
+    def __init__(self, n: int):
+        self.hip = C.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [C.POINTER(C.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [C.c_void_p]
+        self.ev = (C.c_void_p * n)()
+        for i in range(n):
+            h = C.c_void_p()
+            if self.hip.hipEventCreate(C.byref(h)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            self.ev[i] = h
+        self.n = n
+
+    def elapsed_ms(self, i: int, j: int) -> float:
+        ms = C.c_float()
+        if self.hip.hipEventElapsedTime(C.byref(ms), self.ev[i], self.ev[j]) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(ms.value)
+
+    def close(self):
+        for i in range(self.n):
+            self.hip.hipEventDestroy(self.ev[i])
+
+
+def make_trace(B, events: HipEvents, kind_mask: int):
+    cap = events.n // 2
+    tags = (C.c_int32 * cap)()
+    t = B.aiq_trace()
+    t.events = C.cast(events.ev, C.POINTER(C.c_void_p))
+    t.tags = C.cast(tags, C.POINTER(C.c_int32))
+    t.capacity, t.count, t.kind_mask = cap, 0, kind_mask
+    t._tags = tags
+    return t
+
+
+def per_kind_ms(B, trace, events) -> dict:
+    out = {}
+    for i in range(trace.count):
+        k = trace._tags[i]
+        out.setdefault(k, []).append(events.elapsed_ms(2 * i, 2 * i + 1))
+    return out
+
+
+# ------------------------------------------------------------------ algorithmic work
+def prefill_flops(spec, lens: np.ndarray, n_labels: int) -> dict:
+    """Algorithmic FLOPs of the prefill (no padding): the four projections,
+    causal attention (unmasked half: QK^T and PV), and the label head."""
+    T = float(lens.sum())
+    d, dq, dkv, f, L = spec.d_model, spec.d_q, spec.d_kv, spec.d_ff, spec.n_layers
+    n_ffn = 3 if spec.act == "swiglu" else 2
+    per = {
+        "qkv": 2 * T * d * (dq + 2 * dkv) * L,
+        "o": 2 * T * dq * d * L,
+        "up": 2 * T * d * f * (n_ffn - 1) * L,
+        "down": 2 * T * f * d * L,
+        "attn": float(np.sum(2.0 * dq * lens * (lens + 1.0))) * L,
+        "head": 2.0 * len(lens) * n_labels * d,
+    }
+    per["total"] = sum(per.values())
+    return per
+
+
+def host_select(cols: dict, preds) -> np.ndarray:
+    """Split baseline's host WHERE: numpy masks, then the ascending row ids."""
+    n = len(cols["id"])
+    m = np.ones(n, dtype=bool)
+    ops = {"lt": np.less, "le": np.less_equal, "gt": np.greater, "ge": np.greater_equal,
+           "eq": np.equal, "ne": np.not_equal}
+    for p in preds:
+        v = cols[p.col].astype(np.int64)
+        m &= np.isin(v, np.asarray(p.values, dtype=np.int64)) if p.op == "in" else ops[p.op](v, p.k)
+    return np.flatnonzero(m)
+
+
+# ------------------------------------------------------------------ legs
+def cpu_baseline_leg(tables, model, q, n_rows_sample: int) -> dict:
+    """The CPU oracle (fp64, per sequence) on the first rows of the table."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        blas = 1
+    cores = len(os.sched_getaffinity(0))
+    probe = tables["probe"]
+    R = min(n_rows_sample, len(probe["id"]))
+    sub = {k: (v[:R + 1] if k == "offsets" else v if k == "tokens" else v[:R]) for k, v in probe.items()}
+    st = {"probe": sub, "build": tables.get("build"), "prefix": tables["prefix"]}
+    t0 = time.perf_counter()
+    res = oracle.run_query(st, model, q)
+    dt = time.perf_counter() - t0
+    return {"value": R / dt, "unit": "rows/s", "cores": int(max(blas, 1)), "host_cores": cores, "kind": "oracle",
+            "sample": f"first {R} of {len(probe['id'])} table rows: full query on them "
+                      f"({len(res['rows'])} selected rows, {res['n_tokens']} tokens, fp64 per-sequence forward)",
+            "seconds": dt}
+
+
+def split_baseline_leg(tables, model, q, dm, B, torch, micro=128) -> dict:
+    """Host selection + pack, per micro-batch H2D, device prefill with the
+    full-vocabulary last-position logits, D2H, host decision + COUNT."""
+    from paper_2608_10139_amd.device import DevicePrefill
+    probe = tables["probe"]
+    lens_all = np.diff(probe["offsets"])
+    max_tok = micro * (int(lens_all.max()) + q.n_prefix)
+    pf = DevicePrefill(model, labels=q.labels, max_tokens=max_tok, dmodel=dm)
+    V = dm.spec.vocab
+    tok_pin = torch.empty(max_tok, dtype=torch.int32, pin_memory=True)
+    cu_pin = torch.empty(micro + 1, dtype=torch.int32, pin_memory=True)
+    out_pin = torch.empty(micro * V, dtype=torch.float32, pin_memory=True)
+    tok_d = torch.empty(max_tok, dtype=torch.int32, device="cuda")
+    cu_d = torch.empty(micro + 1, dtype=torch.int32, device="cuda")
+    labels = list(q.labels)
+    prefix = np.asarray(tables["prefix"][:q.n_prefix], dtype=np.int32)
+
+    def one_pass():
+        rows = host_select(probe, q.preds)
+        kept = 0
+        for b0 in range(0, len(rows), micro):
+            rb = rows[b0:b0 + micro]
+            seqs = [np.concatenate([prefix, probe["tokens"][probe["offsets"][r]:probe["offsets"][r + 1]]])
+                    for r in rb]
+            cu = np.zeros(len(rb) + 1, dtype=np.int32)
+            cu[1:] = np.cumsum([len(s) for s in seqs])
+            n_tok = int(cu[-1])
+            tok_pin[:n_tok].copy_(torch.from_numpy(np.concatenate(seqs).astype(np.int32)))
+            cu_pin[:len(cu)].copy_(torch.from_numpy(cu))
+            tok_d[:n_tok].copy_(tok_pin[:n_tok], non_blocking=True)
+            cu_d[:len(cu)].copy_(cu_pin[:len(cu)], non_blocking=True)
+            lg = pf.run(tok_d[:n_tok], cu_d[:len(cu)], full_vocab=True)
+            out_pin[:lg.numel()].copy_(lg.reshape(-1), non_blocking=True)
+            torch.cuda.synchronize()
+            full = out_pin[:lg.numel()].numpy().reshape(len(rb), V)
+            kept += int(np.sum(full[:, labels[0]] > full[:, labels[1]]))
+        return len(rows), kept
+
+    one_pass()   # warm-up
+    t0 = time.perf_counter()
+    n_sel, kept = one_pass()
+    dt = time.perf_counter() - t0
+    pf.close()
+    n = len(probe["id"])
+    return {"value": n / dt, "unit": "rows/s", "ms": dt * 1e3, "selected": n_sel, "kept": kept,
+            "micro_batch": micro, "logits": f"fp32 [{micro}, {V}] per micro-batch, D2H"}
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="reviews")
+    ap.add_argument("--cpu-rows", type=int, default=1024)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-split", action="store_true")
+    a = ap.parse_args(argv)
+    if a.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {a.gpus}); the pipeline is single-GPU "
+              "and multi-GPU sharding is not implemented", file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2608_10139_amd import binding as B
+    from paper_2608_10139_amd.device import DeviceModel, DeviceQuery
+    from synth import WORKLOADS
+    from synth.gen import make_model, make_tables
+
+    torch.cuda.set_device(0)
+    w = WORKLOADS[a.workload]
+    q = w.queries[0]
+    spec = w.model
+    log(f"[bench] generating {a.workload}: {w.description}")
+    tables = make_tables(w)
+    model = make_model(spec)
+    dm = DeviceModel(model)
+    dq = DeviceQuery(tables, model, q, dmodel=dm)
+    log(f"[bench] workspace {dq.ws_bytes / 2**30:.2f} GiB; warmup {a.warmup}")
+
+    for _ in range(a.warmup):
+        dq.run()
+    torch.cuda.synchronize()
+    res = dq.results()
+    if res["status"] != 0:
+        raise RuntimeError(f"device status {res['status']:#x}")
+    n_rows = len(tables["probe"]["id"])
+    sel = res["sel_ids"]
+    lens = tables["probe"]["len"][sel].astype(np.float64) + q.n_prefix
+    T = int(lens.sum())
+    assert T == res["n_tokens"]
+
+    # ---- timed region: whole steps; HIP events around the dominant kernel's launches only
+    launches_per_step = spec.n_layers * 8
+    ev = HipEvents(2 * a.steps * launches_per_step)
+    trace = make_trace(B, ev, 1 << B.AIQ_K_GEMM_UP)
+    log(f"[bench] timing {a.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(a.steps):
+        dq.run(trace=trace)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    ms_step = dt / a.steps * 1e3
+    up = per_kind_ms(B, trace, ev).get(B.AIQ_K_GEMM_UP, [])
+    ev.close()
+    fl = prefill_flops(spec, lens, len(q.labels))
+    # every launch of the gate/up GEMM covers one chunk; empty chunks (none at
+    # the default chunk size here) would contribute zero work
+    n_up = len(up)
+    up_flops_per_launch = fl["up"] * a.steps / max(n_up, 1)
+    up_avg_ms = float(np.mean(up)) if up else float("nan")
+    achieved = up_flops_per_launch / (up_avg_ms * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if spec.dtype == "bf16" else PEAK_F32_TFLOPS
+
+    # ---- one untimed traced step for the stage breakdown
+    ev2 = HipEvents(2 * (launches_per_step + 64))
+    tr2 = make_trace(B, ev2, 0xFFFFFFFF)
+    dq.run(trace=tr2)
+    torch.cuda.synchronize()
+    kinds = per_kind_ms(B, tr2, ev2)
+    ev2.close()
+    names = {B.AIQ_K_REL: "relational", B.AIQ_K_PACK: "pack", B.AIQ_K_EMBED: "embed", B.AIQ_K_NORM: "rmsnorm",
+             B.AIQ_K_GEMM_QKV: "gemm_qkv_rope", B.AIQ_K_ATTN: "attention", B.AIQ_K_GEMM_O: "gemm_o_resid",
+             B.AIQ_K_GEMM_UP: "gemm_gate_up_swiglu", B.AIQ_K_GEMM_DOWN: "gemm_down_resid", B.AIQ_K_HEAD: "head",
+             B.AIQ_K_AGG: "decision_agg"}
+    stages = {names[k]: round(float(np.sum(v)), 4) for k, v in sorted(kinds.items())}
+    prefill_kinds = [B.AIQ_K_EMBED, B.AIQ_K_NORM, B.AIQ_K_GEMM_QKV, B.AIQ_K_ATTN, B.AIQ_K_GEMM_O,
+                     B.AIQ_K_GEMM_UP, B.AIQ_K_GEMM_DOWN, B.AIQ_K_HEAD]
+    prefill_ms = sum(float(np.sum(kinds.get(k, []))) for k in prefill_kinds)
+    gemm = {"gemm_qkv_rope": ("qkv", B.AIQ_K_GEMM_QKV), "gemm_o_resid": ("o", B.AIQ_K_GEMM_O),
+            "gemm_gate_up_swiglu": ("up", B.AIQ_K_GEMM_UP), "gemm_down_resid": ("down", B.AIQ_K_GEMM_DOWN)}
+    gemm_frac = {}
+    for nm, (key, k) in gemm.items():
+        t = float(np.sum(kinds.get(k, [0.0])))
+        gemm_frac[nm] = round(fl[key] / (t * 1e-3) / 1e12 / peak, 4) if t > 0 else None
+    # relational bytes: referenced columns per row + 4 B per selected id
+    col_bytes = sum(np.asarray(tables["probe"][p.col]).dtype.itemsize for p in {p.col: p for p in q.preds}.values())
+    rel_bytes = n_rows * col_bytes + 4 * len(sel)
+    rel_ms = float(np.sum(kinds.get(B.AIQ_K_REL, [0.0])))
+
+    result = {
+        "metric": METRIC, "value": round(n_rows / (ms_step * 1e-3), 2), "unit": "rows/s",
+        "n_gpus": 1, "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": spec.dtype,
+        "data": "synthetic (seeded tables and random-init weights)",
+        "config": {"workload": f"{a.workload}: {w.description}", "rows": n_rows, "selected": len(sel),
+                   "kept": res["count"], "tokens": T, "model": f"{spec.n_layers}L d{spec.d_model} "
+                   f"{spec.n_heads}q/{spec.n_kv_heads}kv ffn{spec.d_ff} {spec.act} {spec.dtype}",
+                   "parallelism": "single GPU"},
+        "tokens_per_s": round(T / (ms_step * 1e-3), 1),
+        "prefill_tokens_per_s": round(T / (prefill_ms * 1e-3), 1) if prefill_ms > 0 else None,
+        "prefill_mfma_frac": round(fl["total"] / (prefill_ms * 1e-3) / 1e12 / peak, 4) if prefill_ms > 0 else None,
+        "gemm_mfma_frac": gemm_frac,
+        "stages_ms": stages,
+        "relational_gbps": round(rel_bytes / (rel_ms * 1e-3) / 1e9, 2) if rel_ms > 0 else None,
+        "roofline": {"bound": "mfma", "kernel": "k_gemm_bf16<EPI_SWIGLU> (gate/up projection + SwiGLU)",
+                     "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "traffic": None,
+                     "launches": n_up, "avg_launch_ms": round(up_avg_ms, 5),
+                     "flops_per_launch": up_flops_per_launch},
+    }
+    if not a.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle on a sample)")
+        result["cpu_baseline"] = cpu_baseline_leg(tables, model, q, a.cpu_rows)
+    if not a.no_split:
+        log("[bench] split-execution baseline")
+        result["split_baseline"] = split_baseline_leg(tables, model, q, dm, B, torch)
+    dq.close()
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,293 @@
+/*
+ * aiq.h -- unified AI-query execution on one gfx950 GPU: C ABI.
+ *
+ * One call runs a hybrid SQL + LLM query as a single device-resident
+ * pipeline on one HIP stream:
+ *
+ *   FROM      columnar table already in device memory            (Table 1, FROM)
+ *   WHERE     conjunction of integer predicates -> stable selection (Table 1, WHERE)
+ *   JOIN      optional inner PK-FK hash join with a filtered build table
+ *             (the reviews-JOIN-movies workload of Section 4)
+ *   AI_IF     gather + pack the selected rows' token lists into a variable-
+ *             length batch, decoder-only transformer prefill, last-position
+ *             label logits, strict "yes > no" or argmax decision
+ *             (Table 1, AI_IF; Figure 2)
+ *   aggregate COUNT, kept row ids, or GROUP BY key AVG(label)/COUNT(*)
+ *             (Table 1, SELECT SUM as a masked reduction; Figure 2)
+ *
+ * Nothing is copied between host and device inside aiq_run: only the caller
+ * reads the (small) outputs afterwards (Section 3.3, H2D boundary
+ * consolidation).  Shapes stay data-dependent on the device: survivor counts,
+ * token counts and sequence lengths are never read back, and the selection
+ * skips non-matching rows before the model runs (Section 5, the dynamic-shape
+ * and dynamic data-skipping roadmap items).
+ *
+ * Conventions
+ *  - Every pointer documented as "device" is a device address owned by the
+ *    caller; the library never allocates, frees or retains device memory.
+ *  - Pointers documented as "host" are read during the call only, except
+ *    that aiq_plan_create copies everything it needs into the plan.
+ *  - `stream` is a hipStream_t (NULL = the null stream).  Calls that take a
+ *    stream only enqueue work; they never synchronise the device and never
+ *    copy data to or from the host.
+ *  - Host-detectable errors return a negative aiq_status and enqueue nothing.
+ *    Errors that only the device can see (token id out of range, duplicate
+ *    build key, capacity exceeded, ...) set bits of the device status word
+ *    (aiq_out.scalars[AIQ_S_STATUS]); after such a bit is set the other
+ *    outputs are unspecified.
+ *  - No C++ exception crosses this interface.
+ *  - A plan is immutable after creation and holds host metadata only; one
+ *    plan may be used by concurrent calls provided each call has its own
+ *    workspace and outputs.
+ */
+#ifndef AIQ_H
+#define AIQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define AIQ_ABI_VERSION 1
+
+typedef enum aiq_status {
+  AIQ_OK = 0,
+  AIQ_EINVAL = -1,        /* null pointer, bad enum, inconsistent shapes      */
+  AIQ_EUNSUPPORTED = -2,  /* valid request that this build does not implement */
+  AIQ_ENOSPC = -3,        /* workspace or capacity too small                  */
+  AIQ_EHIP = -4,          /* a HIP runtime call or kernel launch failed       */
+  AIQ_ENOMEM = -5         /* host allocation of the plan failed               */
+} aiq_status;
+
+/* element types of columns and weights */
+typedef enum aiq_dtype {
+  AIQ_I8 = 1, AIQ_I16 = 2, AIQ_I32 = 3, AIQ_F32 = 4, AIQ_BF16 = 5
+} aiq_dtype;
+
+/* predicate operators: `col op k`, or `col IN (set)` */
+typedef enum aiq_op {
+  AIQ_LT = 0, AIQ_LE = 1, AIQ_GT = 2, AIQ_GE = 3, AIQ_EQ = 4, AIQ_NE = 5, AIQ_IN = 6
+} aiq_op;
+
+typedef enum aiq_act { AIQ_ACT_GELU_ERF = 1, AIQ_ACT_SWIGLU = 2 } aiq_act;
+typedef enum aiq_decision { AIQ_DECIDE_BINARY_GT = 1, AIQ_DECIDE_ARGMAX = 2 } aiq_decision;
+typedef enum aiq_agg {
+  AIQ_AGG_COUNT = 1,             /* COUNT(*) of kept rows (+ their ids)                  */
+  AIQ_AGG_AVG_LABEL_COUNT_BY = 2,/* GROUP BY probe column: COUNT(*), SUM/AVG(label)      */
+  AIQ_AGG_COUNT_BY_PAYLOAD = 3   /* GROUP BY joined build payload: COUNT(*) of kept rows */
+} aiq_agg;
+typedef enum aiq_logits_mode { AIQ_LOGITS_LABELS = 1, AIQ_LOGITS_FULL_VOCAB = 2 } aiq_logits_mode;
+
+/* device status bits (aiq_out.scalars[AIQ_S_STATUS]) */
+#define AIQ_DEV_TOKEN_RANGE 0x01  /* a token id outside [0, vocab): treated as 0   */
+#define AIQ_DEV_DUP_KEY     0x02  /* duplicate key among the passing build rows     */
+#define AIQ_DEV_HASH_FULL   0x04  /* hash table overflow                            */
+#define AIQ_DEV_IDS_CAP     0x08  /* more kept rows than aiq_out.ids_cap            */
+#define AIQ_DEV_GROUP_RANGE 0x10  /* group key outside [0, n_group_keys): skipped   */
+#define AIQ_DEV_LIST_LEN    0x20  /* a row's list longer than max_list_len          */
+#define AIQ_DEV_GROUP_CAP   0x40  /* more groups than aiq_out.grp_cap               */
+
+/* indices into aiq_out.scalars (int64, device) */
+#define AIQ_S_SELECTED 0   /* rows passing WHERE (and the join)                      */
+#define AIQ_S_KEPT     1   /* rows kept after the AI decision (argmax: = selected)   */
+#define AIQ_S_TOKENS   2   /* total prefill tokens (prefix + row tokens)             */
+#define AIQ_S_STATUS   3   /* OR of AIQ_DEV_* bits                                   */
+#define AIQ_S_GROUPS   4   /* number of non-empty groups written                     */
+#define AIQ_N_SCALARS  8
+
+#define AIQ_MAX_PREDS 8
+#define AIQ_MAX_IN_SET 32
+#define AIQ_MAX_PREFIX 64
+#define AIQ_MAX_LABELS 8
+
+/* One fixed-width column: `data` is a device array of n_rows elements. */
+typedef struct aiq_col {
+  const void* data;
+  int32_t dtype;          /* AIQ_I8, AIQ_I16 or AIQ_I32 */
+} aiq_col;
+
+/*
+ * A columnar table in device memory.  The probe table also carries one list
+ * column (the text of each row as token ids): row r owns
+ * list_tokens[list_offsets[r] .. list_offsets[r+1]).
+ */
+typedef struct aiq_table {
+  int64_t n_rows;
+  int32_t n_cols;
+  const aiq_col* cols;           /* host array of n_cols descriptors            */
+  const int64_t* list_offsets;   /* device [n_rows + 1], non-decreasing, or NULL */
+  const int32_t* list_tokens;    /* device                                      */
+  int64_t n_list_tokens;         /* host: list_offsets[n_rows] - list_offsets[0] */
+  int32_t max_list_len;          /* host: declared bound on any row's list length */
+} aiq_table;
+
+/* one predicate atom: cols[col] op k, or cols[col] IN set[0..n_set) */
+typedef struct aiq_pred {
+  int32_t col;
+  int32_t op;                    /* aiq_op */
+  int64_t k;
+  int32_t n_set;
+  int64_t set[AIQ_MAX_IN_SET];
+} aiq_pred;
+
+/*
+ * Decoder layer weights, device pointers.  Matrices are row-major [out, in]
+ * in the model's weight dtype; norm gains are float32 [d_model].
+ *   wq [n_heads*hd, d]   wk, wv [n_kv_heads*hd, d]   wo [d, n_heads*hd]
+ *   SwiGLU:  w_gate, w_up [d_ff, d], w_down [d, d_ff]
+ *   GELU:    w_gate = W1 [d_ff, d], w_up unused (NULL), w_down = W2 [d, d_ff]
+ */
+typedef struct aiq_layer {
+  const float* attn_norm;
+  const void* wq; const void* wk; const void* wv; const void* wo;
+  const float* ffn_norm;
+  const void* w_gate; const void* w_up; const void* w_down;
+} aiq_layer;
+
+typedef struct aiq_model {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, d_ff, vocab;
+  int32_t act;                   /* aiq_act */
+  int32_t wdtype;                /* AIQ_F32 or AIQ_BF16 */
+  double rope_theta;             /* rotary base, e.g. 10000 */
+  double norm_eps;               /* RMSNorm epsilon, e.g. 1e-5 */
+  const void* emb;               /* device [vocab, d] */
+  const aiq_layer* layers;       /* host array of n_layers */
+  const float* final_norm;       /* device [d] */
+  const void* lm_head;           /* device [vocab, d] */
+} aiq_model;
+
+typedef struct aiq_query {
+  int32_t n_pred;
+  aiq_pred preds[AIQ_MAX_PREDS];       /* conjunction over probe columns */
+  /* optional inner join probe.cols[probe_key_col] = build.cols[build_key_col]
+     with the build rows passing build_preds; the build key must be unique
+     among passing rows.  build_payload_col is carried to each joined row. */
+  int32_t join;                        /* 0 = no join, 1 = inner PK-FK join */
+  int32_t probe_key_col, build_key_col, build_payload_col;
+  int32_t n_build_pred;
+  aiq_pred build_preds[AIQ_MAX_PREDS];
+  int32_t n_prefix;                    /* prompt tokens placed before each row's list */
+  int32_t prefix[AIQ_MAX_PREFIX];
+  int32_t n_labels;                    /* 2..AIQ_MAX_LABELS */
+  int32_t label_ids[AIQ_MAX_LABELS];
+  int32_t decision;                    /* aiq_decision: BINARY_GT keeps a row iff
+                                          logit[label_ids[0]] > logit[label_ids[1]] */
+  int32_t agg;                         /* aiq_agg */
+  int32_t group_col;                   /* AVG_LABEL_COUNT_BY: probe column (I32) */
+  int32_t n_group_keys;                /* group keys are codes in [0, n_group_keys) */
+} aiq_query;
+
+typedef struct aiq_plan_opts {
+  int64_t chunk_tokens;                /* prefill chunk size in tokens; 0 = default */
+  int32_t n_layers_override;           /* diagnostics: 0 = every layer, n > 0 = the first n
+                                          layers, negative = no layer (embedding -> head) */
+  int32_t reserved[5];
+} aiq_plan_opts;
+
+/*
+ * Outputs, all device buffers owned by the caller.  Optional buffers may be
+ * NULL.  Row ids are probe-table row indices.
+ */
+typedef struct aiq_out {
+  int64_t* scalars;          /* [AIQ_N_SCALARS], see AIQ_S_* */
+  int32_t* ids;              /* kept row ids, ascending; capacity ids_cap */
+  int64_t ids_cap;
+  int32_t* sel_ids;          /* optional: selected row ids (ascending), cap sel_cap */
+  int32_t* sel_labels;       /* optional: label value per selected row (binary 1/0,
+                                argmax: the winning label token id) */
+  float* sel_logits;         /* optional: [sel_cap, n_labels] label logits */
+  int64_t sel_cap;
+  int32_t* grp_key;          /* groups in ascending key order, capacity grp_cap */
+  int64_t* grp_count;
+  int64_t* grp_sum;          /* SUM(label) (0 for COUNT_BY_PAYLOAD) */
+  double* grp_avg;           /* SUM/COUNT in fp64 (0 for COUNT_BY_PAYLOAD) */
+  int64_t grp_cap;
+} aiq_out;
+
+/*
+ * Optional stage timing: the library records a pair of HIP events around
+ * every kernel launch whose kind is selected in `kind_mask` (bit k = kind k,
+ * see AIQ_K_*), writing tags[i] = kind for the pair events[2i], events[2i+1].
+ * Recording starts at pair index `count` and advances it, so one trace can
+ * span several calls (set count = 0 first); it stops silently once
+ * `capacity` pairs are used.  events[] are hipEvent_t created by the caller
+ * with timing enabled.
+ */
+typedef struct aiq_trace {
+  void** events;
+  int32_t* tags;
+  int32_t capacity;
+  int32_t count;
+  uint32_t kind_mask;
+} aiq_trace;
+
+enum {
+  AIQ_K_REL = 0,        /* predicate / join / compaction kernels */
+  AIQ_K_PACK = 1,       /* sequence lengths, scans, token gather, chunking */
+  AIQ_K_EMBED = 2,
+  AIQ_K_NORM = 3,
+  AIQ_K_GEMM_QKV = 4,
+  AIQ_K_ATTN = 5,
+  AIQ_K_GEMM_O = 6,
+  AIQ_K_GEMM_UP = 7,    /* gate/up (SwiGLU) or W1 (GELU) */
+  AIQ_K_GEMM_DOWN = 8,
+  AIQ_K_HEAD = 9,
+  AIQ_K_AGG = 10
+};
+
+typedef struct aiq_plan aiq_plan;
+
+/*
+ * Validates the model, tables and query and builds an immutable plan.
+ * probe may be NULL for a prefill-only plan (aiq_prefill_packed); build must
+ * be non-NULL iff query->join.  query may be NULL for a prefill-only plan
+ * that only uses AIQ_LOGITS_FULL_VOCAB.  opts may be NULL.
+ * Errors: AIQ_EINVAL (bad pointer, dtype, op, column index, d_model % n_heads,
+ * n_heads % n_kv_heads, head dim not in {32, 64, 128}), AIQ_EUNSUPPORTED,
+ * AIQ_ENOMEM.  On error *out is set to NULL.
+ */
+aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const aiq_table* build,
+                           const aiq_query* query, const aiq_plan_opts* opts, aiq_plan** out);
+
+/* Bytes of device workspace aiq_run needs (256-byte aligned base required). */
+aiq_status aiq_workspace_size(const aiq_plan* plan, size_t* bytes);
+
+/*
+ * Enqueues the whole query on `stream`.  The workspace contents on entry do
+ * not matter.  Outputs are valid after the caller synchronises the stream.
+ * Errors: AIQ_EINVAL (NULL plan/out/scalars/ids, prefill-only plan, a
+ * group-by without grp_* buffers), AIQ_ENOSPC (ws_bytes too small),
+ * AIQ_EHIP.  `trace` may be NULL.
+ */
+aiq_status aiq_run(const aiq_plan* plan, void* workspace, size_t ws_bytes, const aiq_out* out,
+                   aiq_trace* trace, void* stream);
+
+/* Bytes of workspace aiq_prefill_packed needs for up to max_tokens tokens. */
+aiq_status aiq_prefill_workspace_size(const aiq_plan* plan, int64_t max_tokens, size_t* bytes);
+
+/*
+ * Runs only the transformer on an already packed batch (device buffers):
+ * sequence i is tok[cu_seqlens[i] .. cu_seqlens[i+1]), cu_seqlens int32
+ * [n_seq+1] with cu_seqlens[0] = 0 and cu_seqlens[n_seq] = n_tok; positions
+ * restart at 0 in every sequence.  Writes the last position's logits of each
+ * sequence: AIQ_LOGITS_LABELS -> logits[n_seq, n_labels] for the plan's
+ * query labels; AIQ_LOGITS_FULL_VOCAB -> logits[n_seq, vocab].  This is the
+ * model half of the split-execution baseline (Section 3.3) and the kernel
+ * parity entry point.  Errors: AIQ_EINVAL, AIQ_ENOSPC (workspace, or n_tok
+ * above the workspace's token capacity), AIQ_EHIP.
+ */
+aiq_status aiq_prefill_packed(const aiq_plan* plan, const int32_t* tok, const int32_t* cu_seqlens,
+                              int32_t n_seq, int64_t n_tok, int32_t logits_mode, float* logits,
+                              void* workspace, size_t ws_bytes, void* stream);
+
+void aiq_plan_destroy(aiq_plan* plan);
+
+const char* aiq_status_str(int32_t status);
+int32_t aiq_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* AIQ_H */

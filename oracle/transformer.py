@@ -117,7 +117,7 @@ def forward_hidden(model: dict, seqs: list, n_layers: int | None = None) -> list
     L = len(model["layers"]) if n_layers is None else n_layers
     for l in range(L):
         Wl = W.layer(l)
-        xs = [_layer(x, Wl, spec) for x in xs]
+        xs = [_layer(x, Wl, spec) if len(x) else x for x in xs]
     return xs
 
 
@@ -126,18 +126,19 @@ def _last_normed(model: dict, xs: list) -> np.ndarray:
     g = Weights64.w(model["final_norm"])
     if not xs:
         return np.zeros((0, spec.d_model))
-    return np.stack([rmsnorm(x[-1], g, spec.norm_eps) for x in xs])
+    return np.stack([rmsnorm(x[-1], g, spec.norm_eps) if len(x) else np.zeros(spec.d_model) for x in xs])
 
 
-def label_logits(model: dict, seqs: list, labels) -> np.ndarray:
+def label_logits(model: dict, seqs: list, labels, n_layers: int | None = None) -> np.ndarray:
     """Last-position logits of the label tokens only, [n_seq, K] (Figure 2:
-    logits[:, -1, :] then the Yes / No columns)."""
-    hf = _last_normed(model, forward_hidden(model, seqs))
+    logits[:, -1, :] then the Yes / No columns).  ``n_layers`` truncates the
+    layer stack (diagnostics).  An empty sequence has all-zero logits."""
+    hf = _last_normed(model, forward_hidden(model, seqs, n_layers))
     rows = Weights64.w(model["lm_head"][np.asarray(labels, dtype=np.int64)])
     return hf @ rows.T
 
 
-def full_logits(model: dict, seqs: list) -> np.ndarray:
+def full_logits(model: dict, seqs: list, n_layers: int | None = None) -> np.ndarray:
     """Last-position logits over the whole vocabulary, [n_seq, V]."""
-    hf = _last_normed(model, forward_hidden(model, seqs))
+    hf = _last_normed(model, forward_hidden(model, seqs, n_layers))
     return hf @ Weights64.w(model["lm_head"]).T

@@ -1,0 +1,197 @@
+"""ctypes binding of libaiq.so (declared in include/aiq.h).
+
+Argument marshalling only: the structs mirror the C declarations field by
+field and the functions keep their C names.  Every step of the query runs in
+the library's HIP kernels; this module never computes a result.  Loading
+fails loudly when the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libaiq.so")
+
+AIQ_OK, AIQ_EINVAL, AIQ_EUNSUPPORTED, AIQ_ENOSPC, AIQ_EHIP, AIQ_ENOMEM = 0, -1, -2, -3, -4, -5
+AIQ_I8, AIQ_I16, AIQ_I32, AIQ_F32, AIQ_BF16 = 1, 2, 3, 4, 5
+AIQ_LT, AIQ_LE, AIQ_GT, AIQ_GE, AIQ_EQ, AIQ_NE, AIQ_IN = range(7)
+AIQ_ACT_GELU_ERF, AIQ_ACT_SWIGLU = 1, 2
+AIQ_DECIDE_BINARY_GT, AIQ_DECIDE_ARGMAX = 1, 2
+AIQ_AGG_COUNT, AIQ_AGG_AVG_LABEL_COUNT_BY, AIQ_AGG_COUNT_BY_PAYLOAD = 1, 2, 3
+AIQ_LOGITS_LABELS, AIQ_LOGITS_FULL_VOCAB = 1, 2
+
+AIQ_DEV_TOKEN_RANGE, AIQ_DEV_DUP_KEY, AIQ_DEV_HASH_FULL, AIQ_DEV_IDS_CAP = 0x01, 0x02, 0x04, 0x08
+AIQ_DEV_GROUP_RANGE, AIQ_DEV_LIST_LEN, AIQ_DEV_GROUP_CAP = 0x10, 0x20, 0x40
+AIQ_S_SELECTED, AIQ_S_KEPT, AIQ_S_TOKENS, AIQ_S_STATUS, AIQ_S_GROUPS = range(5)
+AIQ_N_SCALARS = 8
+AIQ_MAX_PREDS, AIQ_MAX_IN_SET, AIQ_MAX_PREFIX, AIQ_MAX_LABELS = 8, 32, 64, 8
+
+(AIQ_K_REL, AIQ_K_PACK, AIQ_K_EMBED, AIQ_K_NORM, AIQ_K_GEMM_QKV, AIQ_K_ATTN, AIQ_K_GEMM_O,
+ AIQ_K_GEMM_UP, AIQ_K_GEMM_DOWN, AIQ_K_HEAD, AIQ_K_AGG) = range(11)
+
+OPS = {"lt": AIQ_LT, "le": AIQ_LE, "gt": AIQ_GT, "ge": AIQ_GE, "eq": AIQ_EQ, "ne": AIQ_NE, "in": AIQ_IN}
+
+
+class aiq_col(C.Structure):
+    _fields_ = [("data", C.c_void_p), ("dtype", C.c_int32)]
+
+
+class aiq_table(C.Structure):
+    _fields_ = [("n_rows", C.c_int64), ("n_cols", C.c_int32), ("cols", C.POINTER(aiq_col)),
+                ("list_offsets", C.c_void_p), ("list_tokens", C.c_void_p),
+                ("n_list_tokens", C.c_int64), ("max_list_len", C.c_int32)]
+
+
+class aiq_pred(C.Structure):
+    _fields_ = [("col", C.c_int32), ("op", C.c_int32), ("k", C.c_int64), ("n_set", C.c_int32),
+                ("set", C.c_int64 * AIQ_MAX_IN_SET)]
+
+
+class aiq_layer(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm",
+                                           "w_gate", "w_up", "w_down")]
+
+
+class aiq_model(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_heads", C.c_int32),
+                ("n_kv_heads", C.c_int32), ("d_ff", C.c_int32), ("vocab", C.c_int32),
+                ("act", C.c_int32), ("wdtype", C.c_int32), ("rope_theta", C.c_double),
+                ("norm_eps", C.c_double), ("emb", C.c_void_p), ("layers", C.POINTER(aiq_layer)),
+                ("final_norm", C.c_void_p), ("lm_head", C.c_void_p)]
+
+
+class aiq_query(C.Structure):
+    _fields_ = [("n_pred", C.c_int32), ("preds", aiq_pred * AIQ_MAX_PREDS),
+                ("join", C.c_int32), ("probe_key_col", C.c_int32), ("build_key_col", C.c_int32),
+                ("build_payload_col", C.c_int32), ("n_build_pred", C.c_int32),
+                ("build_preds", aiq_pred * AIQ_MAX_PREDS),
+                ("n_prefix", C.c_int32), ("prefix", C.c_int32 * AIQ_MAX_PREFIX),
+                ("n_labels", C.c_int32), ("label_ids", C.c_int32 * AIQ_MAX_LABELS),
+                ("decision", C.c_int32), ("agg", C.c_int32), ("group_col", C.c_int32),
+                ("n_group_keys", C.c_int32)]
+
+
+class aiq_plan_opts(C.Structure):
+    _fields_ = [("chunk_tokens", C.c_int64), ("n_layers_override", C.c_int32),
+                ("reserved", C.c_int32 * 5)]
+
+
+class aiq_out(C.Structure):
+    _fields_ = [("scalars", C.c_void_p), ("ids", C.c_void_p), ("ids_cap", C.c_int64),
+                ("sel_ids", C.c_void_p), ("sel_labels", C.c_void_p), ("sel_logits", C.c_void_p),
+                ("sel_cap", C.c_int64), ("grp_key", C.c_void_p), ("grp_count", C.c_void_p),
+                ("grp_sum", C.c_void_p), ("grp_avg", C.c_void_p), ("grp_cap", C.c_int64)]
+
+
+class aiq_trace(C.Structure):
+    _fields_ = [("events", C.POINTER(C.c_void_p)), ("tags", C.POINTER(C.c_int32)),
+                ("capacity", C.c_int32), ("count", C.c_int32), ("kind_mask", C.c_uint32)]
+
+
+EXPORTS = ("aiq_plan_create", "aiq_workspace_size", "aiq_run", "aiq_prefill_workspace_size",
+           "aiq_prefill_packed", "aiq_plan_destroy", "aiq_status_str", "aiq_abi_version")
+
+
+class AiqError(RuntimeError):
+    def __init__(self, fn: str, status: int, msg: str):
+        super().__init__(f"{fn} failed: {msg} ({status})")
+        self.status = status
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> C.CDLL:
+    """Loads libaiq.so; raises if it has not been built (no fallback exists)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2608_10139_amd.build`")
+    lib = C.CDLL(path)
+    P = C.c_void_p
+    lib.aiq_plan_create.argtypes = [C.POINTER(aiq_model), C.POINTER(aiq_table), C.POINTER(aiq_table),
+                                    C.POINTER(aiq_query), C.POINTER(aiq_plan_opts), C.POINTER(P)]
+    lib.aiq_plan_create.restype = C.c_int
+    lib.aiq_workspace_size.argtypes = [P, C.POINTER(C.c_size_t)]
+    lib.aiq_workspace_size.restype = C.c_int
+    lib.aiq_run.argtypes = [P, P, C.c_size_t, C.POINTER(aiq_out), C.POINTER(aiq_trace), P]
+    lib.aiq_run.restype = C.c_int
+    lib.aiq_prefill_workspace_size.argtypes = [P, C.c_int64, C.POINTER(C.c_size_t)]
+    lib.aiq_prefill_workspace_size.restype = C.c_int
+    lib.aiq_prefill_packed.argtypes = [P, P, P, C.c_int32, C.c_int64, C.c_int32, P, P, C.c_size_t, P]
+    lib.aiq_prefill_packed.restype = C.c_int
+    lib.aiq_plan_destroy.argtypes = [P]
+    lib.aiq_plan_destroy.restype = None
+    lib.aiq_status_str.argtypes = [C.c_int32]
+    lib.aiq_status_str.restype = C.c_char_p
+    lib.aiq_abi_version.argtypes = []
+    lib.aiq_abi_version.restype = C.c_int32
+    _lib = lib
+    return lib
+
+
+def check(fn: str, status: int) -> None:
+    if status != AIQ_OK:
+        raise AiqError(fn, status, load().aiq_status_str(status).decode())
+
+
+# ---------------------------------------------------------------- same-name wrappers
+
+def aiq_plan_create(model, probe, build, query, opts=None) -> C.c_void_p:
+    plan = C.c_void_p()
+    st = load().aiq_plan_create(C.byref(model), C.byref(probe) if probe is not None else None,
+                                C.byref(build) if build is not None else None,
+                                C.byref(query) if query is not None else None,
+                                C.byref(opts) if opts is not None else None, C.byref(plan))
+    check("aiq_plan_create", st)
+    return plan
+
+
+def aiq_plan_create_status(model, probe, build, query, opts=None) -> int:
+    """Like aiq_plan_create but returns the status (for error-path tests)."""
+    plan = C.c_void_p()
+    st = load().aiq_plan_create(C.byref(model) if model is not None else None,
+                                C.byref(probe) if probe is not None else None,
+                                C.byref(build) if build is not None else None,
+                                C.byref(query) if query is not None else None,
+                                C.byref(opts) if opts is not None else None, C.byref(plan))
+    if st == AIQ_OK:
+        load().aiq_plan_destroy(plan)
+    return st
+
+
+def aiq_workspace_size(plan) -> int:
+    n = C.c_size_t()
+    check("aiq_workspace_size", load().aiq_workspace_size(plan, C.byref(n)))
+    return n.value
+
+
+def aiq_prefill_workspace_size(plan, max_tokens: int) -> int:
+    n = C.c_size_t()
+    check("aiq_prefill_workspace_size", load().aiq_prefill_workspace_size(plan, max_tokens, C.byref(n)))
+    return n.value
+
+
+def aiq_run(plan, ws_ptr: int, ws_bytes: int, out: aiq_out, trace=None, stream: int = 0) -> None:
+    check("aiq_run", load().aiq_run(plan, ws_ptr, ws_bytes, C.byref(out),
+                                    C.byref(trace) if trace is not None else None, stream))
+
+
+def aiq_prefill_packed(plan, tok_ptr: int, cu_ptr: int, n_seq: int, n_tok: int, mode: int,
+                       logits_ptr: int, ws_ptr: int, ws_bytes: int, stream: int = 0) -> None:
+    check("aiq_prefill_packed", load().aiq_prefill_packed(plan, tok_ptr, cu_ptr, n_seq, n_tok, mode,
+                                                          logits_ptr, ws_ptr, ws_bytes, stream))
+
+
+def aiq_plan_destroy(plan) -> None:
+    load().aiq_plan_destroy(plan)
+
+
+def aiq_abi_version() -> int:
+    return load().aiq_abi_version()
+
+
+def aiq_status_str(st: int) -> str:
+    return load().aiq_status_str(st).decode()

@@ -1,0 +1,629 @@
+// Host side of the C ABI: validation, plan construction, workspace carving and
+// the single-stream enqueue of the whole AI query.
+//
+// The sequence of launches is fixed on the host; every data-dependent extent
+// (selected rows, tokens, sequences per chunk) is produced and consumed on the
+// device.  The host loops over an upper bound of chunks computed from sizes it
+// knows (table rows and list tokens); kernels of a chunk with no work exit at
+// once.  Nothing is copied between host and device and nothing synchronises.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "aiq_internal.h"
+
+using namespace aiq;
+
+struct aiq_plan {
+  aiq_model model;
+  std::vector<aiq_layer> layers;
+  bool has_probe = false, has_build = false, has_query = false;
+  aiq_table probe{}, build{};
+  std::vector<aiq_col> probe_cols, build_cols;
+  aiq_query q{};
+  int n_layers = 0;
+  // derived model shapes
+  int hd = 0, d_q = 0, d_kv = 0, n_qkv = 0, n_up = 0;
+  bool bf16 = false;
+  // derived run shapes
+  int64_t n_rows = 0, t_ub = 0, chunk_tokens = 0, n_chunks = 0, t_cap = 0, seq_ub = 0;
+  int32_t max_seq = 0;
+  int hash_log2 = 0;
+  DPredList probe_preds{}, build_preds{};
+  Prefix prefix{};
+};
+
+namespace {
+
+constexpr size_t ALIGN = 256;
+
+struct Carver {
+  size_t off = 0;
+  size_t take(size_t bytes) {
+    const size_t o = off;
+    off += (bytes + ALIGN - 1) / ALIGN * ALIGN;
+    return o;
+  }
+};
+
+bool int_dtype(int dt) { return dt == AIQ_I8 || dt == AIQ_I16 || dt == AIQ_I32; }
+
+int64_t dtype_min(int dt) { return dt == AIQ_I8 ? INT8_MIN : dt == AIQ_I16 ? INT16_MIN : INT32_MIN; }
+int64_t dtype_max(int dt) { return dt == AIQ_I8 ? INT8_MAX : dt == AIQ_I16 ? INT16_MAX : INT32_MAX; }
+
+aiq_status make_preds(const aiq_pred* src, int n, const std::vector<aiq_col>& cols, DPredList* out) {
+  if (n < 0 || n > AIQ_MAX_PREDS) return AIQ_EINVAL;
+  out->n = n;
+  for (int i = 0; i < n; ++i) {
+    const aiq_pred& p = src[i];
+    if (p.col < 0 || p.col >= static_cast<int>(cols.size())) return AIQ_EINVAL;
+    const aiq_col& c = cols[p.col];
+    if (!int_dtype(c.dtype)) return AIQ_EUNSUPPORTED;
+    if (p.op < AIQ_LT || p.op > AIQ_IN) return AIQ_EINVAL;
+    DPred& d = out->p[i];
+    d.data = c.data;
+    d.dtype = c.dtype;
+    d.op = p.op;
+    d.k = p.k;
+    d.n_set = 0;
+    if (p.op == AIQ_IN) {
+      if (p.n_set < 0 || p.n_set > AIQ_MAX_IN_SET) return AIQ_EINVAL;
+      // values the column type cannot hold never match; drop them
+      for (int j = 0; j < p.n_set; ++j)
+        if (p.set[j] >= dtype_min(c.dtype) && p.set[j] <= dtype_max(c.dtype))
+          d.set[d.n_set++] = static_cast<int32_t>(p.set[j]);
+    }
+  }
+  return AIQ_OK;
+}
+
+aiq_status copy_table(const aiq_table* t, aiq_table* dst, std::vector<aiq_col>* cols, bool need_list) {
+  if (t->n_rows < 0 || t->n_rows > INT32_MAX) return AIQ_EINVAL;
+  if (t->n_cols < 0 || (t->n_cols > 0 && !t->cols)) return AIQ_EINVAL;
+  cols->assign(t->cols, t->cols + t->n_cols);
+  for (const aiq_col& c : *cols) {
+    if (!int_dtype(c.dtype) && c.dtype != AIQ_F32) return AIQ_EINVAL;
+    if (!c.data && t->n_rows > 0) return AIQ_EINVAL;
+  }
+  if (need_list) {
+    if (!t->list_offsets || !t->list_tokens) return AIQ_EINVAL;
+    if (t->n_list_tokens < 0 || t->max_list_len < 1) return AIQ_EINVAL;
+  }
+  *dst = *t;
+  dst->cols = cols->data();
+  return AIQ_OK;
+}
+
+aiq_status validate_model(const aiq_model* m) {
+  if (m->n_layers < 0 || m->d_model <= 0 || m->n_heads <= 0 || m->n_kv_heads <= 0 || m->d_ff <= 0 ||
+      m->vocab <= 0)
+    return AIQ_EINVAL;
+  if (m->d_model % m->n_heads) return AIQ_EINVAL;
+  if (m->n_heads % m->n_kv_heads) return AIQ_EINVAL;
+  const int hd = m->d_model / m->n_heads;
+  if (hd != 32 && hd != 64 && hd != 128) return AIQ_EINVAL;
+  if (m->wdtype != AIQ_F32 && m->wdtype != AIQ_BF16) return AIQ_EINVAL;
+  if (m->act != AIQ_ACT_GELU_ERF && m->act != AIQ_ACT_SWIGLU) return AIQ_EINVAL;
+  if (!(m->norm_eps > 0.0) || !(m->rope_theta > 0.0)) return AIQ_EINVAL;
+  if (!m->emb || !m->final_norm || !m->lm_head || (m->n_layers > 0 && !m->layers)) return AIQ_EINVAL;
+  for (int l = 0; l < m->n_layers; ++l) {
+    const aiq_layer& L = m->layers[l];
+    if (!L.attn_norm || !L.wq || !L.wk || !L.wv || !L.wo || !L.ffn_norm || !L.w_gate || !L.w_down)
+      return AIQ_EINVAL;
+    if (m->act == AIQ_ACT_SWIGLU && !L.w_up) return AIQ_EINVAL;
+  }
+  const int d = m->d_model, d_q = m->n_heads * hd, d_kv = m->n_kv_heads * hd;
+  if (m->wdtype == AIQ_BF16) {
+    // MFMA path: 256-wide output tiles, 64-deep K steps, rotary pairs in registers
+    if (m->act != AIQ_ACT_SWIGLU) return AIQ_EUNSUPPORTED;
+    if (hd == 32) return AIQ_EUNSUPPORTED;
+    if ((d_q + 2 * d_kv) % 256 || d % 256 || (2 * m->d_ff) % 256) return AIQ_EUNSUPPORTED;
+    if (d % 64 || d_q % 64 || m->d_ff % 64) return AIQ_EUNSUPPORTED;
+  } else {
+    if (m->act != AIQ_ACT_GELU_ERF) return AIQ_EUNSUPPORTED;
+    if (hd == 128) return AIQ_EUNSUPPORTED;
+    if ((d_q + 2 * d_kv) % 64 || d % 64 || m->d_ff % 64 || d % 16 || d_q % 16 || m->d_ff % 16)
+      return AIQ_EUNSUPPORTED;
+  }
+  return AIQ_OK;
+}
+
+struct Layout {
+  size_t ctr, mask, blk_cnt, blk_off, sel, payload, lens, label, logits, cu, scan_tmp, packed, hkeys, hvals,
+      bins, desc, rcos, rsin, x, h, qkv, att, ffn, pos, hf, total;
+};
+
+size_t act_bytes(const aiq_plan* p) { return p->bf16 ? 2 : 4; }
+
+Layout run_layout(const aiq_plan* p) {
+  Layout L{};
+  Carver c;
+  const int64_t n = p->n_rows;
+  const int64_t nb = (n + REL_ROWS_PER_BLOCK - 1) / REL_ROWS_PER_BLOCK + 1;
+  const int d = p->model.d_model;
+  const size_t ab = act_bytes(p);
+  L.ctr = c.take(C_COUNT * 8);
+  L.mask = c.take(static_cast<size_t>(nb) * REL_WORDS_PER_BLOCK * 8);
+  L.blk_cnt = c.take(static_cast<size_t>(nb) * 4);
+  L.blk_off = c.take(static_cast<size_t>(nb + 1) * 8);
+  L.sel = c.take(static_cast<size_t>(n + 1) * 4);
+  L.payload = c.take(static_cast<size_t>(n + 1) * 4);
+  L.lens = c.take(static_cast<size_t>(n + 1) * 4);
+  L.label = c.take(static_cast<size_t>(n + 1) * 4);
+  L.logits = c.take(static_cast<size_t>(n + 1) * p->q.n_labels * 4);
+  L.cu = c.take(static_cast<size_t>(n + 1) * 8);
+  L.scan_tmp = c.take(static_cast<size_t>(n / 4096 + 2) * 8);
+  L.packed = c.take(static_cast<size_t>(p->t_ub + 1) * 4);
+  const size_t hcap = p->hash_log2 ? (size_t(1) << p->hash_log2) : 1;
+  L.hkeys = c.take(hcap * 4);
+  L.hvals = c.take(hcap * 4);
+  L.bins = c.take(static_cast<size_t>(std::max(p->q.n_group_keys, 1)) * 16);
+  L.desc = c.take(static_cast<size_t>(p->n_chunks) * D_STRIDE * 8);
+  L.rcos = c.take(static_cast<size_t>(p->max_seq) * (p->hd / 2) * 4);
+  L.rsin = c.take(static_cast<size_t>(p->max_seq) * (p->hd / 2) * 4);
+  const size_t T = static_cast<size_t>(p->t_cap);
+  L.x = c.take(T * d * 4);
+  L.h = c.take(T * d * ab);
+  L.qkv = c.take(T * p->n_qkv * ab);
+  L.att = c.take(T * p->d_q * ab);
+  L.ffn = c.take(T * p->model.d_ff * ab);
+  L.pos = c.take(T * 4);
+  L.hf = 0;
+  L.total = c.off;
+  return L;
+}
+
+// prefill-only layout for up to max_tokens tokens (and as many sequences)
+Layout prefill_layout(const aiq_plan* p, int64_t max_tokens) {
+  Layout L{};
+  Carver c;
+  const int d = p->model.d_model;
+  const size_t ab = act_bytes(p);
+  const size_t T = static_cast<size_t>(max_tokens);
+  L.ctr = c.take(C_COUNT * 8);
+  L.desc = c.take(D_STRIDE * 8);
+  L.cu = c.take((T + 1) * 8);
+  L.label = c.take((T + 1) * 4);
+  L.rcos = c.take(T * (p->hd / 2) * 4);
+  L.rsin = c.take(T * (p->hd / 2) * 4);
+  L.x = c.take(T * d * 4);
+  L.h = c.take(T * d * ab);
+  L.qkv = c.take(T * p->n_qkv * ab);
+  L.att = c.take(T * p->d_q * ab);
+  L.ffn = c.take(T * p->model.d_ff * ab);
+  L.pos = c.take(T * 4);
+  L.hf = c.take(T * d * ab);
+  L.total = c.off;
+  return L;
+}
+
+template <typename T>
+T* at(void* ws, size_t off) {
+  return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+struct Tracer {
+  aiq_trace* t;
+  hipStream_t s;
+  bool open = false;
+  int kind = 0;
+  void begin(int k) {
+    open = false;
+    if (!t || !t->events || !t->tags || t->count >= t->capacity || !((t->kind_mask >> k) & 1u)) return;
+    if (hipEventRecord(static_cast<hipEvent_t>(t->events[2 * t->count]), s) != hipSuccess) return;
+    open = true;
+    kind = k;
+  }
+  void end() {
+    if (!open) return;
+    if (hipEventRecord(static_cast<hipEvent_t>(t->events[2 * t->count + 1]), s) == hipSuccess) {
+      t->tags[t->count] = kind;
+      t->count += 1;
+    }
+    open = false;
+  }
+};
+
+#define HIP_TRY(expr)                         \
+  do {                                        \
+    if ((expr) != hipSuccess) return AIQ_EHIP; \
+  } while (0)
+
+#define TRACED(tr, kind, expr) \
+  do {                         \
+    (tr).begin(kind);          \
+    HIP_TRY(expr);             \
+    (tr).end();                \
+  } while (0)
+
+// Enqueues embedding, the layer stack and the label head for one chunk.
+aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int64_t* desc, const int64_t* cu,
+                         int64_t* ctr, const int32_t* packed, int64_t t_cap, int64_t seq_ub, int32_t* label_out,
+                         float* logits_out, void* hf_out, Tracer& tr, hipStream_t s) {
+  const aiq_model& m = p->model;
+  const int d = m.d_model;
+  const int64_t* m_ptr = desc + D_NTOK;
+  float* x = at<float>(ws, L.x);
+  void* h = at<void>(ws, L.h);
+  void* qkv = at<void>(ws, L.qkv);
+  void* att = at<void>(ws, L.att);
+  void* ffn = at<void>(ws, L.ffn);
+  int32_t* pos = at<int32_t>(ws, L.pos);
+  const float* rcos = at<float>(ws, L.rcos);
+  const float* rsin = at<float>(ws, L.rsin);
+  const float eps = static_cast<float>(m.norm_eps);
+  auto gemm = [&](int epi, const void* A, int64_t lda, int N, int K, const void* B0, const void* B1, const void* B2,
+                  void* C, int64_t ldc) {
+    GemmArgs g{};
+    g.A = A;
+    g.lda = lda;
+    g.m_ptr = m_ptr;
+    g.m_ub = t_cap;
+    g.N = N;
+    g.K = K;
+    g.B0 = B0;
+    g.B1 = B1;
+    g.B2 = B2;
+    g.n_q = p->d_q;
+    g.n_kv = p->d_kv;
+    g.hd = p->hd;
+    g.C = C;
+    g.ldc = ldc;
+    g.X = x;
+    g.ldx = d;
+    g.pos = pos;
+    g.rope_cos = rcos;
+    g.rope_sin = rsin;
+    return p->bf16 ? launch_gemm_bf16(epi, g, s) : launch_gemm_f32(epi, g, s);
+  };
+
+  TRACED(tr, AIQ_K_EMBED, launch_embed(desc, cu, packed, m.emb, m.wdtype, d, m.vocab, x, pos, ctr, t_cap, s));
+  for (int l = 0; l < p->n_layers; ++l) {
+    const aiq_layer& W = p->layers[l];
+    TRACED(tr, AIQ_K_NORM, launch_rmsnorm(desc, x, W.attn_norm, d, eps, h, p->bf16, t_cap, s));
+    TRACED(tr, AIQ_K_GEMM_QKV, gemm(EPI_QKV_ROPE, h, d, p->n_qkv, d, W.wq, W.wk, W.wv, qkv, p->n_qkv));
+    if (!p->bf16)
+      TRACED(tr, AIQ_K_GEMM_QKV, launch_rope_f32(desc, static_cast<float*>(qkv), p->n_qkv, p->d_q, p->d_kv, p->hd,
+                                                 pos, rcos, rsin, t_cap, s));
+    AttnArgs aa{};
+    aa.qkv = qkv;
+    aa.ld = p->n_qkv;
+    aa.out = att;
+    aa.ldo = p->d_q;
+    aa.desc = desc;
+    aa.cu = cu;
+    aa.n_heads = m.n_heads;
+    aa.n_kv = m.n_kv_heads;
+    aa.hd = p->hd;
+    aa.seq_ub = seq_ub;
+    TRACED(tr, AIQ_K_ATTN, p->bf16 ? launch_attention_bf16(aa, s) : launch_attention_f32(aa, s));
+    TRACED(tr, AIQ_K_GEMM_O, gemm(EPI_RESID, att, p->d_q, d, p->d_q, W.wo, nullptr, nullptr, nullptr, 0));
+    TRACED(tr, AIQ_K_NORM, launch_rmsnorm(desc, x, W.ffn_norm, d, eps, h, p->bf16, t_cap, s));
+    if (p->bf16)
+      TRACED(tr, AIQ_K_GEMM_UP, gemm(EPI_SWIGLU, h, d, 2 * m.d_ff, d, W.w_gate, W.w_up, nullptr, ffn, m.d_ff));
+    else
+      TRACED(tr, AIQ_K_GEMM_UP, gemm(EPI_GELU, h, d, m.d_ff, d, W.w_gate, nullptr, nullptr, ffn, m.d_ff));
+    TRACED(tr, AIQ_K_GEMM_DOWN, gemm(EPI_RESID, ffn, m.d_ff, d, m.d_ff, W.w_down, nullptr, nullptr, nullptr, 0));
+  }
+  HeadArgs ha{};
+  ha.desc = desc;
+  ha.cu = cu;
+  ha.x = x;
+  ha.g = m.final_norm;
+  ha.eps = eps;
+  ha.d = d;
+  ha.lm_head = m.lm_head;
+  ha.wdtype = m.wdtype;
+  ha.n_labels = p->has_query ? p->q.n_labels : 0;
+  for (int k = 0; k < ha.n_labels; ++k) ha.labels[k] = p->q.label_ids[k];
+  ha.decision = p->has_query ? p->q.decision : AIQ_DECIDE_BINARY_GT;
+  ha.label_out = ha.n_labels >= 2 ? label_out : nullptr;
+  ha.logits_out = ha.n_labels >= 2 ? logits_out : nullptr;
+  ha.hf_out = hf_out;
+  ha.hf_bf16 = p->bf16;
+  ha.seq_ub = seq_ub;
+  TRACED(tr, AIQ_K_HEAD, launch_head(ha, s));
+  return AIQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t aiq_abi_version(void) { return AIQ_ABI_VERSION; }
+
+const char* aiq_status_str(int32_t st) {
+  switch (st) {
+    case AIQ_OK: return "ok";
+    case AIQ_EINVAL: return "invalid argument";
+    case AIQ_EUNSUPPORTED: return "unsupported";
+    case AIQ_ENOSPC: return "workspace or capacity too small";
+    case AIQ_EHIP: return "HIP runtime error";
+    case AIQ_ENOMEM: return "host out of memory";
+    default: return "unknown status";
+  }
+}
+
+aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const aiq_table* build,
+                           const aiq_query* query, const aiq_plan_opts* opts, aiq_plan** out) {
+  if (!out) return AIQ_EINVAL;
+  *out = nullptr;
+  if (!model) return AIQ_EINVAL;
+  aiq_status st = validate_model(model);
+  if (st != AIQ_OK) return st;
+  aiq_plan* p = new (std::nothrow) aiq_plan();
+  if (!p) return AIQ_ENOMEM;
+  auto fail = [&](aiq_status e) {
+    delete p;
+    return e;
+  };
+  p->model = *model;
+  p->layers.assign(model->layers, model->layers + model->n_layers);
+  p->model.layers = p->layers.data();
+  p->n_layers = model->n_layers;
+  if (opts && opts->n_layers_override > 0) p->n_layers = std::min(opts->n_layers_override, model->n_layers);
+  if (opts && opts->n_layers_override < 0) p->n_layers = 0;
+  p->hd = model->d_model / model->n_heads;
+  p->d_q = model->n_heads * p->hd;
+  p->d_kv = model->n_kv_heads * p->hd;
+  p->n_qkv = p->d_q + 2 * p->d_kv;
+  p->bf16 = model->wdtype == AIQ_BF16;
+  p->n_up = p->bf16 ? 2 * model->d_ff : model->d_ff;
+
+  if (query) {
+    p->has_query = true;
+    p->q = *query;
+    const aiq_query& q = p->q;
+    if (q.n_labels < 2 || q.n_labels > AIQ_MAX_LABELS) return fail(AIQ_EINVAL);
+    for (int k = 0; k < q.n_labels; ++k)
+      if (q.label_ids[k] < 0 || q.label_ids[k] >= model->vocab) return fail(AIQ_EINVAL);
+    if (q.decision != AIQ_DECIDE_BINARY_GT && q.decision != AIQ_DECIDE_ARGMAX) return fail(AIQ_EINVAL);
+    if (q.n_prefix < 0 || q.n_prefix > AIQ_MAX_PREFIX) return fail(AIQ_EINVAL);
+    for (int k = 0; k < q.n_prefix; ++k)
+      if (q.prefix[k] < 0 || q.prefix[k] >= model->vocab) return fail(AIQ_EINVAL);
+  }
+  if (probe) {
+    if (!query) return fail(AIQ_EINVAL);
+    p->has_probe = true;
+    st = copy_table(probe, &p->probe, &p->probe_cols, true);
+    if (st != AIQ_OK) return fail(st);
+    const aiq_query& q = p->q;
+    st = make_preds(q.preds, q.n_pred, p->probe_cols, &p->probe_preds);
+    if (st != AIQ_OK) return fail(st);
+    if (q.join != 0 && q.join != 1) return fail(AIQ_EINVAL);
+    if ((q.join == 1) != (build != nullptr)) return fail(AIQ_EINVAL);
+    if (q.join) {
+      p->has_build = true;
+      st = copy_table(build, &p->build, &p->build_cols, false);
+      if (st != AIQ_OK) return fail(st);
+      const int nc = static_cast<int>(p->build_cols.size());
+      if (q.build_key_col < 0 || q.build_key_col >= nc || q.build_payload_col < 0 || q.build_payload_col >= nc)
+        return fail(AIQ_EINVAL);
+      if (q.probe_key_col < 0 || q.probe_key_col >= static_cast<int>(p->probe_cols.size())) return fail(AIQ_EINVAL);
+      if (!int_dtype(p->build_cols[q.build_key_col].dtype) || !int_dtype(p->build_cols[q.build_payload_col].dtype) ||
+          !int_dtype(p->probe_cols[q.probe_key_col].dtype))
+        return fail(AIQ_EUNSUPPORTED);
+      st = make_preds(q.build_preds, q.n_build_pred, p->build_cols, &p->build_preds);
+      if (st != AIQ_OK) return fail(st);
+      int lg = 6;
+      while ((int64_t(1) << lg) < 2 * std::max<int64_t>(p->build.n_rows, 1)) ++lg;
+      if (lg > 30) return fail(AIQ_EUNSUPPORTED);
+      p->hash_log2 = lg;
+    }
+    switch (q.agg) {
+      case AIQ_AGG_COUNT: break;
+      case AIQ_AGG_AVG_LABEL_COUNT_BY:
+        if (q.group_col < 0 || q.group_col >= static_cast<int>(p->probe_cols.size())) return fail(AIQ_EINVAL);
+        if (!int_dtype(p->probe_cols[q.group_col].dtype)) return fail(AIQ_EUNSUPPORTED);
+        if (q.n_group_keys <= 0) return fail(AIQ_EINVAL);
+        break;
+      case AIQ_AGG_COUNT_BY_PAYLOAD:
+        if (!q.join || q.n_group_keys <= 0) return fail(AIQ_EINVAL);
+        break;
+      default: return fail(AIQ_EINVAL);
+    }
+    p->n_rows = p->probe.n_rows;
+    p->t_ub = p->probe.n_list_tokens + p->n_rows * q.n_prefix;
+    p->max_seq = p->probe.max_list_len + q.n_prefix;
+    // default chunk: about 48 GB of per-token activations (a fraction of one
+    // MI355X's 288 GB), at most 4M tokens
+    const int64_t per_tok = static_cast<int64_t>(model->d_model) * 4 +
+                            static_cast<int64_t>(model->d_model + p->n_qkv + p->d_q + model->d_ff) *
+                                (p->bf16 ? 2 : 4) + 4;
+    const int64_t def_chunk = std::min<int64_t>((int64_t(48) << 30) / per_tok, int64_t(4) << 20);
+    int64_t ct = (opts && opts->chunk_tokens > 0) ? opts->chunk_tokens : def_chunk;
+    ct = std::max<int64_t>(ct, p->max_seq);
+    ct = std::min<int64_t>(ct, std::max<int64_t>(p->t_ub, p->max_seq));
+    p->chunk_tokens = ct;
+    p->n_chunks = std::max<int64_t>((p->t_ub + ct - 1) / ct, 1);
+    p->t_cap = ct + p->max_seq;
+    p->seq_ub = std::min<int64_t>(p->n_rows, p->t_cap);
+    p->prefix.n = q.n_prefix;
+    for (int k = 0; k < q.n_prefix; ++k) p->prefix.tok[k] = q.prefix[k];
+  }
+  *out = p;
+  return AIQ_OK;
+}
+
+void aiq_plan_destroy(aiq_plan* plan) { delete plan; }
+
+aiq_status aiq_workspace_size(const aiq_plan* plan, size_t* bytes) {
+  if (!plan || !bytes) return AIQ_EINVAL;
+  if (!plan->has_probe) return AIQ_EINVAL;
+  *bytes = run_layout(plan).total;
+  return AIQ_OK;
+}
+
+aiq_status aiq_prefill_workspace_size(const aiq_plan* plan, int64_t max_tokens, size_t* bytes) {
+  if (!plan || !bytes || max_tokens <= 0) return AIQ_EINVAL;
+  *bytes = prefill_layout(plan, max_tokens).total;
+  return AIQ_OK;
+}
+
+aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* out, aiq_trace* trace,
+                   void* stream) {
+  if (!p || !out || !out->scalars || !ws) return AIQ_EINVAL;
+  if (!p->has_probe) return AIQ_EINVAL;
+  if (out->ids_cap < 0 || (out->ids_cap > 0 && !out->ids)) return AIQ_EINVAL;
+  const aiq_query& q = p->q;
+  if (q.agg != AIQ_AGG_COUNT &&
+      (!out->grp_key || !out->grp_count || !out->grp_sum || !out->grp_avg || out->grp_cap <= 0))
+    return AIQ_EINVAL;
+  if (out->sel_cap < 0) return AIQ_EINVAL;
+  const Layout L = run_layout(p);
+  if (ws_bytes < L.total) return AIQ_ENOSPC;
+  if (reinterpret_cast<uintptr_t>(ws) % ALIGN) return AIQ_EINVAL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Tracer tr{trace, s};
+
+  int64_t* ctr = at<int64_t>(ws, L.ctr);
+  uint64_t* mask = at<uint64_t>(ws, L.mask);
+  int32_t* blk_cnt = at<int32_t>(ws, L.blk_cnt);
+  int64_t* blk_off = at<int64_t>(ws, L.blk_off);
+  int32_t* sel = at<int32_t>(ws, L.sel);
+  int32_t* payload = at<int32_t>(ws, L.payload);
+  int32_t* lens = at<int32_t>(ws, L.lens);
+  int32_t* label = at<int32_t>(ws, L.label);
+  float* logits = at<float>(ws, L.logits);
+  int64_t* cu = at<int64_t>(ws, L.cu);
+  int64_t* scan_tmp = at<int64_t>(ws, L.scan_tmp);
+  int32_t* packed = at<int32_t>(ws, L.packed);
+  int64_t* desc = at<int64_t>(ws, L.desc);
+  const int64_t n = p->n_rows;
+
+  HashArgs h{};
+  if (p->has_build) {
+    h.keys = at<int32_t>(ws, L.hkeys);
+    h.vals = at<int32_t>(ws, L.hvals);
+    h.cap_log2 = p->hash_log2;
+  }
+  const void* pkey = p->has_build ? p->probe_cols[q.probe_key_col].data : nullptr;
+  const int32_t pkey_dt = p->has_build ? p->probe_cols[q.probe_key_col].dtype : AIQ_I32;
+
+  HIP_TRY(launch_fill_i64(ctr, C_COUNT, 0, s));
+  // ---- relational: WHERE (+ join) -> ascending survivor ids
+  tr.begin(AIQ_K_REL);
+  if (p->has_build) {
+    HIP_TRY(launch_fill_i32(h.keys, int64_t(1) << p->hash_log2, HASH_EMPTY, s));
+    const aiq_col& kc = p->build_cols[q.build_key_col];
+    const aiq_col& pc = p->build_cols[q.build_payload_col];
+    HIP_TRY(launch_hash_build(p->build_preds, kc.data, kc.dtype, pc.data, pc.dtype, p->build.n_rows, h, ctr, s));
+  }
+  HIP_TRY(launch_row_mask(p->probe_preds, n, pkey, pkey_dt, h, p->has_build, mask, blk_cnt, s));
+  HIP_TRY(launch_scan_blocks(blk_cnt, nullptr, n, blk_off, ctr + C_SEL, s));
+  HIP_TRY(launch_scatter_rows(mask, blk_off, nullptr, n, nullptr, sel, n, pkey, pkey_dt, h, p->has_build,
+                              payload, ctr, s));
+  tr.end();
+  // ---- pack: lengths, offsets, tokens, chunk descriptors
+  tr.begin(AIQ_K_PACK);
+  HIP_TRY(launch_seq_lengths(sel, ctr + C_SEL, n, p->probe.list_offsets, p->probe.max_list_len, q.n_prefix, lens,
+                             ctr, s));
+  HIP_TRY(launch_scan_lengths(lens, ctr + C_SEL, n, scan_tmp, cu, ctr + C_TOK, s));
+  HIP_TRY(launch_gather_tokens(sel, ctr + C_SEL, n, p->probe.list_offsets, p->probe.list_tokens, cu, p->prefix,
+                               p->model.vocab, p->t_ub, packed, ctr, s));
+  HIP_TRY(launch_chunk_desc(cu, ctr + C_SEL, p->chunk_tokens, p->n_chunks, p->t_ub, desc, s));
+  HIP_TRY(launch_rope_table(p->max_seq, p->hd / 2, p->model.rope_theta, p->hd, at<float>(ws, L.rcos),
+                            at<float>(ws, L.rsin), s));
+  tr.end();
+  // ---- prefill + label head, chunk by chunk
+  for (int64_t c = 0; c < p->n_chunks; ++c) {
+    const aiq_status e = enqueue_chunk(p, ws, L, desc + c * D_STRIDE, cu, ctr, packed, p->t_cap, p->seq_ub, label,
+                                       logits, nullptr, tr, s);
+    if (e != AIQ_OK) return e;
+  }
+  // ---- decision -> kept ids, aggregates
+  tr.begin(AIQ_K_AGG);
+  if (q.decision == AIQ_DECIDE_BINARY_GT) {
+    HIP_TRY(launch_label_mask(label, ctr + C_SEL, n, mask, blk_cnt, s));
+    HIP_TRY(launch_scan_blocks(blk_cnt, ctr + C_SEL, n, blk_off, ctr + C_KEPT, s));
+    HIP_TRY(launch_scatter_rows(mask, blk_off, ctr + C_SEL, n, sel, out->ids, out->ids_cap, nullptr, AIQ_I32, h, 0,
+                                nullptr, ctr, s));
+  } else {
+    HIP_TRY(launch_copy_ids(sel, ctr + C_SEL, n, out->ids, out->ids_cap, ctr, 1, s));
+  }
+  if (q.agg != AIQ_AGG_COUNT) {
+    int64_t* bins = at<int64_t>(ws, L.bins);
+    HIP_TRY(launch_fill_i64(bins, 2 * int64_t(q.n_group_keys), 0, s));
+    const int mode = q.agg == AIQ_AGG_AVG_LABEL_COUNT_BY ? 1 : 2;
+    const void* kcol = mode == 1 ? p->probe_cols[q.group_col].data : nullptr;
+    const int32_t kdt = mode == 1 ? p->probe_cols[q.group_col].dtype : AIQ_I32;
+    HIP_TRY(launch_group_accumulate(sel, label, payload, nullptr, ctr + C_SEL, n, kcol, kdt, mode, q.n_group_keys,
+                                    bins, ctr, s));
+    HIP_TRY(launch_group_emit(bins, q.n_group_keys, out->grp_key, out->grp_count, out->grp_sum, out->grp_avg,
+                              out->grp_cap, mode, ctr, s));
+  }
+  if (out->sel_cap > 0) {
+    if (out->sel_ids) HIP_TRY(launch_copy_ids(sel, ctr + C_SEL, n, out->sel_ids, out->sel_cap, ctr, 0, s));
+    if (out->sel_labels) HIP_TRY(launch_copy_ids(label, ctr + C_SEL, n, out->sel_labels, out->sel_cap, ctr, 0, s));
+    if (out->sel_logits)
+      HIP_TRY(launch_copy_f32(logits, ctr + C_SEL, n, q.n_labels, out->sel_logits, out->sel_cap, s));
+  }
+  HIP_TRY(launch_finalize(ctr, out->scalars, s));
+  tr.end();
+  return AIQ_OK;
+}
+
+aiq_status aiq_prefill_packed(const aiq_plan* p, const int32_t* tok, const int32_t* cu_seqlens, int32_t n_seq,
+                              int64_t n_tok, int32_t logits_mode, float* logits, void* ws, size_t ws_bytes,
+                              void* stream) {
+  if (!p || !tok || !cu_seqlens || !logits || !ws) return AIQ_EINVAL;
+  if (n_seq <= 0 || n_tok < n_seq) return AIQ_EINVAL;
+  if (logits_mode != AIQ_LOGITS_LABELS && logits_mode != AIQ_LOGITS_FULL_VOCAB) return AIQ_EINVAL;
+  if (logits_mode == AIQ_LOGITS_LABELS && !p->has_query) return AIQ_EINVAL;
+  if (logits_mode == AIQ_LOGITS_FULL_VOCAB && p->model.vocab % (p->bf16 ? 256 : 64)) return AIQ_EUNSUPPORTED;
+  if (reinterpret_cast<uintptr_t>(ws) % ALIGN) return AIQ_EINVAL;
+  // the workspace must have been sized for at least n_tok tokens
+  int64_t cap = n_tok;
+  Layout L = prefill_layout(p, cap);
+  if (ws_bytes < L.total) return AIQ_ENOSPC;
+  // use the largest token capacity the workspace holds so layouts agree between calls
+  {
+    int64_t lo = n_tok, hi = n_tok;
+    while (prefill_layout(p, hi * 2).total <= ws_bytes && hi < (int64_t(1) << 40)) hi *= 2;
+    if (hi != n_tok) {
+      lo = hi;
+      hi = hi * 2;
+      while (hi - lo > 1) {
+        const int64_t mid = lo + (hi - lo) / 2;
+        if (prefill_layout(p, mid).total <= ws_bytes) lo = mid;
+        else hi = mid;
+      }
+      cap = lo;
+    }
+    L = prefill_layout(p, cap);
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Tracer tr{nullptr, s};
+  int64_t* ctr = at<int64_t>(ws, L.ctr);
+  int64_t* desc = at<int64_t>(ws, L.desc);
+  int64_t* cu = at<int64_t>(ws, L.cu);
+  HIP_TRY(launch_fill_i64(ctr, C_COUNT, 0, s));
+  HIP_TRY(launch_packed_desc(cu_seqlens, n_seq, n_tok, cu, desc, ctr, s));
+  HIP_TRY(launch_rope_table(static_cast<int32_t>(std::min<int64_t>(cap, INT32_MAX)), p->hd / 2, p->model.rope_theta,
+                            p->hd, at<float>(ws, L.rcos), at<float>(ws, L.rsin), s));
+  const bool full = logits_mode == AIQ_LOGITS_FULL_VOCAB;
+  void* hf = full ? at<void>(ws, L.hf) : nullptr;
+  int32_t* label = at<int32_t>(ws, L.label);
+  const aiq_status e = enqueue_chunk(p, ws, L, desc, cu, ctr, tok, n_tok, n_seq, full ? nullptr : label,
+                                     full ? nullptr : logits, hf, tr, s);
+  if (e != AIQ_OK) return e;
+  if (full) {
+    GemmArgs g{};
+    g.A = hf;
+    g.lda = p->model.d_model;
+    g.m_ptr = ctr + C_NSEQ;
+    g.m_ub = n_seq;
+    g.N = p->model.vocab;
+    g.K = p->model.d_model;
+    g.B0 = p->model.lm_head;
+    g.C = logits;
+    g.ldc = p->model.vocab;
+    HIP_TRY(p->bf16 ? launch_gemm_bf16(EPI_STORE_F32, g, s) : launch_gemm_f32(EPI_STORE_F32, g, s));
+  }
+  return AIQ_OK;
+}
+
+}  // extern "C"

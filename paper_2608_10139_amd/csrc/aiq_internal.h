@@ -1,0 +1,180 @@
+// Internal declarations shared by the HIP kernel files and the host orchestrator.
+// Not part of the public ABI.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/aiq.h"
+
+namespace aiq {
+
+// ---------------------------------------------------------------- device counters
+// int64 slots in the workspace; cleared at the start of every run.
+enum Ctr : int {
+  C_SEL = 0,      // rows passing WHERE (+ join)
+  C_KEPT = 1,     // rows kept after the decision
+  C_TOK = 2,      // total prefill tokens
+  C_STATUS = 3,   // OR of AIQ_DEV_* bits
+  C_GROUPS = 4,   // non-empty groups
+  C_SCRATCH = 5,  // scan totals land here before being copied
+  C_NSEQ = 6,     // prefill-only: number of sequences
+  C_COUNT = 16
+};
+
+// chunk descriptor: int64 x 4 per chunk
+enum Desc : int { D_TOK_BEGIN = 0, D_NTOK = 1, D_SEQ_BEGIN = 2, D_NSEQ = 3, D_STRIDE = 4 };
+
+struct DPred {
+  const void* data;
+  int32_t dtype;
+  int32_t op;
+  int64_t k;
+  int32_t n_set;
+  int32_t set[AIQ_MAX_IN_SET];
+};
+
+struct DPredList {
+  int32_t n;
+  DPred p[AIQ_MAX_PREDS];
+};
+
+struct HashArgs {
+  int32_t* keys;      // [cap], EMPTY = INT32_MIN
+  int32_t* vals;      // [cap]
+  int32_t cap_log2;
+};
+
+constexpr int32_t HASH_EMPTY = INT32_MIN;
+
+// relational block geometry: 256 threads x 8 rows
+constexpr int REL_THREADS = 256;
+constexpr int REL_ROWS_PER_THREAD = 8;
+constexpr int REL_ROWS_PER_BLOCK = REL_THREADS * REL_ROWS_PER_THREAD;   // 2048
+constexpr int REL_WORDS_PER_BLOCK = REL_ROWS_PER_BLOCK / 64;             // 32
+
+// ---------------------------------------------------------------- launchers
+// Every launcher enqueues on `s` and returns hipGetLastError().
+
+// relational
+hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
+hipError_t launch_fill_i64(int64_t* p, int64_t n, int64_t v, hipStream_t s);
+hipError_t launch_hash_build(const DPredList& preds, const void* key_col, int32_t key_dtype,
+                             const void* pay_col, int32_t pay_dtype, int64_t n_rows, HashArgs h,
+                             int64_t* ctr, hipStream_t s);
+hipError_t launch_row_mask(const DPredList& preds, int64_t n_rows, const void* probe_key,
+                           int32_t probe_key_dtype, HashArgs h, int join, uint64_t* mask,
+                           int32_t* blk_cnt, hipStream_t s);
+hipError_t launch_label_mask(const int32_t* label, const int64_t* n_ptr, int64_t n_ub,
+                             uint64_t* mask, int32_t* blk_cnt, hipStream_t s);
+hipError_t launch_scan_blocks(const int32_t* blk_cnt, const int64_t* n_ptr, int64_t n_ub,
+                              int64_t* blk_off, int64_t* total_out, hipStream_t s);
+hipError_t launch_scatter_rows(const uint64_t* mask, const int64_t* blk_off, const int64_t* n_ptr,
+                               int64_t n_ub, const int32_t* src_ids, int32_t* out_ids,
+                               int64_t out_cap, const void* probe_key, int32_t probe_key_dtype,
+                               HashArgs h, int join, int32_t* out_payload, int64_t* ctr,
+                               hipStream_t s);
+hipError_t launch_group_accumulate(const int32_t* sel, const int32_t* label, const int32_t* payload,
+                                   const uint8_t* keep_by_label, const int64_t* n_ptr, int64_t n_ub,
+                                   const void* key_col, int32_t key_dtype, int mode,
+                                   int32_t n_keys, int64_t* bins, int64_t* ctr, hipStream_t s);
+hipError_t launch_group_emit(const int64_t* bins, int32_t n_keys, int32_t* key_out,
+                             int64_t* cnt_out, int64_t* sum_out, double* avg_out, int64_t cap,
+                             int mode, int64_t* ctr, hipStream_t s);
+hipError_t launch_copy_ids(const int32_t* src, const int64_t* n_ptr, int64_t n_ub, int32_t* dst,
+                           int64_t cap, int64_t* ctr, int set_kept, hipStream_t s);
+hipError_t launch_copy_f32(const float* src, const int64_t* n_ptr, int64_t n_ub, int32_t per_row,
+                           float* dst, int64_t cap_rows, hipStream_t s);
+hipError_t launch_finalize(const int64_t* ctr, int64_t* scalars, hipStream_t s);
+
+// packing / chunking
+hipError_t launch_seq_lengths(const int32_t* sel, const int64_t* n_ptr, int64_t n_ub,
+                              const int64_t* offsets, int32_t max_len, int32_t n_prefix,
+                              int32_t* lens, int64_t* ctr, hipStream_t s);
+hipError_t launch_scan_lengths(const int32_t* lens, const int64_t* n_ptr, int64_t n_ub,
+                               int64_t* block_tmp, int64_t* cu, int64_t* total_out,
+                               hipStream_t s);
+struct Prefix {
+  int32_t n;
+  int32_t tok[AIQ_MAX_PREFIX];
+};
+hipError_t launch_gather_tokens(const int32_t* sel, const int64_t* n_ptr, int64_t n_ub,
+                                const int64_t* offsets, const int32_t* tokens, const int64_t* cu,
+                                const Prefix& prefix, int32_t vocab, int64_t t_ub, int32_t* packed,
+                                int64_t* ctr, hipStream_t s);
+hipError_t launch_chunk_desc(const int64_t* cu, const int64_t* n_ptr, int64_t chunk_tokens,
+                             int64_t n_chunks, int64_t t_ub, int64_t* desc, hipStream_t s);
+hipError_t launch_packed_desc(const int32_t* cu32, int32_t n_seq, int64_t n_tok, int64_t* cu64,
+                              int64_t* desc, int64_t* ctr, hipStream_t s);
+
+// per-chunk transformer
+hipError_t launch_rope_table(int32_t max_pos, int32_t half, double theta, int32_t hd, float* cos_t,
+                             float* sin_t, hipStream_t s);
+hipError_t launch_embed(const int64_t* desc, const int64_t* cu, const int32_t* packed,
+                        const void* emb, int32_t wdtype, int32_t d, int32_t vocab, float* x, int32_t* pos,
+                        int64_t* ctr, int64_t t_cap, hipStream_t s);
+hipError_t launch_rmsnorm(const int64_t* desc, const float* x, const float* g, int32_t d,
+                          float eps, void* out, int32_t out_bf16, int64_t t_cap, hipStream_t s);
+
+enum Epi : int { EPI_STORE_F32 = 0, EPI_QKV_ROPE = 1, EPI_RESID = 2, EPI_SWIGLU = 3, EPI_GELU = 4,
+                 EPI_STORE_ACT = 5 };
+
+struct GemmArgs {
+  const void* A;             // [M, K] activations (bf16 or f32), row stride lda
+  int64_t lda;
+  const int64_t* m_ptr;      // device: number of rows M
+  int64_t m_ub;              // host: upper bound on M (grid sizing)
+  int32_t N, K;
+  const void* B0;            // weight sources, row-major [rows, K]
+  const void* B1;
+  const void* B2;
+  int32_t n_q, n_kv;         // QKV section widths (d_q, d_kv); SwiGLU: d_ff in n_q
+  int32_t hd;
+  void* C;                   // output
+  int64_t ldc;
+  float* X;                  // residual stream [M, ldx] (EPI_RESID)
+  int64_t ldx;
+  const int32_t* pos;        // [M] positions (EPI_QKV_ROPE)
+  const float* rope_cos;     // [max_pos, hd/2]
+  const float* rope_sin;
+};
+
+hipError_t launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t s);
+hipError_t launch_gemm_f32(int epi, const GemmArgs& a, hipStream_t s);
+hipError_t launch_rope_f32(const int64_t* desc, float* qkv, int64_t ld, int32_t n_q, int32_t n_kv,
+                           int32_t hd, const int32_t* pos, const float* cos_t, const float* sin_t,
+                           int64_t t_cap, hipStream_t s);
+
+struct AttnArgs {
+  const void* qkv;           // [T, ld] : q | k | v
+  int64_t ld;
+  void* out;                 // [T, ldo]
+  int64_t ldo;
+  const int64_t* desc;       // chunk descriptor (n_tok, n_seq, seq_begin)
+  const int64_t* cu;         // global cu_seqlens (int64)
+  int32_t n_heads, n_kv, hd;
+  int64_t seq_ub;            // host upper bound on sequences per chunk
+};
+hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s);
+hipError_t launch_attention_f32(const AttnArgs& a, hipStream_t s);
+
+struct HeadArgs {
+  const int64_t* desc;
+  const int64_t* cu;
+  const float* x;            // residual [T, d]
+  const float* g;            // final norm gains
+  float eps;
+  int32_t d;
+  const void* lm_head;       // [vocab, d]
+  int32_t wdtype;
+  int32_t n_labels;
+  int32_t labels[AIQ_MAX_LABELS];
+  int32_t decision;
+  int32_t* label_out;        // [global seq]
+  float* logits_out;         // [global seq, n_labels] or NULL
+  void* hf_out;              // optional normalised rows [local seq, d] (full-vocab mode)
+  int32_t hf_bf16;
+  int64_t seq_ub;
+};
+hipError_t launch_head(const HeadArgs& a, hipStream_t s);
+
+}  // namespace aiq

@@ -1,0 +1,142 @@
+// RMSNorm of the residual stream, and the last-position label head.
+//
+// The semantic decision reads only the last position's logits of each row
+// and only the label columns (Figure 2: logits[:, -1, :], then the Yes / No
+// columns compared on chip).  The head therefore never forms the [tokens,
+// vocab] logits: one wave per sequence normalises the last token's residual
+// row in fp32 and takes K dot products with the label rows of the LM head.
+#include "aiq_internal.h"
+
+namespace aiq {
+
+static int grid_for(int64_t n, int per_block, int cap) {
+  int64_t g = (n + per_block - 1) / per_block;
+  if (g < 1) g = 1;
+  if (g > cap) g = cap;
+  return static_cast<int>(g);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
+
+// ------------------------------------------------------------------ RMSNorm
+// One wave per row: out = x / sqrt(mean(x^2) + eps) * g.  The sum of squares
+// is reduced in a fixed order inside the row, so a row's result does not
+// depend on which other rows share the launch.
+__global__ __launch_bounds__(256) void k_rmsnorm(const int64_t* desc, const float* x, const float* g, int32_t d,
+                                                 float eps, void* out, int32_t out_bf16) {
+  const int64_t nt = desc[D_NTOK];
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6;
+  const int64_t n_waves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  const int nv = d >> 2;
+  for (int64_t t = wave; t < nt; t += n_waves) {
+    const float4* xr = reinterpret_cast<const float4*>(x + t * d);
+    float ss = 0.f;
+    for (int v = lane; v < nv; v += 64) {
+      const float4 a = xr[v];
+      ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
+    }
+    ss = wave_sum(ss);
+    const float r = 1.0f / sqrtf(ss / static_cast<float>(d) + eps);
+    const float4* gr = reinterpret_cast<const float4*>(g);
+    if (out_bf16) {
+      uint2* o = reinterpret_cast<uint2*>(static_cast<uint16_t*>(out) + t * d);
+      for (int v = lane; v < nv; v += 64) {
+        const float4 a = xr[v], w = gr[v];
+        uint2 p;
+        p.x = f2bf(a.x * r * w.x) | (static_cast<uint32_t>(f2bf(a.y * r * w.y)) << 16);
+        p.y = f2bf(a.z * r * w.z) | (static_cast<uint32_t>(f2bf(a.w * r * w.w)) << 16);
+        o[v] = p;
+      }
+    } else {
+      float4* o = reinterpret_cast<float4*>(static_cast<float*>(out) + t * d);
+      for (int v = lane; v < nv; v += 64) {
+        const float4 a = xr[v], w = gr[v];
+        o[v] = make_float4(a.x * r * w.x, a.y * r * w.y, a.z * r * w.z, a.w * r * w.w);
+      }
+    }
+  }
+}
+
+hipError_t launch_rmsnorm(const int64_t* desc, const float* x, const float* g, int32_t d,
+                          float eps, void* out, int32_t out_bf16, int64_t t_cap, hipStream_t s) {
+  hipLaunchKernelGGL(k_rmsnorm, dim3(grid_for(t_cap, 4, 4096)), dim3(256), 0, s, desc, x, g, d, eps, out, out_bf16);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ label head + decision
+// Wave per sequence of the chunk.  label_out / logits_out are indexed by the
+// global sequence number (seq_begin + local index).
+__global__ __launch_bounds__(256) void k_head(HeadArgs a) {
+  const int64_t tb = a.desc[D_TOK_BEGIN], sb = a.desc[D_SEQ_BEGIN], ns = a.desc[D_NSEQ];
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6;
+  const int64_t n_waves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  const int d = a.d;
+  for (int64_t i = wave; i < ns; i += n_waves) {
+    const int64_t gi = sb + i;
+    const bool empty = a.cu[gi + 1] == a.cu[gi];   // no token: every logit is 0
+    const int64_t last = empty ? 0 : a.cu[gi + 1] - 1 - tb;
+    const float* xr = a.x + last * d;
+    float ss = 0.f;
+    for (int c = lane; c < d; c += 64) ss += xr[c] * xr[c];
+    ss = wave_sum(ss);
+    const float r = empty ? 0.f : 1.0f / sqrtf(ss / static_cast<float>(d) + a.eps);
+    float lg[AIQ_MAX_LABELS];
+    for (int k = 0; k < a.n_labels; ++k) {
+      float acc = 0.f;
+      if (a.wdtype == AIQ_BF16) {
+        const uint16_t* w = static_cast<const uint16_t*>(a.lm_head) + static_cast<int64_t>(a.labels[k]) * d;
+        for (int c = lane; c < d; c += 64) acc += (xr[c] * r * a.g[c]) * bf2f(w[c]);
+      } else {
+        const float* w = static_cast<const float*>(a.lm_head) + static_cast<int64_t>(a.labels[k]) * d;
+        for (int c = lane; c < d; c += 64) acc += (xr[c] * r * a.g[c]) * w[c];
+      }
+      lg[k] = wave_sum(acc);
+    }
+    if (a.hf_out) {
+      if (a.hf_bf16) {
+        uint16_t* o = static_cast<uint16_t*>(a.hf_out) + i * d;
+        for (int c = lane; c < d; c += 64) o[c] = f2bf(xr[c] * r * a.g[c]);
+      } else {
+        float* o = static_cast<float*>(a.hf_out) + i * d;
+        for (int c = lane; c < d; c += 64) o[c] = xr[c] * r * a.g[c];
+      }
+    }
+    if (lane == 0) {
+      if (a.logits_out)
+        for (int k = 0; k < a.n_labels; ++k) a.logits_out[gi * a.n_labels + k] = lg[k];
+      if (a.label_out) {
+        int32_t lab;
+        if (a.decision == AIQ_DECIDE_BINARY_GT) {
+          lab = lg[0] > lg[1] ? 1 : 0;
+        } else {
+          int best = 0;
+          for (int k = 1; k < a.n_labels; ++k)
+            if (lg[k] > lg[best]) best = k;
+          lab = a.labels[best];
+        }
+        a.label_out[gi] = lab;
+      }
+    }
+  }
+}
+
+hipError_t launch_head(const HeadArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_head, dim3(grid_for(a.seq_ub, 4, 2048)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace aiq

@@ -1,0 +1,337 @@
+// Packing of the selected rows into one variable-length token batch, and the
+// device-side chunk descriptors that stand in for static shapes.
+//
+// The paper's prototype pads every row to a static maximum length and feeds
+// fixed micro-batches through the model (Section 3.2 scan loop; Section 5
+// names dynamic shapes as future work).  Here sequence i (the prompt prefix
+// followed by selected row i's token list) occupies packed[cu[i] .. cu[i+1])
+// with no padding, and the packed batch is cut at sequence boundaries into
+// chunks of at most chunk_tokens + longest-sequence tokens.  Every count
+// lives in device memory; kernels read their real extents from it.
+#include "aiq_internal.h"
+
+namespace aiq {
+
+static int grid_for(int64_t n, int threads, int cap = 4096) {
+  int64_t g = (n + threads - 1) / threads;
+  if (g < 1) g = 1;
+  if (g > cap) g = cap;
+  return static_cast<int>(g);
+}
+
+__device__ __forceinline__ void set_status(int64_t* ctr, int64_t bits) {
+  atomicOr(reinterpret_cast<unsigned long long*>(ctr + C_STATUS), static_cast<unsigned long long>(bits));
+}
+
+// ------------------------------------------------------------------ lengths
+__global__ void k_seq_lengths(const int32_t* sel, const int64_t* n_ptr, const int64_t* off, int32_t max_len,
+                              int32_t n_prefix, int32_t* lens, int64_t* ctr) {
+  const int64_t n = *n_ptr;
+  bool bad = false;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = sel[i];
+    int64_t len = off[r + 1] - off[r];
+    if (len < 0 || len > max_len) {
+      bad = true;
+      len = len < 0 ? 0 : max_len;
+    }
+    lens[i] = static_cast<int32_t>(len) + n_prefix;
+  }
+  if (bad) set_status(ctr, AIQ_DEV_LIST_LEN);
+}
+
+hipError_t launch_seq_lengths(const int32_t* sel, const int64_t* n_ptr, int64_t n_ub,
+                              const int64_t* offsets, int32_t max_len, int32_t n_prefix,
+                              int32_t* lens, int64_t* ctr, hipStream_t s) {
+  hipLaunchKernelGGL(k_seq_lengths, dim3(grid_for(n_ub, 256)), dim3(256), 0, s, sel, n_ptr, offsets,
+                     max_len, n_prefix, lens, ctr);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ scan of lengths -> cu (int64)
+// Three phases over tiles of 4096 lengths: tile sums, one-workgroup scan of
+// the tile sums, then per-tile inclusive scan plus the tile offset.
+
+constexpr int SCAN_T = 1024;
+constexpr int SCAN_PER = 4;
+constexpr int SCAN_TILE = SCAN_T * SCAN_PER;
+
+__device__ __forceinline__ int64_t wg_exclusive_scan(int64_t v, int64_t* total) {
+  __shared__ int64_t wsum[SCAN_T / 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int64_t x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int64_t y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) wsum[w] = x;
+  __syncthreads();
+  int64_t before = 0, all = 0;
+  for (int i = 0; i < SCAN_T / 64; ++i) {
+    const int64_t ws = wsum[i];
+    if (i < w) before += ws;
+    all += ws;
+  }
+  __syncthreads();
+  *total = all;
+  return before + x - v;
+}
+
+__global__ __launch_bounds__(SCAN_T) void k_scan_tile_sums(const int32_t* lens, const int64_t* n_ptr,
+                                                           int64_t* tile_sum) {
+  const int64_t n = *n_ptr;
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * SCAN_TILE;
+  if (base >= n) return;
+  int64_t v = 0;
+  for (int j = 0; j < SCAN_PER; ++j) {
+    const int64_t i = base + threadIdx.x * SCAN_PER + j;
+    if (i < n) v += lens[i];
+  }
+  int64_t tot;
+  wg_exclusive_scan(v, &tot);
+  if (threadIdx.x == 0) tile_sum[blockIdx.x] = tot;
+}
+
+__global__ __launch_bounds__(SCAN_T) void k_scan_tile_offsets(int64_t* tile_sum, const int64_t* n_ptr,
+                                                              int64_t* total_out, int64_t* cu) {
+  const int64_t n = *n_ptr;
+  const int64_t nt = (n + SCAN_TILE - 1) / SCAN_TILE;
+  int64_t carry = 0;
+  for (int64_t t0 = 0; t0 < nt; t0 += SCAN_T) {
+    const int64_t t = t0 + threadIdx.x;
+    const int64_t v = t < nt ? tile_sum[t] : 0;
+    int64_t tot;
+    const int64_t ex = wg_exclusive_scan(v, &tot);
+    if (t < nt) tile_sum[t] = carry + ex;   // becomes the tile's exclusive offset
+    carry += tot;
+  }
+  if (threadIdx.x == 0) {
+    *total_out = carry;
+    cu[0] = 0;
+  }
+}
+
+__global__ __launch_bounds__(SCAN_T) void k_scan_tile_apply(const int32_t* lens, const int64_t* n_ptr,
+                                                            const int64_t* tile_off, int64_t* cu) {
+  const int64_t n = *n_ptr;
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * SCAN_TILE;
+  if (base >= n) return;
+  int64_t v[SCAN_PER];
+  int64_t s = 0;
+  for (int j = 0; j < SCAN_PER; ++j) {
+    const int64_t i = base + threadIdx.x * SCAN_PER + j;
+    v[j] = i < n ? lens[i] : 0;
+    s += v[j];
+  }
+  int64_t tot;
+  int64_t run = tile_off[blockIdx.x] + wg_exclusive_scan(s, &tot);
+  for (int j = 0; j < SCAN_PER; ++j) {
+    const int64_t i = base + threadIdx.x * SCAN_PER + j;
+    run += v[j];
+    if (i < n) cu[i + 1] = run;
+  }
+}
+
+hipError_t launch_scan_lengths(const int32_t* lens, const int64_t* n_ptr, int64_t n_ub,
+                               int64_t* block_tmp, int64_t* cu, int64_t* total_out,
+                               hipStream_t s) {
+  const int64_t nt = (n_ub + SCAN_TILE - 1) / SCAN_TILE;
+  const unsigned g = static_cast<unsigned>(nt < 1 ? 1 : nt);
+  hipLaunchKernelGGL(k_scan_tile_sums, dim3(g), dim3(SCAN_T), 0, s, lens, n_ptr, block_tmp);
+  hipLaunchKernelGGL(k_scan_tile_offsets, dim3(1), dim3(SCAN_T), 0, s, block_tmp, n_ptr, total_out, cu);
+  hipLaunchKernelGGL(k_scan_tile_apply, dim3(g), dim3(SCAN_T), 0, s, lens, n_ptr, block_tmp, cu);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ gather
+// One wave per sequence: the prompt prefix, then the row's tokens.  Token ids
+// outside [0, vocab) are flagged and replaced by 0 so later gathers stay in
+// bounds.
+__global__ __launch_bounds__(256) void k_gather(const int32_t* sel, const int64_t* n_ptr, const int64_t* off,
+                                                const int32_t* tokens, const int64_t* cu, Prefix pre,
+                                                int32_t vocab, int64_t t_ub, int32_t* packed, int64_t* ctr) {
+  const int64_t n = *n_ptr;
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6;
+  const int64_t n_waves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  bool bad = false;
+  for (int64_t i = wave; i < n; i += n_waves) {
+    if (cu[i + 1] > t_ub) {   // more tokens than the table declared: never written
+      bad = true;
+      continue;
+    }
+    const int64_t r = sel[i];
+    int32_t* dst = packed + cu[i];
+    for (int j = lane; j < pre.n; j += 64) dst[j] = pre.tok[j];
+    const int64_t L = cu[i + 1] - cu[i] - pre.n;
+    const int32_t* src = tokens + off[r];
+    for (int64_t j = lane; j < L; j += 64) {
+      int32_t t = src[j];
+      if (t < 0 || t >= vocab) {
+        bad = true;
+        t = 0;
+      }
+      dst[pre.n + j] = t;
+    }
+  }
+  if (bad) set_status(ctr, AIQ_DEV_TOKEN_RANGE);
+}
+
+hipError_t launch_gather_tokens(const int32_t* sel, const int64_t* n_ptr, int64_t n_ub,
+                                const int64_t* offsets, const int32_t* tokens, const int64_t* cu,
+                                const Prefix& prefix, int32_t vocab, int64_t t_ub, int32_t* packed,
+                                int64_t* ctr, hipStream_t s) {
+  hipLaunchKernelGGL(k_gather, dim3(grid_for(n_ub, 4, 2048)), dim3(256), 0, s, sel, n_ptr, offsets,
+                     tokens, cu, prefix, vocab, t_ub, packed, ctr);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ chunk descriptors
+// Chunk c holds the sequences whose first token index lies in
+// [c*chunk_tokens, (c+1)*chunk_tokens).
+__device__ __forceinline__ int64_t lower_bound_cu(const int64_t* cu, int64_t n, int64_t v) {
+  int64_t lo = 0, hi = n;  // first i in [0, n) with cu[i] >= v, else n
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) >> 1;
+    if (cu[mid] < v) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
+__global__ void k_chunk_desc(const int64_t* cu, const int64_t* n_ptr, int64_t chunk_tokens, int64_t n_chunks,
+                             int64_t t_ub, int64_t* desc) {
+  // only sequences that end inside the packed buffer take part
+  int64_t n = *n_ptr;
+  {
+    int64_t lo = 0, hi = n;   // first i with cu[i + 1] > t_ub
+    while (lo < hi) {
+      const int64_t mid = (lo + hi) >> 1;
+      if (cu[mid + 1] > t_ub) hi = mid;
+      else lo = mid + 1;
+    }
+    n = lo;
+  }
+  for (int64_t c = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; c < n_chunks; c += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t sb = lower_bound_cu(cu, n, c * chunk_tokens);
+    const int64_t se = lower_bound_cu(cu, n, (c + 1) * chunk_tokens);
+    int64_t* d = desc + c * D_STRIDE;
+    d[D_TOK_BEGIN] = cu[sb];
+    d[D_NTOK] = cu[se] - cu[sb];
+    d[D_SEQ_BEGIN] = sb;
+    d[D_NSEQ] = se - sb;
+  }
+}
+
+hipError_t launch_chunk_desc(const int64_t* cu, const int64_t* n_ptr, int64_t chunk_tokens,
+                             int64_t n_chunks, int64_t t_ub, int64_t* desc, hipStream_t s) {
+  hipLaunchKernelGGL(k_chunk_desc, dim3(grid_for(n_chunks, 256)), dim3(256), 0, s, cu, n_ptr,
+                     chunk_tokens, n_chunks, t_ub, desc);
+  return hipGetLastError();
+}
+
+// prefill-only entry: one chunk covering a caller-packed batch.  One
+// workgroup checks cu_seqlens (starts at 0, ends at n_tok, every sequence at
+// least one token); a malformed array empties the chunk and sets a status bit
+// so no later kernel indexes outside the caller's buffers.
+__global__ __launch_bounds__(1024) void k_packed_desc(const int32_t* cu32, int32_t n_seq, int64_t n_tok,
+                                                      int64_t* cu64, int64_t* desc, int64_t* ctr) {
+  int bad = 0;
+  for (int64_t i = threadIdx.x; i <= n_seq; i += blockDim.x) {
+    const int64_t v = cu32[i];
+    cu64[i] = v;
+    if (i == 0 && v != 0) bad = 1;
+    if (i == n_seq && v != n_tok) bad = 1;
+    if (i < n_seq && static_cast<int64_t>(cu32[i + 1]) <= v) bad = 1;
+  }
+  bad = __syncthreads_or(bad);
+  if (threadIdx.x == 0) {
+    desc[D_TOK_BEGIN] = 0;
+    desc[D_NTOK] = bad ? 0 : n_tok;
+    desc[D_SEQ_BEGIN] = 0;
+    desc[D_NSEQ] = bad ? 0 : n_seq;
+    ctr[C_NSEQ] = bad ? 0 : n_seq;
+    if (bad) ctr[C_STATUS] |= AIQ_DEV_LIST_LEN;
+  }
+}
+
+hipError_t launch_packed_desc(const int32_t* cu32, int32_t n_seq, int64_t n_tok, int64_t* cu64,
+                              int64_t* desc, int64_t* ctr, hipStream_t s) {
+  hipLaunchKernelGGL(k_packed_desc, dim3(1), dim3(1024), 0, s, cu32, n_seq, n_tok, cu64, desc, ctr);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ rotary table
+// cos / sin of pos * theta**(-2i/hd), evaluated in fp64 and rounded to fp32.
+__global__ void k_rope_table(int32_t max_pos, int32_t half, double theta, int32_t hd, float* cos_t, float* sin_t) {
+  const int64_t n = static_cast<int64_t>(max_pos) * half;
+  for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < n; j += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t p = j / half;
+    const int i = static_cast<int>(j % half);
+    const double inv = pow(theta, -2.0 * static_cast<double>(i) / static_cast<double>(hd));
+    const double a = static_cast<double>(p) * inv;
+    cos_t[j] = static_cast<float>(cos(a));
+    sin_t[j] = static_cast<float>(sin(a));
+  }
+}
+
+hipError_t launch_rope_table(int32_t max_pos, int32_t half, double theta, int32_t hd, float* cos_t,
+                             float* sin_t, hipStream_t s) {
+  hipLaunchKernelGGL(k_rope_table, dim3(grid_for(static_cast<int64_t>(max_pos) * half, 256)), dim3(256), 0,
+                     s, max_pos, half, theta, hd, cos_t, sin_t);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ embedding
+// One workgroup per chunk token (grid-stride): x[t, :] = E[tok, :] in fp32 and
+// pos[t] = position of the token inside its own sequence.
+__global__ __launch_bounds__(256) void k_embed(const int64_t* desc, const int64_t* cu, const int32_t* packed,
+                                               const void* emb, int32_t wdtype, int32_t d, int32_t vocab,
+                                               float* x, int32_t* pos, int64_t* ctr) {
+  const int64_t tb = desc[D_TOK_BEGIN], nt = desc[D_NTOK], sb = desc[D_SEQ_BEGIN], ns = desc[D_NSEQ];
+  for (int64_t t = blockIdx.x; t < nt; t += gridDim.x) {
+    const int64_t g = tb + t;
+    int32_t tok = packed[g];
+    if (tok < 0 || tok >= vocab) {   // only reachable through caller-packed batches
+      if (threadIdx.x == 0) set_status(ctr, AIQ_DEV_TOKEN_RANGE);
+      tok = 0;
+    }
+    if (threadIdx.x == 0) {
+      int64_t lo = sb, hi = sb + ns - 1;   // last i with cu[i] <= g
+      while (lo < hi) {
+        const int64_t mid = (lo + hi + 1) >> 1;
+        if (cu[mid] <= g) lo = mid;
+        else hi = mid - 1;
+      }
+      pos[t] = static_cast<int32_t>(g - cu[lo]);
+    }
+    float* xr = x + t * d;
+    if (wdtype == AIQ_BF16) {
+      const uint16_t* er = static_cast<const uint16_t*>(emb) + static_cast<int64_t>(tok) * d;
+      for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
+        const uint2 v = *reinterpret_cast<const uint2*>(er + c);
+        float4 o;
+        o.x = __uint_as_float((v.x & 0xFFFFu) << 16);
+        o.y = __uint_as_float(v.x & 0xFFFF0000u);
+        o.z = __uint_as_float((v.y & 0xFFFFu) << 16);
+        o.w = __uint_as_float(v.y & 0xFFFF0000u);
+        *reinterpret_cast<float4*>(xr + c) = o;
+      }
+    } else {
+      const float* er = static_cast<const float*>(emb) + static_cast<int64_t>(tok) * d;
+      for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4)
+        *reinterpret_cast<float4*>(xr + c) = *reinterpret_cast<const float4*>(er + c);
+    }
+  }
+}
+
+hipError_t launch_embed(const int64_t* desc, const int64_t* cu, const int32_t* packed,
+                        const void* emb, int32_t wdtype, int32_t d, int32_t vocab, float* x, int32_t* pos,
+                        int64_t* ctr, int64_t t_cap, hipStream_t s) {
+  hipLaunchKernelGGL(k_embed, dim3(grid_for(t_cap, 1, 8192)), dim3(256), 0, s, desc, cu, packed, emb, wdtype,
+                     d, vocab, x, pos, ctr);
+  return hipGetLastError();
+}
+
+}  // namespace aiq

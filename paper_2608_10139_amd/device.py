@@ -1,0 +1,271 @@
+"""Device-memory plumbing around the C ABI: uploads host arrays into torch
+device tensors, fills the ABI structs with their addresses, allocates the
+workspace and output buffers, and calls the library on torch's current
+stream.  No arithmetic of the query happens here.
+
+Inputs are plain host structures:
+  tables = {"probe": {col: ndarray, "offsets": int64[n+1], "tokens": int32[nnz]},
+            "build": {col: ndarray} or None, "prefix": int32[...]}
+  model  = {"spec": <object with n_layers, d_model, ...>, "emb", "layers": [...],
+            "final_norm", "lm_head"} with bf16 weights as uint16 bit patterns
+  query  = <object with preds, labels, decision, agg, join, n_prefix, group_col,
+            n_group_keys>
+"""
+from __future__ import annotations
+
+import ctypes as C
+
+import numpy as np
+import torch
+
+from . import binding as B
+
+_NP_DTYPE = {np.dtype(np.int8): B.AIQ_I8, np.dtype(np.int16): B.AIQ_I16, np.dtype(np.int32): B.AIQ_I32}
+_DECISION = {"binary_gt": B.AIQ_DECIDE_BINARY_GT, "argmax": B.AIQ_DECIDE_ARGMAX}
+_AGG = {"count": B.AIQ_AGG_COUNT, "avg_label_count_by": B.AIQ_AGG_AVG_LABEL_COUNT_BY,
+        "count_by_payload": B.AIQ_AGG_COUNT_BY_PAYLOAD}
+_LIST_KEYS = ("offsets", "tokens")
+
+
+def _dev(a: np.ndarray, device) -> torch.Tensor:
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:   # bf16 bit patterns
+        return torch.from_numpy(a.view(np.int16)).to(device).view(torch.bfloat16)
+    return torch.from_numpy(a).to(device)
+
+
+def _layers_opt(n_layers) -> int:
+    # 0 asks for every layer; a request for zero layers is encoded as -1
+    if n_layers is None:
+        return 0
+    return -1 if int(n_layers) == 0 else int(n_layers)
+
+
+def _ptr(t) -> int:
+    return 0 if t is None else int(t.data_ptr())
+
+
+class DeviceModel:
+    """Model weights resident in device memory plus the aiq_model struct."""
+
+    def __init__(self, model: dict, device="cuda"):
+        spec = model["spec"]
+        self.spec = spec
+        self.keep = []
+
+        def up(a):
+            t = _dev(a, device)
+            self.keep.append(t)
+            return t
+
+        self.emb = up(model["emb"])
+        self.lm_head = up(model["lm_head"])
+        self.final_norm = up(np.asarray(model["final_norm"], dtype=np.float32))
+        L = len(model["layers"])
+        self.layers = (B.aiq_layer * max(L, 1))()
+        for i, lw in enumerate(model["layers"]):
+            s = self.layers[i]
+            s.attn_norm = _ptr(up(np.asarray(lw["attn_norm"], dtype=np.float32)))
+            s.ffn_norm = _ptr(up(np.asarray(lw["ffn_norm"], dtype=np.float32)))
+            for k in ("wq", "wk", "wv", "wo", "w_gate", "w_down"):
+                setattr(s, k, _ptr(up(lw[k])))
+            s.w_up = _ptr(up(lw["w_up"])) if "w_up" in lw else 0
+        m = B.aiq_model()
+        m.n_layers, m.d_model, m.n_heads = L, spec.d_model, spec.n_heads
+        m.n_kv_heads, m.d_ff, m.vocab = spec.n_kv_heads, spec.d_ff, spec.vocab
+        m.act = B.AIQ_ACT_SWIGLU if spec.act == "swiglu" else B.AIQ_ACT_GELU_ERF
+        m.wdtype = B.AIQ_BF16 if spec.dtype == "bf16" else B.AIQ_F32
+        m.rope_theta, m.norm_eps = spec.rope_theta, spec.norm_eps
+        m.emb, m.lm_head, m.final_norm = _ptr(self.emb), _ptr(self.lm_head), _ptr(self.final_norm)
+        m.layers = C.cast(self.layers, C.POINTER(B.aiq_layer))
+        self.struct = m
+
+
+class DeviceTable:
+    def __init__(self, cols: dict, device="cuda", with_list=True, max_list_len=None):
+        self.names = [k for k in cols if k not in _LIST_KEYS]
+        self.index = {k: i for i, k in enumerate(self.names)}
+        self.tensors = {k: _dev(cols[k], device) for k in self.names}
+        self.dtypes = {k: np.asarray(cols[k]).dtype for k in self.names}
+        n = len(cols[self.names[0]]) if self.names else len(cols["offsets"]) - 1
+        self.n_rows = n
+        self.cols = (B.aiq_col * max(len(self.names), 1))()
+        for i, k in enumerate(self.names):
+            self.cols[i].data = _ptr(self.tensors[k])
+            self.cols[i].dtype = _NP_DTYPE[self.dtypes[k]]
+        t = B.aiq_table()
+        t.n_rows, t.n_cols = n, len(self.names)
+        t.cols = C.cast(self.cols, C.POINTER(B.aiq_col))
+        if with_list:
+            off = np.asarray(cols["offsets"], dtype=np.int64)
+            self.offsets = _dev(off, device)
+            tok = np.asarray(cols["tokens"], dtype=np.int32)
+            self.tokens = _dev(tok if len(tok) else np.zeros(1, np.int32), device)
+            t.list_offsets, t.list_tokens = _ptr(self.offsets), _ptr(self.tokens)
+            t.n_list_tokens = int(off[-1] - off[0])
+            lens = np.diff(off)
+            t.max_list_len = int(max_list_len if max_list_len is not None else max(1, lens.max(initial=1)))
+        self.struct = t
+
+
+def _pred(p, index: dict) -> B.aiq_pred:
+    s = B.aiq_pred()
+    s.col = index[p.col]
+    s.op = B.OPS[p.op]
+    s.k = int(p.k)
+    vals = list(p.values)
+    s.n_set = len(vals)
+    for i, v in enumerate(vals):
+        s.set[i] = int(v)
+    return s
+
+
+def make_query(query, probe: DeviceTable | None, build: DeviceTable | None, prefix) -> B.aiq_query:
+    q = B.aiq_query()
+    preds = list(getattr(query, "preds", ()))
+    q.n_pred = len(preds)
+    for i, p in enumerate(preds):
+        q.preds[i] = _pred(p, probe.index)
+    j = getattr(query, "join", None)
+    if j is not None:
+        q.join = 1
+        q.probe_key_col = probe.index[j.probe_key]
+        q.build_key_col = build.index[j.build_key]
+        q.build_payload_col = build.index[j.payload]
+        q.n_build_pred = len(j.build_preds)
+        for i, p in enumerate(j.build_preds):
+            q.build_preds[i] = _pred(p, build.index)
+    n_prefix = int(getattr(query, "n_prefix", 0))
+    q.n_prefix = n_prefix
+    for i in range(n_prefix):
+        q.prefix[i] = int(prefix[i])
+    q.n_labels = len(query.labels)
+    for i, l in enumerate(query.labels):
+        q.label_ids[i] = int(l)
+    q.decision = _DECISION[query.decision]
+    q.agg = _AGG[query.agg]
+    if getattr(query, "group_col", None):
+        q.group_col = probe.index[query.group_col]
+    q.n_group_keys = int(getattr(query, "n_group_keys", 0))
+    return q
+
+
+class DeviceQuery:
+    """A planned query over device-resident tables and weights."""
+
+    def __init__(self, tables: dict, model, query, device="cuda", chunk_tokens: int = 0,
+                 n_layers: int | None = None, dmodel: DeviceModel | None = None):
+        self.device = torch.device(device)
+        self.query = query
+        self.dm = dmodel if dmodel is not None else DeviceModel(model, device)
+        self.probe = DeviceTable(tables["probe"], device)
+        self.build = DeviceTable(tables["build"], device, with_list=False) if tables.get("build") is not None else None
+        self.q = make_query(query, self.probe, self.build, tables.get("prefix", ()))
+        opts = B.aiq_plan_opts()
+        opts.chunk_tokens = int(chunk_tokens)
+        opts.n_layers_override = _layers_opt(n_layers)
+        self.plan = B.aiq_plan_create(self.dm.struct, self.probe.struct,
+                                      self.build.struct if self.build else None, self.q, opts)
+        self.ws_bytes = B.aiq_workspace_size(self.plan)
+        self.ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=self.device)
+        base = self.ws.data_ptr()
+        self.ws_ptr = (base + 255) // 256 * 256
+        n = self.probe.n_rows
+        K = len(query.labels)
+        dev = self.device
+        self.scalars = torch.zeros(B.AIQ_N_SCALARS, dtype=torch.int64, device=dev)
+        self.ids = torch.zeros(max(n, 1), dtype=torch.int32, device=dev)
+        self.sel_ids = torch.zeros(max(n, 1), dtype=torch.int32, device=dev)
+        self.sel_labels = torch.zeros(max(n, 1), dtype=torch.int32, device=dev)
+        self.sel_logits = torch.zeros(max(n, 1) * K, dtype=torch.float32, device=dev)
+        G = max(int(getattr(query, "n_group_keys", 0)), 1)
+        self.grp_key = torch.zeros(G, dtype=torch.int32, device=dev)
+        self.grp_count = torch.zeros(G, dtype=torch.int64, device=dev)
+        self.grp_sum = torch.zeros(G, dtype=torch.int64, device=dev)
+        self.grp_avg = torch.zeros(G, dtype=torch.float64, device=dev)
+        o = B.aiq_out()
+        o.scalars, o.ids, o.ids_cap = _ptr(self.scalars), _ptr(self.ids), n
+        o.sel_ids, o.sel_labels, o.sel_logits, o.sel_cap = (_ptr(self.sel_ids), _ptr(self.sel_labels),
+                                                            _ptr(self.sel_logits), n)
+        o.grp_key, o.grp_count, o.grp_sum, o.grp_avg = (_ptr(self.grp_key), _ptr(self.grp_count),
+                                                        _ptr(self.grp_sum), _ptr(self.grp_avg))
+        o.grp_cap = G
+        self.out = o
+
+    def run(self, trace=None, stream=None) -> None:
+        s = stream if stream is not None else torch.cuda.current_stream(self.device)
+        B.aiq_run(self.plan, self.ws_ptr, self.ws_bytes, self.out, trace, s.cuda_stream)
+
+    def results(self) -> dict:
+        """Copies the outputs to the host (after the stream has been synchronised)."""
+        sc = self.scalars.cpu().numpy()
+        n_sel, n_kept, n_groups = int(sc[B.AIQ_S_SELECTED]), int(sc[B.AIQ_S_KEPT]), int(sc[B.AIQ_S_GROUPS])
+        K = len(self.query.labels)
+        r = {"scalars": sc, "status": int(sc[B.AIQ_S_STATUS]), "n_selected": n_sel, "count": n_kept,
+             "n_tokens": int(sc[B.AIQ_S_TOKENS]),
+             "kept_ids": self.ids[:n_kept].cpu().numpy().astype(np.int64),
+             "sel_ids": self.sel_ids[:n_sel].cpu().numpy().astype(np.int64),
+             "labels": self.sel_labels[:n_sel].cpu().numpy().astype(np.int64),
+             "logits": self.sel_logits[:n_sel * K].cpu().numpy().reshape(n_sel, K)}
+        if self.query.agg != "count":
+            r["groups"] = (self.grp_key[:n_groups].cpu().numpy().astype(np.int64),
+                           self.grp_count[:n_groups].cpu().numpy(), self.grp_sum[:n_groups].cpu().numpy(),
+                           self.grp_avg[:n_groups].cpu().numpy())
+        return r
+
+    def close(self) -> None:
+        if self.plan:
+            B.aiq_plan_destroy(self.plan)
+            self.plan = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class DevicePrefill:
+    """Prefill-only plan: runs the transformer on caller-packed sequences."""
+
+    def __init__(self, model, labels=(1, 2), max_tokens: int = 4096, device="cuda",
+                 n_layers: int | None = None, dmodel: DeviceModel | None = None):
+        self.device = torch.device(device)
+        self.dm = dmodel if dmodel is not None else DeviceModel(model, device)
+        q = B.aiq_query()
+        q.n_labels = len(labels)
+        for i, l in enumerate(labels):
+            q.label_ids[i] = int(l)
+        q.decision = B.AIQ_DECIDE_BINARY_GT if len(labels) == 2 else B.AIQ_DECIDE_ARGMAX
+        q.agg = B.AIQ_AGG_COUNT
+        self.q = q
+        self.K = len(labels)
+        opts = B.aiq_plan_opts()
+        opts.n_layers_override = _layers_opt(n_layers)
+        self.plan = B.aiq_plan_create(self.dm.struct, None, None, q, opts)
+        self.max_tokens = int(max_tokens)
+        self.ws_bytes = B.aiq_prefill_workspace_size(self.plan, self.max_tokens)
+        self.ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=self.device)
+        self.ws_ptr = (self.ws.data_ptr() + 255) // 256 * 256
+
+    def run(self, tok: torch.Tensor, cu: torch.Tensor, full_vocab: bool = False, stream=None) -> torch.Tensor:
+        n_seq = cu.numel() - 1
+        n_tok = tok.numel()
+        width = self.dm.spec.vocab if full_vocab else self.K
+        out = torch.empty(n_seq * width, dtype=torch.float32, device=self.device)
+        s = stream if stream is not None else torch.cuda.current_stream(self.device)
+        B.aiq_prefill_packed(self.plan, _ptr(tok), _ptr(cu), n_seq, n_tok,
+                             B.AIQ_LOGITS_FULL_VOCAB if full_vocab else B.AIQ_LOGITS_LABELS,
+                             _ptr(out), self.ws_ptr, self.ws_bytes, s.cuda_stream)
+        return out.view(n_seq, width)
+
+    def close(self) -> None:
+        if self.plan:
+            B.aiq_plan_destroy(self.plan)
+            self.plan = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,140 @@
+"""Host side of the C ABI, no device needed: the library loads, exports every
+symbol the header declares, and rejects bad requests with the documented
+status codes before enqueueing anything (fake device addresses are never
+dereferenced on these paths)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2608_10139_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x10000   # never dereferenced: plan creation only records addresses
+
+
+def header_functions():
+    src = open(os.path.join(ROOT, "include", "aiq.h")).read()
+    return sorted(set(re.findall(r"\b(aiq_[a-z_]+)\s*\(", src)) - {"aiq_status"})
+
+
+def test_library_exports_every_declared_function():
+    lib = B.load()
+    declared = header_functions()
+    assert set(declared) == set(B.EXPORTS)
+    for fn in declared:
+        assert hasattr(lib, fn), fn
+    assert B.aiq_abi_version() == 1
+    assert B.aiq_status_str(B.AIQ_ENOSPC) == "workspace or capacity too small"
+
+
+def model(**kw):
+    m = B.aiq_model()
+    m.n_layers, m.d_model, m.n_heads, m.n_kv_heads, m.d_ff, m.vocab = 2, 512, 8, 8, 2048, 32000
+    m.act, m.wdtype, m.rope_theta, m.norm_eps = B.AIQ_ACT_SWIGLU, B.AIQ_BF16, 10000.0, 1e-5
+    m.emb = m.final_norm = m.lm_head = FAKE
+    layers = (B.aiq_layer * 2)()
+    for L in layers:
+        for f, _ in B.aiq_layer._fields_:
+            setattr(L, f, FAKE)
+    m.layers = C.cast(layers, C.POINTER(B.aiq_layer))
+    m._keep = layers
+    for k, v in kw.items():
+        setattr(m, k, v)
+    return m
+
+
+def table(n=1000):
+    cols = (B.aiq_col * 2)()
+    cols[0].data, cols[0].dtype = FAKE, B.AIQ_I8
+    cols[1].data, cols[1].dtype = FAKE, B.AIQ_I32
+    t = B.aiq_table()
+    t.n_rows, t.n_cols, t.cols = n, 2, C.cast(cols, C.POINTER(B.aiq_col))
+    t.list_offsets = t.list_tokens = FAKE
+    t.n_list_tokens, t.max_list_len = n * 100, 512
+    t._keep = cols
+    return t
+
+
+def query(**kw):
+    q = B.aiq_query()
+    q.n_pred = 1
+    q.preds[0].col, q.preds[0].op, q.preds[0].k = 0, B.AIQ_LE, 2
+    q.n_labels, q.label_ids[0], q.label_ids[1] = 2, 1, 2
+    q.decision, q.agg = B.AIQ_DECIDE_BINARY_GT, B.AIQ_AGG_COUNT
+    for k, v in kw.items():
+        setattr(q, k, v)
+    return q
+
+
+def test_valid_plan_and_workspace_size():
+    p = B.aiq_plan_create(model(), table(), None, query())
+    try:
+        n = B.aiq_workspace_size(p)
+        assert n > 0
+        assert B.aiq_prefill_workspace_size(p, 4096) > 0
+    finally:
+        B.aiq_plan_destroy(p)
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("d_model", 500, B.AIQ_EINVAL),          # d % n_heads
+    ("n_kv_heads", 3, B.AIQ_EINVAL),         # n_heads % n_kv
+    ("d_model", 8 * 48, B.AIQ_EINVAL),       # head dim 48
+    ("wdtype", 9, B.AIQ_EINVAL),
+    ("act", 7, B.AIQ_EINVAL),
+    ("emb", 0, B.AIQ_EINVAL),
+    ("norm_eps", 0.0, B.AIQ_EINVAL),
+    ("act", B.AIQ_ACT_GELU_ERF, B.AIQ_EUNSUPPORTED),   # bf16 path is SwiGLU only
+])
+def test_model_validation(field, value, code):
+    assert B.aiq_plan_create_status(model(**{field: value}), table(), None, query()) == code
+
+
+def test_null_model_and_bad_query():
+    assert B.aiq_plan_create_status(None, table(), None, query()) == B.AIQ_EINVAL
+    assert B.aiq_plan_create_status(model(), table(), None, query(n_labels=1)) == B.AIQ_EINVAL
+    q = query(); q.preds[0].col = 5
+    assert B.aiq_plan_create_status(model(), table(), None, q) == B.AIQ_EINVAL
+    q = query(); q.preds[0].op = 42
+    assert B.aiq_plan_create_status(model(), table(), None, q) == B.AIQ_EINVAL
+    q = query(); q.label_ids[1] = 32000
+    assert B.aiq_plan_create_status(model(), table(), None, q) == B.AIQ_EINVAL
+    # a join without a build table, and a build table without a join
+    assert B.aiq_plan_create_status(model(), table(), None, query(join=1)) == B.AIQ_EINVAL
+    assert B.aiq_plan_create_status(model(), table(), table(), query()) == B.AIQ_EINVAL
+    # group-by needs a key domain
+    assert B.aiq_plan_create_status(model(), table(), None, query(agg=B.AIQ_AGG_AVG_LABEL_COUNT_BY,
+                                                                  group_col=1)) == B.AIQ_EINVAL
+    # count-by-payload needs a join
+    assert B.aiq_plan_create_status(model(), table(), None, query(agg=B.AIQ_AGG_COUNT_BY_PAYLOAD,
+                                                                  n_group_keys=4)) == B.AIQ_EINVAL
+
+
+def test_table_validation():
+    t = table(); t.list_offsets = 0
+    assert B.aiq_plan_create_status(model(), t, None, query()) == B.AIQ_EINVAL
+    t = table(); t.max_list_len = 0
+    assert B.aiq_plan_create_status(model(), t, None, query()) == B.AIQ_EINVAL
+    t = table(); t.n_rows = -1
+    assert B.aiq_plan_create_status(model(), t, None, query()) == B.AIQ_EINVAL
+
+
+def test_run_rejects_before_enqueue():
+    p = B.aiq_plan_create(model(), table(), None, query())
+    try:
+        need = B.aiq_workspace_size(p)
+        out = B.aiq_out()
+        out.scalars, out.ids, out.ids_cap = FAKE, FAKE, 1000
+        lib = B.load()
+        assert lib.aiq_run(p, FAKE, need - 1, C.byref(out), None, None) == B.AIQ_ENOSPC
+        assert lib.aiq_run(p, None, need, C.byref(out), None, None) == B.AIQ_EINVAL
+        assert lib.aiq_run(None, FAKE, need, C.byref(out), None, None) == B.AIQ_EINVAL
+        out.scalars = 0
+        assert lib.aiq_run(p, FAKE, need, C.byref(out), None, None) == B.AIQ_EINVAL
+        assert lib.aiq_prefill_packed(p, FAKE, FAKE, 0, 10, B.AIQ_LOGITS_LABELS, FAKE, FAKE, 1 << 30, None) == B.AIQ_EINVAL
+        assert lib.aiq_prefill_packed(p, FAKE, FAKE, 2, 10, 9, FAKE, FAKE, 1 << 30, None) == B.AIQ_EINVAL
+        assert lib.aiq_prefill_packed(p, FAKE, FAKE, 2, 10, B.AIQ_LOGITS_LABELS, FAKE, FAKE, 16, None) == B.AIQ_ENOSPC
+    finally:
+        B.aiq_plan_destroy(p)

@@ -196,3 +196,17 @@ def test_zero_output_projections_make_layers_identity(model):
     hf = e / math.sqrt(float(np.mean(e * e)) + spec.norm_eps)
     exp = as_f32(model["lm_head"][[1, 2]]).astype(np.float64) @ hf
     np.testing.assert_allclose(oracle.label_logits(m, [s], (1, 2))[0], exp, rtol=1e-12)
+
+
+def test_empty_sequence_has_zero_logits(model):
+    lg = oracle.label_logits(model, [np.zeros(0, dtype=np.int64)], (1, 2))
+    assert lg.shape == (1, 2) and np.all(lg == 0.0)
+
+
+def test_truncated_stack_matches_zero_layers_closed_form(model):
+    spec = model["spec"]
+    s = _seqs(spec, 1)[0]
+    e = as_f32(model["emb"][s[-1]]).astype(np.float64)
+    hf = e / math.sqrt(float(np.mean(e * e)) + spec.norm_eps)
+    exp = as_f32(model["lm_head"][[1, 2]]).astype(np.float64) @ hf
+    np.testing.assert_allclose(oracle.label_logits(model, [s], (1, 2), n_layers=0)[0], exp, rtol=1e-12)
