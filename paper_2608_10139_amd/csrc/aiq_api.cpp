@@ -133,7 +133,7 @@ aiq_status validate_model(const aiq_model* m) {
 
 struct Layout {
   size_t ctr, mask, blk_cnt, blk_off, sel, payload, lens, label, logits, cu, scan_tmp, packed, hkeys, hvals,
-      bins, desc, rcos, rsin, x, h, qkv, att, ffn, pos, hf, total;
+      bins, desc, rcos, rsin, x, delta, h, qkv, att, ffn, pos, hf, total;
 };
 
 size_t act_bytes(const aiq_plan* p) { return p->bf16 ? 2 : 4; }
@@ -166,6 +166,7 @@ Layout run_layout(const aiq_plan* p) {
   L.rsin = c.take(static_cast<size_t>(p->max_seq) * (p->hd / 2) * 4);
   const size_t T = static_cast<size_t>(p->t_cap);
   L.x = c.take(T * d * 4);
+  L.delta = c.take(T * d * 4);
   L.h = c.take(T * d * ab);
   L.qkv = c.take(T * p->n_qkv * ab);
   L.att = c.take(T * p->d_q * ab);
@@ -190,6 +191,7 @@ Layout prefill_layout(const aiq_plan* p, int64_t max_tokens) {
   L.rcos = c.take(T * (p->hd / 2) * 4);
   L.rsin = c.take(T * (p->hd / 2) * 4);
   L.x = c.take(T * d * 4);
+  L.delta = c.take(T * d * 4);
   L.h = c.take(T * d * ab);
   L.qkv = c.take(T * p->n_qkv * ab);
   L.att = c.take(T * p->d_q * ab);
@@ -247,6 +249,7 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
   const int d = m.d_model;
   const int64_t* m_ptr = desc + D_NTOK;
   float* x = at<float>(ws, L.x);
+  float* delta = at<float>(ws, L.delta);   // output of the last O / down projection, added by the next norm
   void* h = at<void>(ws, L.h);
   void* qkv = at<void>(ws, L.qkv);
   void* att = at<void>(ws, L.att);
@@ -272,8 +275,6 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
     g.hd = p->hd;
     g.C = C;
     g.ldc = ldc;
-    g.X = x;
-    g.ldx = d;
     g.pos = pos;
     g.rope_cos = rcos;
     g.rope_sin = rsin;
@@ -283,7 +284,7 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
   TRACED(tr, AIQ_K_EMBED, launch_embed(desc, cu, packed, m.emb, m.wdtype, d, m.vocab, x, pos, ctr, t_cap, s));
   for (int l = 0; l < p->n_layers; ++l) {
     const aiq_layer& W = p->layers[l];
-    TRACED(tr, AIQ_K_NORM, launch_rmsnorm(desc, x, W.attn_norm, d, eps, h, p->bf16, t_cap, s));
+    TRACED(tr, AIQ_K_NORM, launch_rmsnorm(desc, x, l ? delta : nullptr, W.attn_norm, d, eps, h, p->bf16, t_cap, s));
     TRACED(tr, AIQ_K_GEMM_QKV, gemm(EPI_QKV_ROPE, h, d, p->n_qkv, d, W.wq, W.wk, W.wv, qkv, p->n_qkv));
     if (!p->bf16)
       TRACED(tr, AIQ_K_GEMM_QKV, launch_rope_f32(desc, static_cast<float*>(qkv), p->n_qkv, p->d_q, p->d_kv, p->hd,
@@ -300,18 +301,19 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
     aa.hd = p->hd;
     aa.seq_ub = seq_ub;
     TRACED(tr, AIQ_K_ATTN, p->bf16 ? launch_attention_bf16(aa, s) : launch_attention_f32(aa, s));
-    TRACED(tr, AIQ_K_GEMM_O, gemm(EPI_RESID, att, p->d_q, d, p->d_q, W.wo, nullptr, nullptr, nullptr, 0));
-    TRACED(tr, AIQ_K_NORM, launch_rmsnorm(desc, x, W.ffn_norm, d, eps, h, p->bf16, t_cap, s));
+    TRACED(tr, AIQ_K_GEMM_O, gemm(EPI_STORE_F32, att, p->d_q, d, p->d_q, W.wo, nullptr, nullptr, delta, d));
+    TRACED(tr, AIQ_K_NORM, launch_rmsnorm(desc, x, delta, W.ffn_norm, d, eps, h, p->bf16, t_cap, s));
     if (p->bf16)
       TRACED(tr, AIQ_K_GEMM_UP, gemm(EPI_SWIGLU, h, d, 2 * m.d_ff, d, W.w_gate, W.w_up, nullptr, ffn, m.d_ff));
     else
       TRACED(tr, AIQ_K_GEMM_UP, gemm(EPI_GELU, h, d, m.d_ff, d, W.w_gate, nullptr, nullptr, ffn, m.d_ff));
-    TRACED(tr, AIQ_K_GEMM_DOWN, gemm(EPI_RESID, ffn, m.d_ff, d, m.d_ff, W.w_down, nullptr, nullptr, nullptr, 0));
+    TRACED(tr, AIQ_K_GEMM_DOWN, gemm(EPI_STORE_F32, ffn, m.d_ff, d, m.d_ff, W.w_down, nullptr, nullptr, delta, d));
   }
   HeadArgs ha{};
   ha.desc = desc;
   ha.cu = cu;
   ha.x = x;
+  ha.delta = p->n_layers > 0 ? delta : nullptr;
   ha.g = m.final_norm;
   ha.eps = eps;
   ha.d = d;
@@ -430,7 +432,7 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
     p->max_seq = p->probe.max_list_len + q.n_prefix;
     // default chunk: about 48 GB of per-token activations (a fraction of one
     // MI355X's 288 GB), at most 4M tokens
-    const int64_t per_tok = static_cast<int64_t>(model->d_model) * 4 +
+    const int64_t per_tok = static_cast<int64_t>(model->d_model) * 8 +   // x and delta (fp32)
                             static_cast<int64_t>(model->d_model + p->n_qkv + p->d_q + model->d_ff) *
                                 (p->bf16 ? 2 : 4) + 4;
     const int64_t def_chunk = std::min<int64_t>((int64_t(48) << 30) / per_tok, int64_t(4) << 20);

@@ -112,11 +112,11 @@ hipError_t launch_rope_table(int32_t max_pos, int32_t half, double theta, int32_
 hipError_t launch_embed(const int64_t* desc, const int64_t* cu, const int32_t* packed,
                         const void* emb, int32_t wdtype, int32_t d, int32_t vocab, float* x, int32_t* pos,
                         int64_t* ctr, int64_t t_cap, hipStream_t s);
-hipError_t launch_rmsnorm(const int64_t* desc, const float* x, const float* g, int32_t d,
+// x += delta (when delta is non-null, written back), then out = RMSNorm(x) * g
+hipError_t launch_rmsnorm(const int64_t* desc, float* x, const float* delta, const float* g, int32_t d,
                           float eps, void* out, int32_t out_bf16, int64_t t_cap, hipStream_t s);
 
-enum Epi : int { EPI_STORE_F32 = 0, EPI_QKV_ROPE = 1, EPI_RESID = 2, EPI_SWIGLU = 3, EPI_GELU = 4,
-                 EPI_STORE_ACT = 5 };
+enum Epi : int { EPI_STORE_F32 = 0, EPI_QKV_ROPE = 1, EPI_SWIGLU = 3, EPI_GELU = 4, EPI_STORE_ACT = 5 };
 
 struct GemmArgs {
   const void* A;             // [M, K] activations (bf16 or f32), row stride lda
@@ -131,8 +131,6 @@ struct GemmArgs {
   int32_t hd;
   void* C;                   // output
   int64_t ldc;
-  float* X;                  // residual stream [M, ldx] (EPI_RESID)
-  int64_t ldx;
   const int32_t* pos;        // [M] positions (EPI_QKV_ROPE)
   const float* rope_cos;     // [max_pos, hd/2]
   const float* rope_sin;
@@ -161,6 +159,7 @@ struct HeadArgs {
   const int64_t* desc;
   const int64_t* cu;
   const float* x;            // residual [T, d]
+  const float* delta;        // pending output of the last projection [T, d], or NULL
   const float* g;            // final norm gains
   float eps;
   int32_t d;

@@ -2,14 +2,12 @@
 // epilogues (rotary embedding on q/k, SwiGLU, GELU, residual add).
 //
 // bf16 path (gfx950 MFMA): 256 x 256 output tile per 512-thread workgroup,
-// K stepped by 64 through a double-buffered LDS stage (2 x 64 KB).  Eight
-// waves in a 2 x 4 grid each own a 128 x 64 sub-tile = 8 x 4 blocks of
-// v_mfma_f32_16x16x32_bf16.  The weight block is the MFMA's first operand and
-// the activation block its second, so every lane ends up holding four
-// consecutive output columns of one row: stores are 8- or 16-byte vectors and
-// the column pairs the epilogues need (rotary halves, gate/up) sit in the
-// same lane.  LDS rows are 128 bytes; the 16-byte chunk index is XORed with
-// (row & 7) so the 16 rows a fragment read touches fall in distinct banks.
+// K stepped by 64 through two LDS stages (2 x 64 KB) filled by 16-byte
+// direct-to-LDS loads, the next stage in flight while the current one feeds
+// the MFMAs.  Eight waves in a 2 x 4 grid each own a 128 x 64 sub-tile =
+// 4 x 2 blocks of v_mfma_f32_32x32x16_bf16 (the 32x32 form sustains about
+// twice the rate of the 16x16x32 form on gfx950).  The next tile's first
+// stage is fetched while the epilogue of the current one runs.
 //
 // M (tokens in the chunk) is read from device memory; the grid is persistent
 // (one workgroup per CU) and walks the tiles, so an empty chunk costs one
@@ -78,10 +76,11 @@ __device__ __forceinline__ const T* b_row(const GemmArgs& a, int n) {
     n -= a.n_kv;
     return static_cast<const T*>(a.B2) + static_cast<int64_t>(n) * a.K;
   } else if (EPI == EPI_SWIGLU) {
-    // interleave 16-row groups: gate rows 16b.., up rows 16b.., ...
-    const int b16 = n >> 4, r = n & 15;
-    const int row = (b16 >> 1) * 16 + r;
-    return static_cast<const T*>((b16 & 1) ? a.B1 : a.B0) + static_cast<int64_t>(row) * a.K;
+    // interleave 32-row groups: gate rows 32b.., up rows 32b.., ... so each
+    // 64-column wave slice holds 32 gate columns and the 32 matching up columns
+    const int b32 = n >> 5, r = n & 31;
+    const int row = (b32 >> 1) * 32 + r;
+    return static_cast<const T*>((b32 & 1) ? a.B1 : a.B0) + static_cast<int64_t>(row) * a.K;
   } else {
     return static_cast<const T*>(a.B0) + static_cast<int64_t>(n) * a.K;
   }
@@ -89,185 +88,284 @@ __device__ __forceinline__ const T* b_row(const GemmArgs& a, int n) {
 
 // ======================================================================= bf16 MFMA
 constexpr int GM = 256, GN = 256, GK = 64, GT = 512;
-constexpr int STAGE = (GM + GN) * GK;   // bf16 elements per LDS stage
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// Accumulator layout (v_mfma_f32_32x32x16_bf16, activations as the first
+// operand): acc[i][j][4g + e] holds C[m][n] with
+//   m = m0 + wm*128 + i*32 + 8g + 4*(lane/32) + e,   n = n0 + wn*64 + j*32 + lane%32.
+// A lane owns one column of each 32-wide block, so the rotary pair (j = 0
+// lower half, j = 1 upper half of a head) and the SwiGLU pair (j = 0 gate,
+// j = 1 up) sit in the same lane.
+//
+// Output goes through LDS: each wave owns an 8 KB slice of the idle LDS stage,
+// writes a slab of its sub-tile there in row-major order, then stores whole
+// 16-byte pieces of rows to global memory (8 store instructions per slab
+// instead of one 2-byte store per value).
+
+__device__ __forceinline__ float silu_fast(float g) {
+  return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g));
+}
+
+// Writes a slab of `rows` x `cols` elements of type T from the wave's LDS slice
+// (row-major, `cols` per row) to C[m][col_of(c)] for rows m < M, 16 B per lane.
+template <typename T, typename ColMap>
+__device__ __forceinline__ void flush_slab(const T* slab, int rows, int cols, T* C, int64_t ldc, int64_t m_first,
+                                           int64_t M, int lane, ColMap col_of) {
+  constexpr int PER = 16 / sizeof(T);               // elements per 16-byte piece
+  const int pieces_per_row = cols / PER;
+  const int total = rows * pieces_per_row;
+  for (int p = lane; p < total; p += 64) {
+    const int r = p / pieces_per_row, c = (p % pieces_per_row) * PER;
+    const int64_t m = m_first + r;
+    if (m < M)
+      *reinterpret_cast<uint4*>(C + m * ldc + col_of(c)) = *reinterpret_cast<const uint4*>(slab + r * cols + c);
+  }
+}
 
 template <int EPI>
-__device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x4 (&acc)[4][8], int64_t m0, int n0,
-                                              int64_t M, int wm, int wn, int lane) {
-  const int c4 = 4 * (lane >> 4);
+__device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4][2], int64_t m0, int n0,
+                                              int64_t M, int wm, int wn, int lane, uint16_t* slice) {
+  const int l32 = lane & 31, hi = lane >> 5;
   const int nw = n0 + wn * 64;   // first GEMM column of this wave
+  const int64_t mw = m0 + wm * 128;   // first row of this wave's sub-tile
+  if (EPI == EPI_STORE_F32) {
+    // fp32: four slabs of 32 rows x 64 columns (8 KB each)
+    float* slab = reinterpret_cast<float*>(slice);
+    float* C = static_cast<float*>(a.C);
 #pragma unroll
-  for (int mi = 0; mi < 8; ++mi) {
-    const int64_t m = m0 + wm * 128 + mi * 16 + (lane & 15);
-    if (m >= M) continue;
-    if (EPI == EPI_STORE_F32) {
-      float* C = static_cast<float*>(a.C) + m * a.ldc;
+    for (int i = 0; i < 4; ++i) {
 #pragma unroll
-      for (int ni = 0; ni < 4; ++ni) {
-        const f32x4 v = acc[ni][mi];
-        *reinterpret_cast<float4*>(C + nw + ni * 16 + c4) = make_float4(v[0], v[1], v[2], v[3]);
-      }
-    } else if (EPI == EPI_STORE_ACT) {
-      uint16_t* C = static_cast<uint16_t*>(a.C) + m * a.ldc;
+      for (int g = 0; g < 4; ++g)
 #pragma unroll
-      for (int ni = 0; ni < 4; ++ni) {
-        const f32x4 v = acc[ni][mi];
-        *reinterpret_cast<uint2*>(C + nw + ni * 16 + c4) = pack_bf16x4(v[0], v[1], v[2], v[3]);
-      }
-    } else if (EPI == EPI_RESID) {
-      float* X = a.X + m * a.ldx;
-#pragma unroll
-      for (int ni = 0; ni < 4; ++ni) {
-        float4* px = reinterpret_cast<float4*>(X + nw + ni * 16 + c4);
-        float4 x = *px;
-        const f32x4 v = acc[ni][mi];
-        x.x += v[0]; x.y += v[1]; x.z += v[2]; x.w += v[3];
-        *px = x;
-      }
-    } else if (EPI == EPI_SWIGLU) {
-      uint16_t* C = static_cast<uint16_t*>(a.C) + m * a.ldc;
-#pragma unroll
-      for (int p = 0; p < 2; ++p) {
-        const f32x4 g = acc[2 * p][mi], u = acc[2 * p + 1][mi];
-        const int col = nw / 2 + p * 16 + c4;
-        *reinterpret_cast<uint2*>(C + col) =
-            pack_bf16x4(silu(g[0]) * u[0], silu(g[1]) * u[1], silu(g[2]) * u[2], silu(g[3]) * u[3]);
-      }
-    } else if (EPI == EPI_QKV_ROPE) {
-      uint16_t* C = static_cast<uint16_t*>(a.C) + m * a.ldc;
-      if (nw >= a.n_q + a.n_kv) {  // v: stored as is
-#pragma unroll
-        for (int ni = 0; ni < 4; ++ni) {
-          const f32x4 v = acc[ni][mi];
-          *reinterpret_cast<uint2*>(C + nw + ni * 16 + c4) = pack_bf16x4(v[0], v[1], v[2], v[3]);
+        for (int e = 0; e < 4; ++e) {
+          const int r = g * 8 + hi * 4 + e;
+          slab[r * 64 + l32] = acc[i][0][4 * g + e];
+          slab[r * 64 + 32 + l32] = acc[i][1][4 * g + e];
         }
-      } else {
-        const int sbase = nw < a.n_q ? 0 : a.n_q;
-        const int c = nw - sbase;
-        const int head = c / a.hd;
-        const int hh = (c % a.hd) >> 6;   // 0 except the second half-wave of a 128-dim head
-        const int half = a.hd >> 1;
-        const int p = a.pos[m];
-        const float* cs = a.rope_cos + static_cast<int64_t>(p) * half;
-        const float* sn = a.rope_sin + static_cast<int64_t>(p) * half;
-        uint16_t* Ch = C + sbase + head * a.hd;
-#pragma unroll
-        for (int ni = 0; ni < 2; ++ni) {
-          const int dlo = hh * 32 + ni * 16 + c4;   // lower-half dim of this lane's 4 columns
-          const f32x4 x1 = acc[ni][mi], x2 = acc[ni + 2][mi];
-          const float4 cv = *reinterpret_cast<const float4*>(cs + dlo);
-          const float4 sv = *reinterpret_cast<const float4*>(sn + dlo);
-          *reinterpret_cast<uint2*>(Ch + dlo) =
-              pack_bf16x4(x1[0] * cv.x - x2[0] * sv.x, x1[1] * cv.y - x2[1] * sv.y,
-                          x1[2] * cv.z - x2[2] * sv.z, x1[3] * cv.w - x2[3] * sv.w);
-          *reinterpret_cast<uint2*>(Ch + dlo + half) =
-              pack_bf16x4(x2[0] * cv.x + x1[0] * sv.x, x2[1] * cv.y + x1[1] * sv.y,
-                          x2[2] * cv.z + x1[2] * sv.z, x2[3] * cv.w + x1[3] * sv.w);
-        }
-      }
+      flush_slab<float>(slab, 32, 64, C, a.ldc, mw + i * 32, M, lane, [&](int c) { return nw + c; });
     }
+    return;
+  }
+  // bf16 outputs: slab of 64 rows (two i-blocks) x 64 (or 32 for SwiGLU) columns
+  uint16_t* C = static_cast<uint16_t*>(a.C);
+  const bool is_v = EPI == EPI_QKV_ROPE && nw >= a.n_q + a.n_kv;
+  int sbase = 0, head = 0, hh = 0, half = 0;
+  if (EPI == EPI_QKV_ROPE && !is_v) {
+    sbase = nw < a.n_q ? 0 : a.n_q;
+    const int c = nw - sbase;
+    head = c / a.hd;
+    hh = (c % a.hd) >> 6;   // 0 except the second half-wave of a 128-dim head
+    half = a.hd >> 1;
+  }
+  constexpr int COLS = EPI == EPI_SWIGLU ? 32 : 64;
+#pragma unroll
+  for (int h2 = 0; h2 < 2; ++h2) {
+#pragma unroll
+    for (int ii = 0; ii < 2; ++ii) {
+      const int i = h2 * 2 + ii;
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = ii * 32 + g * 8 + hi * 4 + e;   // row inside the 64-row slab
+          const float v0 = acc[i][0][4 * g + e], v1 = acc[i][1][4 * g + e];
+          if (EPI == EPI_SWIGLU) {
+            slice[r * 32 + l32] = f2bf(silu_fast(v0) * v1);
+          } else if (EPI == EPI_QKV_ROPE && !is_v) {
+            int64_t m = mw + i * 32 + g * 8 + hi * 4 + e;
+            if (m > M - 1) m = M - 1;   // rows past M are computed but never stored
+            const int dlo = hh * 32 + l32;
+            const int64_t ti = static_cast<int64_t>(a.pos[m]) * half + dlo;
+            const float cs = a.rope_cos[ti], sn = a.rope_sin[ti];
+            slice[r * 64 + l32] = f2bf(v0 * cs - v1 * sn);        // lower half dims
+            slice[r * 64 + 32 + l32] = f2bf(v1 * cs + v0 * sn);   // upper half dims
+          } else {
+            slice[r * 64 + l32] = f2bf(v0);
+            slice[r * 64 + 32 + l32] = f2bf(v1);
+          }
+        }
+    }
+    const int64_t m_first = mw + h2 * 64;
+    if (EPI == EPI_SWIGLU) {
+      flush_slab<uint16_t>(slice, 64, 32, C, a.ldc, m_first, M, lane, [&](int c) { return nw / 2 + c; });
+    } else if (EPI == EPI_QKV_ROPE && !is_v) {
+      // slab columns 0..31: lower-half dims hh*32.., 32..63: the matching upper-half dims
+      const int base = sbase + head * a.hd + hh * 32;
+      flush_slab<uint16_t>(slice, 64, 64, C, a.ldc, m_first, M, lane,
+                           [&](int c) { return base + (c < 32 ? c : half + c - 32); });
+    } else {
+      flush_slab<uint16_t>(slice, 64, 64, C, a.ldc, m_first, M, lane, [&](int c) { return nw + c; });
+    }
+  }
+}
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+// LDS stage: [256 rows][64 bf16], 128-byte rows of eight 16-byte chunks.  The
+// chunk index is XORed with bits 1..3 of the row: 16 consecutive rows then
+// cover all 64 banks once (row parity already picks the bank half).
+__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
+
+// One 64-deep k-step of the wave's 128 x 64 sub-tile from one LDS stage.
+// Fragments of the next 16-deep sub-step are read while the MFMAs of the
+// current one run (two register sets), so LDS latency hides behind MFMA work.
+__device__ __forceinline__ void load_frags(const uint16_t* As, const uint16_t* Bs, int s, int wm, int wn, int lane,
+                                           bf16x8 (&af)[4], bf16x8 (&bw)[2]) {
+  const int r32 = lane & 31;
+  const int sw = swz(r32, 2 * s + (lane >> 5)) << 3;   // same for every 32-row block
+#pragma unroll
+  for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const bf16x8*>(As + (wm * 128 + i * 32 + r32) * GK + sw);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) bw[j] = *reinterpret_cast<const bf16x8*>(Bs + (wn * 64 + j * 32 + r32) * GK + sw);
+}
+
+__device__ __forceinline__ void mma_stage(const uint16_t* As, const uint16_t* Bs, f32x16 (&acc)[4][2], int wm,
+                                          int wn, int lane) {
+  bf16x8 af[2][4], bw[2][2];
+  load_frags(As, Bs, 0, wm, wn, lane, af[0], bw[0]);
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    const int cur = s & 1;
+    if (s < 3) load_frags(As, Bs, s + 1, wm, wn, lane, af[cur ^ 1], bw[cur ^ 1]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bw[cur][j], acc[i][j], 0, 0, 0);
+    if (s < 3) {
+      // interleave: one MFMA, one LDS read, ... then the remaining MFMAs
+      for (int q = 0; q < 6; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    }
+  }
+}
+
+// Global -> LDS tile copy with the 16-byte direct-to-LDS load: a wave's
+// instruction fills 1 KB (8 rows) at consecutive lane slots, so lane l
+// fetches the global chunk that belongs at row 8c + l/8, slot l%8.
+__device__ __forceinline__ void dma_stage(uint16_t* sA, uint16_t* sB, const uint16_t* const (&ga)[4],
+                                          const uint16_t* const (&gb)[4], int k0, int w) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int c = i * 8 + w;
+    __builtin_amdgcn_global_load_lds(static_cast<const void*>(ga[i] + k0), (lds_ptr_t)(sA + c * 512), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(static_cast<const void*>(gb[i] + k0), (lds_ptr_t)(sB + c * 512), 16, 0, 0);
+  }
+}
+
+template <int EPI>
+__device__ __forceinline__ void tile_sources(const GemmArgs& a, const uint16_t* A, int64_t M, int64_t m0, int n0,
+                                             int w, int lane, const uint16_t* (&ga)[4], const uint16_t* (&gb)[4]) {
+  const int lr = lane >> 3;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = (i * 8 + w) * 8 + lr;
+    const int lc = swz(row, lane & 7);   // logical chunk stored in this lane's slot
+    int64_t mr = m0 + row;
+    if (mr > M - 1) mr = M - 1;
+    ga[i] = A + mr * a.lda + lc * 8;
+    gb[i] = b_row<EPI, uint16_t>(a, n0 + row) + lc * 8;
   }
 }
 
 template <int EPI>
 __global__ __launch_bounds__(GT) void k_gemm_bf16(GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * STAGE];
+  // two stages in distinct arrays: the compiler can then tell the in-flight
+  // loads into one stage from the reads of the other and only waits at the
+  // barrier that ends the stage
+  __shared__ __attribute__((aligned(16))) uint16_t sA0[GM * GK];
+  __shared__ __attribute__((aligned(16))) uint16_t sB0[GN * GK];
+  __shared__ __attribute__((aligned(16))) uint16_t sA1[GM * GK];
+  __shared__ __attribute__((aligned(16))) uint16_t sB1[GN * GK];
   const int64_t M = *a.m_ptr;
   if (M <= 0) return;
   const int tiles_n = a.N / GN;
-  const int64_t n_tiles = ((M + GM - 1) / GM) * tiles_n;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6, wm = w >> 2, wn = w & 3;
   const int nk = a.K / GK;
   const uint16_t* A = static_cast<const uint16_t*>(a.A);
 
-  for (int64_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
-    const int64_t m0 = (tile / tiles_n) * GM;
-    const int n0 = static_cast<int>(tile % tiles_n) * GN;
-    const uint16_t* ap[4];
-    const uint16_t* bp[4];
-    int so[4];
+  // XCD-aware order: workgroups are dispatched round-robin over the 8 XCDs,
+  // so workgroup b runs on XCD b % 8.  XCD x owns the M-tile rows
+  // tm = x, x + 8, x + 16, ...; inside an XCD the tiles go in groups of
+  // GROUP_M of its rows, column by column, so the 32 workgroups resident on
+  // one XCD share a few activation row-panels and a few weight column-panels
+  // in that XCD's L2 instead of streaming 32 distinct panels.
+  constexpr int GROUP_M = 4;
+  const int64_t tiles_m = (M + GM - 1) / GM;
+  const int xcd = blockIdx.x & 7;
+  const int64_t per_xcd = gridDim.x >> 3;   // grid is a multiple of 8
+  const int64_t rows_x = tiles_m > xcd ? (tiles_m - xcd + 7) / 8 : 0;
+  const int64_t count_x = rows_x * tiles_n;
+  auto tile_mn = [&](int64_t q, int64_t& m0, int& n0) {
+    const int64_t per_group = static_cast<int64_t>(GROUP_M) * tiles_n;
+    const int64_t grp = q / per_group, within = q % per_group;
+    const int64_t rows_here = (rows_x - grp * GROUP_M) < GROUP_M ? (rows_x - grp * GROUP_M) : GROUP_M;
+    const int64_t lr = grp * GROUP_M + within % rows_here;
+    m0 = (lr * 8 + xcd) * GM;
+    n0 = static_cast<int>(within / rows_here) * GN;
+  };
+  int64_t q = blockIdx.x >> 3;
+  if (q >= count_x) return;
+  const uint16_t* ga[4];
+  const uint16_t* gb[4];
+  {
+    int64_t m0;
+    int n0;
+    tile_mn(q, m0, n0);
+    tile_sources<EPI>(a, A, M, m0, n0, w, lane, ga, gb);
+  }
+  dma_stage(sA0, sB0, ga, gb, 0, w);
+  for (; q < count_x; q += per_xcd) {
+    int64_t m0;
+    int n0;
+    tile_mn(q, m0, n0);
+    f32x16 acc[4][2];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int id = i * GT + t, row = id >> 3, ch = id & 7;
-      int64_t mr = m0 + row;
-      if (mr > M - 1) mr = M - 1;
-      ap[i] = A + mr * a.lda + ch * 8;
-      bp[i] = b_row<EPI, uint16_t>(a, n0 + row) + ch * 8;
-      so[i] = row * GK + ((ch ^ (row & 7)) << 3);
-    }
-    uint4 ra[4], rb[4];
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      ra[i] = *reinterpret_cast<const uint4*>(ap[i]);
-      rb[i] = *reinterpret_cast<const uint4*>(bp[i]);
-    }
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      *reinterpret_cast<uint4*>(lds + so[i]) = ra[i];
-      *reinterpret_cast<uint4*>(lds + GM * GK + so[i]) = rb[i];
-    }
-    __syncthreads();
-
-    f32x4 acc[4][8];
-#pragma unroll
-    for (int ni = 0; ni < 4; ++ni)
-#pragma unroll
-      for (int mi = 0; mi < 8; ++mi) acc[ni][mi] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    for (int kt = 0; kt < nk; ++kt) {
-      const int st = kt & 1;
-      const uint16_t* As = lds + st * STAGE;
-      const uint16_t* Bs = As + GM * GK;
-      const bool more = kt + 1 < nk;
-      if (more) {
-        const int ko = (kt + 1) * GK;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          ra[i] = *reinterpret_cast<const uint4*>(ap[i] + ko);
-          rb[i] = *reinterpret_cast<const uint4*>(bp[i] + ko);
-        }
-      }
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        const int ch = kk * 4 + (lane >> 4);
-        const int sw = (ch ^ (lane & 7)) << 3;   // row & 7 == lane & 7 for every fragment row
-        bf16x8 af[8], bw[4];
-#pragma unroll
-        for (int mi = 0; mi < 8; ++mi)
-          af[mi] = *reinterpret_cast<const bf16x8*>(As + (wm * 128 + mi * 16 + (lane & 15)) * GK + sw);
-#pragma unroll
-        for (int ni = 0; ni < 4; ++ni)
-          bw[ni] = *reinterpret_cast<const bf16x8*>(Bs + (wn * 64 + ni * 16 + (lane & 15)) * GK + sw);
-#pragma unroll
-        for (int ni = 0; ni < 4; ++ni)
-#pragma unroll
-          for (int mi = 0; mi < 8; ++mi)
-            acc[ni][mi] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bw[ni], af[mi], acc[ni][mi], 0, 0, 0);
-      }
-      if (more) {
-        uint16_t* As2 = lds + (st ^ 1) * STAGE;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          *reinterpret_cast<uint4*>(As2 + so[i]) = ra[i];
-          *reinterpret_cast<uint4*>(As2 + GM * GK + so[i]) = rb[i];
-        }
-      }
+        for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
+    __syncthreads();   // stage 0 of this tile has landed
+    for (int kt = 0; kt < nk; kt += 2) {
+      if (kt + 1 < nk) dma_stage(sA1, sB1, ga, gb, (kt + 1) * GK, w);
+      mma_stage(sA0, sB0, acc, wm, wn, lane);
       __syncthreads();
+      if (kt + 1 < nk) {
+        if (kt + 2 < nk) dma_stage(sA0, sB0, ga, gb, (kt + 2) * GK, w);
+        mma_stage(sA1, sB1, acc, wm, wn, lane);
+        __syncthreads();
+      }
     }
-    epilogue_bf16<EPI>(a, acc, m0, n0, M, wm, wn, lane);
+    // stage 0 is free: start the next tile's first k-step under the epilogue
+    if (q + per_xcd < count_x) {
+      int64_t m1;
+      int n1;
+      tile_mn(q + per_xcd, m1, n1);
+      tile_sources<EPI>(a, A, M, m1, n1, w, lane, ga, gb);
+      dma_stage(sA0, sB0, ga, gb, 0, w);
+    }
+    // each wave stages its output in its own 8 KB slice of stage 1, which is
+    // idle until the next tile's first barrier
+    uint16_t* slice = (w < 4 ? sA1 : sB1) + (w & 3) * 4096;
+    epilogue_bf16<EPI>(a, acc, m0, n0, M, wm, wn, lane, slice);
   }
 }
 
 hipError_t launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t s) {
+  // one workgroup per CU, rounded to whole XCD groups; fewer for small problems
   const int64_t tiles = ((a.m_ub + GM - 1) / GM) * (a.N / GN);
   int64_t g = num_cus();
   if (tiles < g) g = tiles;
-  if (g < 1) g = 1;
+  g = (g + 7) / 8 * 8;
   const dim3 grid(static_cast<unsigned>(g)), block(GT);
   switch (epi) {
     case EPI_STORE_F32: hipLaunchKernelGGL(k_gemm_bf16<EPI_STORE_F32>, grid, block, 0, s, a); break;
     case EPI_STORE_ACT: hipLaunchKernelGGL(k_gemm_bf16<EPI_STORE_ACT>, grid, block, 0, s, a); break;
-    case EPI_RESID: hipLaunchKernelGGL(k_gemm_bf16<EPI_RESID>, grid, block, 0, s, a); break;
     case EPI_SWIGLU: hipLaunchKernelGGL(k_gemm_bf16<EPI_SWIGLU>, grid, block, 0, s, a); break;
     case EPI_QKV_ROPE: hipLaunchKernelGGL(k_gemm_bf16<EPI_QKV_ROPE>, grid, block, 0, s, a); break;
     default: return hipErrorInvalidValue;
@@ -323,12 +421,7 @@ __global__ __launch_bounds__(FT) void k_gemm_f32(GemmArgs a) {
     for (int i = 0; i < 4; ++i) {
       const int64_t m = m0 + ty * 4 + i;
       if (m >= M) continue;
-      if (EPI == EPI_RESID) {
-        float4* px = reinterpret_cast<float4*>(a.X + m * a.ldx + n);
-        float4 x = *px;
-        x.x += acc[i][0]; x.y += acc[i][1]; x.z += acc[i][2]; x.w += acc[i][3];
-        *px = x;
-      } else if (EPI == EPI_GELU) {
+      if (EPI == EPI_GELU) {
         *reinterpret_cast<float4*>(static_cast<float*>(a.C) + m * a.ldc + n) =
             make_float4(gelu_erf(acc[i][0]), gelu_erf(acc[i][1]), gelu_erf(acc[i][2]), gelu_erf(acc[i][3]));
       } else {  // plain fp32 store (QKV columns in natural order; rotary applied afterwards)
@@ -349,7 +442,6 @@ hipError_t launch_gemm_f32(int epi, const GemmArgs& a, hipStream_t s) {
     case EPI_STORE_F32:
     case EPI_STORE_ACT: hipLaunchKernelGGL(k_gemm_f32<EPI_STORE_F32>, grid, block, 0, s, a); break;
     case EPI_QKV_ROPE: hipLaunchKernelGGL(k_gemm_f32<EPI_QKV_ROPE>, grid, block, 0, s, a); break;
-    case EPI_RESID: hipLaunchKernelGGL(k_gemm_f32<EPI_RESID>, grid, block, 0, s, a); break;
     case EPI_GELU: hipLaunchKernelGGL(k_gemm_f32<EPI_GELU>, grid, block, 0, s, a); break;
     default: return hipErrorInvalidValue;
   }

@@ -30,49 +30,65 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
 
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
 
-// ------------------------------------------------------------------ RMSNorm
-// One wave per row: out = x / sqrt(mean(x^2) + eps) * g.  The sum of squares
-// is reduced in a fixed order inside the row, so a row's result does not
-// depend on which other rows share the launch.
-__global__ __launch_bounds__(256) void k_rmsnorm(const int64_t* desc, const float* x, const float* g, int32_t d,
-                                                 float eps, void* out, int32_t out_bf16) {
+// ------------------------------------------------------------------ residual add + RMSNorm
+// One wave per row.  With a pending projection output `delta` the residual
+// stream is updated first (x += delta, fp32, written back), then
+// out = x / sqrt(mean(x^2) + eps) * g.  The sum of squares is reduced in a
+// fixed order inside the row, so a row's result does not depend on which
+// other rows share the launch.
+__global__ __launch_bounds__(256) void k_rmsnorm(const int64_t* desc, float* x, const float* delta, const float* g,
+                                                 int32_t d, float eps, void* out, int32_t out_bf16) {
   const int64_t nt = desc[D_NTOK];
   const int lane = threadIdx.x & 63;
   const int64_t wave = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6;
   const int64_t n_waves = ((int64_t)gridDim.x * blockDim.x) >> 6;
   const int nv = d >> 2;
+  constexpr int MAXV = 16;   // d <= 64 lanes * 16 float4 = 4096
   for (int64_t t = wave; t < nt; t += n_waves) {
-    const float4* xr = reinterpret_cast<const float4*>(x + t * d);
+    float4* xr = reinterpret_cast<float4*>(x + t * d);
+    float4 v[MAXV];
     float ss = 0.f;
-    for (int v = lane; v < nv; v += 64) {
-      const float4 a = xr[v];
-      ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
+#pragma unroll
+    for (int j = 0; j < MAXV; ++j) {
+      const int c = lane + 64 * j;
+      if (c < nv) {
+        float4 a = xr[c];
+        if (delta) {
+          const float4 b = reinterpret_cast<const float4*>(delta + t * d)[c];
+          a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w;
+          xr[c] = a;
+        }
+        v[j] = a;
+        ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
+      }
     }
     ss = wave_sum(ss);
     const float r = 1.0f / sqrtf(ss / static_cast<float>(d) + eps);
     const float4* gr = reinterpret_cast<const float4*>(g);
-    if (out_bf16) {
-      uint2* o = reinterpret_cast<uint2*>(static_cast<uint16_t*>(out) + t * d);
-      for (int v = lane; v < nv; v += 64) {
-        const float4 a = xr[v], w = gr[v];
-        uint2 p;
-        p.x = f2bf(a.x * r * w.x) | (static_cast<uint32_t>(f2bf(a.y * r * w.y)) << 16);
-        p.y = f2bf(a.z * r * w.z) | (static_cast<uint32_t>(f2bf(a.w * r * w.w)) << 16);
-        o[v] = p;
-      }
-    } else {
-      float4* o = reinterpret_cast<float4*>(static_cast<float*>(out) + t * d);
-      for (int v = lane; v < nv; v += 64) {
-        const float4 a = xr[v], w = gr[v];
-        o[v] = make_float4(a.x * r * w.x, a.y * r * w.y, a.z * r * w.z, a.w * r * w.w);
+#pragma unroll
+    for (int j = 0; j < MAXV; ++j) {
+      const int c = lane + 64 * j;
+      if (c < nv) {
+        const float4 a = v[j], w = gr[c];
+        if (out_bf16) {
+          uint2 p;
+          p.x = f2bf(a.x * r * w.x) | (static_cast<uint32_t>(f2bf(a.y * r * w.y)) << 16);
+          p.y = f2bf(a.z * r * w.z) | (static_cast<uint32_t>(f2bf(a.w * r * w.w)) << 16);
+          reinterpret_cast<uint2*>(static_cast<uint16_t*>(out) + t * d)[c] = p;
+        } else {
+          reinterpret_cast<float4*>(static_cast<float*>(out) + t * d)[c] =
+              make_float4(a.x * r * w.x, a.y * r * w.y, a.z * r * w.z, a.w * r * w.w);
+        }
       }
     }
   }
 }
 
-hipError_t launch_rmsnorm(const int64_t* desc, const float* x, const float* g, int32_t d,
+hipError_t launch_rmsnorm(const int64_t* desc, float* x, const float* delta, const float* g, int32_t d,
                           float eps, void* out, int32_t out_bf16, int64_t t_cap, hipStream_t s) {
-  hipLaunchKernelGGL(k_rmsnorm, dim3(grid_for(t_cap, 4, 4096)), dim3(256), 0, s, desc, x, g, d, eps, out, out_bf16);
+  if (d > 64 * 4 * 16) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_rmsnorm, dim3(grid_for(t_cap, 4, 4096)), dim3(256), 0, s, desc, x, delta, g, d, eps, out,
+                     out_bf16);
   return hipGetLastError();
 }
 
@@ -90,8 +106,10 @@ __global__ __launch_bounds__(256) void k_head(HeadArgs a) {
     const bool empty = a.cu[gi + 1] == a.cu[gi];   // no token: every logit is 0
     const int64_t last = empty ? 0 : a.cu[gi + 1] - 1 - tb;
     const float* xr = a.x + last * d;
+    const float* dr = a.delta ? a.delta + last * d : nullptr;   // last layer's pending output
+    auto xv = [&](int c) { return dr ? xr[c] + dr[c] : xr[c]; };
     float ss = 0.f;
-    for (int c = lane; c < d; c += 64) ss += xr[c] * xr[c];
+    for (int c = lane; c < d; c += 64) ss += xv(c) * xv(c);
     ss = wave_sum(ss);
     const float r = empty ? 0.f : 1.0f / sqrtf(ss / static_cast<float>(d) + a.eps);
     float lg[AIQ_MAX_LABELS];
@@ -99,20 +117,20 @@ __global__ __launch_bounds__(256) void k_head(HeadArgs a) {
       float acc = 0.f;
       if (a.wdtype == AIQ_BF16) {
         const uint16_t* w = static_cast<const uint16_t*>(a.lm_head) + static_cast<int64_t>(a.labels[k]) * d;
-        for (int c = lane; c < d; c += 64) acc += (xr[c] * r * a.g[c]) * bf2f(w[c]);
+        for (int c = lane; c < d; c += 64) acc += (xv(c) * r * a.g[c]) * bf2f(w[c]);
       } else {
         const float* w = static_cast<const float*>(a.lm_head) + static_cast<int64_t>(a.labels[k]) * d;
-        for (int c = lane; c < d; c += 64) acc += (xr[c] * r * a.g[c]) * w[c];
+        for (int c = lane; c < d; c += 64) acc += (xv(c) * r * a.g[c]) * w[c];
       }
       lg[k] = wave_sum(acc);
     }
     if (a.hf_out) {
       if (a.hf_bf16) {
         uint16_t* o = static_cast<uint16_t*>(a.hf_out) + i * d;
-        for (int c = lane; c < d; c += 64) o[c] = f2bf(xr[c] * r * a.g[c]);
+        for (int c = lane; c < d; c += 64) o[c] = f2bf(xv(c) * r * a.g[c]);
       } else {
         float* o = static_cast<float*>(a.hf_out) + i * d;
-        for (int c = lane; c < d; c += 64) o[c] = xr[c] * r * a.g[c];
+        for (int c = lane; c < d; c += 64) o[c] = xv(c) * r * a.g[c];
       }
     }
     if (lane == 0) {
