@@ -198,6 +198,9 @@ def main(argv=None) -> int:
     ap.add_argument("--cpu-rows", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-split", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB (3 times): the reference "
+                         "for scaling HBM traffic counters")
     a = ap.parse_args(argv)
     if a.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {a.gpus}); the pipeline is single-GPU "
@@ -205,6 +208,15 @@ def main(argv=None) -> int:
         return 2
 
     import torch
+    if a.calibrate_copy:
+        n = a.calibrate_copy << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": n, "repeats": 3}), flush=True)
+        return 0
     from paper_2608_10139_amd import binding as B
     from paper_2608_10139_amd.device import DeviceModel, DeviceQuery
     from synth import WORKLOADS

@@ -133,7 +133,7 @@ aiq_status validate_model(const aiq_model* m) {
 
 struct Layout {
   size_t ctr, mask, blk_cnt, blk_off, sel, payload, lens, label, logits, cu, scan_tmp, packed, hkeys, hvals,
-      bins, desc, rcos, rsin, x, delta, h, qkv, att, ffn, pos, hf, total;
+      bins, desc, rcos, rsin, rrev, x, delta, h, qkv, att, ffn, pos, hf, total;
 };
 
 size_t act_bytes(const aiq_plan* p) { return p->bf16 ? 2 : 4; }
@@ -164,6 +164,7 @@ Layout run_layout(const aiq_plan* p) {
   L.desc = c.take(static_cast<size_t>(p->n_chunks) * D_STRIDE * 8);
   L.rcos = c.take(static_cast<size_t>(p->max_seq) * (p->hd / 2) * 4);
   L.rsin = c.take(static_cast<size_t>(p->max_seq) * (p->hd / 2) * 4);
+  L.rrev = c.take(static_cast<size_t>(p->hd / 2) * 4);
   const size_t T = static_cast<size_t>(p->t_cap);
   L.x = c.take(T * d * 4);
   L.delta = c.take(T * d * 4);
@@ -171,7 +172,7 @@ Layout run_layout(const aiq_plan* p) {
   L.qkv = c.take(T * p->n_qkv * ab);
   L.att = c.take(T * p->d_q * ab);
   L.ffn = c.take(T * p->model.d_ff * ab);
-  L.pos = c.take(T * 4);
+  L.pos = c.take((T + 256) * 4);   // GEMM epilogues read positions in 4-row groups up to the tile edge
   L.hf = 0;
   L.total = c.off;
   return L;
@@ -190,13 +191,14 @@ Layout prefill_layout(const aiq_plan* p, int64_t max_tokens) {
   L.label = c.take((T + 1) * 4);
   L.rcos = c.take(T * (p->hd / 2) * 4);
   L.rsin = c.take(T * (p->hd / 2) * 4);
+  L.rrev = c.take(static_cast<size_t>(p->hd / 2) * 4);
   L.x = c.take(T * d * 4);
   L.delta = c.take(T * d * 4);
   L.h = c.take(T * d * ab);
   L.qkv = c.take(T * p->n_qkv * ab);
   L.att = c.take(T * p->d_q * ab);
   L.ffn = c.take(T * p->model.d_ff * ab);
-  L.pos = c.take(T * 4);
+  L.pos = c.take((T + 256) * 4);
   L.hf = c.take(T * d * ab);
   L.total = c.off;
   return L;
@@ -257,6 +259,7 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
   int32_t* pos = at<int32_t>(ws, L.pos);
   const float* rcos = at<float>(ws, L.rcos);
   const float* rsin = at<float>(ws, L.rsin);
+  const float* rrev = at<float>(ws, L.rrev);
   const float eps = static_cast<float>(m.norm_eps);
   auto gemm = [&](int epi, const void* A, int64_t lda, int N, int K, const void* B0, const void* B1, const void* B2,
                   void* C, int64_t ldc) {
@@ -278,6 +281,7 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
     g.pos = pos;
     g.rope_cos = rcos;
     g.rope_sin = rsin;
+    g.rope_rev = rrev;
     return p->bf16 ? launch_gemm_bf16(epi, g, s) : launch_gemm_f32(epi, g, s);
   };
 
@@ -528,7 +532,7 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
                                p->model.vocab, p->t_ub, packed, ctr, s));
   HIP_TRY(launch_chunk_desc(cu, ctr + C_SEL, p->chunk_tokens, p->n_chunks, p->t_ub, desc, s));
   HIP_TRY(launch_rope_table(p->max_seq, p->hd / 2, p->model.rope_theta, p->hd, at<float>(ws, L.rcos),
-                            at<float>(ws, L.rsin), s));
+                            at<float>(ws, L.rsin), at<float>(ws, L.rrev), s));
   tr.end();
   // ---- prefill + label head, chunk by chunk
   for (int64_t c = 0; c < p->n_chunks; ++c) {
@@ -605,7 +609,7 @@ aiq_status aiq_prefill_packed(const aiq_plan* p, const int32_t* tok, const int32
   HIP_TRY(launch_fill_i64(ctr, C_COUNT, 0, s));
   HIP_TRY(launch_packed_desc(cu_seqlens, n_seq, n_tok, cu, desc, ctr, s));
   HIP_TRY(launch_rope_table(static_cast<int32_t>(std::min<int64_t>(cap, INT32_MAX)), p->hd / 2, p->model.rope_theta,
-                            p->hd, at<float>(ws, L.rcos), at<float>(ws, L.rsin), s));
+                            p->hd, at<float>(ws, L.rcos), at<float>(ws, L.rsin), at<float>(ws, L.rrev), s));
   const bool full = logits_mode == AIQ_LOGITS_FULL_VOCAB;
   void* hf = full ? at<void>(ws, L.hf) : nullptr;
   int32_t* label = at<int32_t>(ws, L.label);

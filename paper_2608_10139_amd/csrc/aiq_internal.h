@@ -107,8 +107,9 @@ hipError_t launch_packed_desc(const int32_t* cu32, int32_t n_seq, int64_t n_tok,
                               int64_t* desc, int64_t* ctr, hipStream_t s);
 
 // per-chunk transformer
+// cos/sin table [max_pos, hd/2] and the per-dim frequency in revolutions [hd/2]
 hipError_t launch_rope_table(int32_t max_pos, int32_t half, double theta, int32_t hd, float* cos_t,
-                             float* sin_t, hipStream_t s);
+                             float* sin_t, float* rev, hipStream_t s);
 hipError_t launch_embed(const int64_t* desc, const int64_t* cu, const int32_t* packed,
                         const void* emb, int32_t wdtype, int32_t d, int32_t vocab, float* x, int32_t* pos,
                         int64_t* ctr, int64_t t_cap, hipStream_t s);
@@ -131,9 +132,10 @@ struct GemmArgs {
   int32_t hd;
   void* C;                   // output
   int64_t ldc;
-  const int32_t* pos;        // [M] positions (EPI_QKV_ROPE)
-  const float* rope_cos;     // [max_pos, hd/2]
+  const int32_t* pos;        // [M + 256] positions (EPI_QKV_ROPE; entries past M are ignored)
+  const float* rope_cos;     // [max_pos, hd/2] (fp32 path)
   const float* rope_sin;
+  const float* rope_rev;     // [hd/2] theta^(-2i/hd) / (2 pi) (bf16 path)
 };
 
 hipError_t launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t s);

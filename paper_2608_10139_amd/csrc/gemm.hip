@@ -151,12 +151,15 @@ __device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4
   uint16_t* C = static_cast<uint16_t*>(a.C);
   const bool is_v = EPI == EPI_QKV_ROPE && nw >= a.n_q + a.n_kv;
   int sbase = 0, head = 0, hh = 0, half = 0;
+  float rev_per_pos = 0.f;
   if (EPI == EPI_QKV_ROPE && !is_v) {
     sbase = nw < a.n_q ? 0 : a.n_q;
     const int c = nw - sbase;
     head = c / a.hd;
     hh = (c % a.hd) >> 6;   // 0 except the second half-wave of a 128-dim head
     half = a.hd >> 1;
+    // rotary frequency of this lane's lower-half dim, in revolutions per position
+    rev_per_pos = a.rope_rev[hh * 32 + l32];
   }
   constexpr int COLS = EPI == EPI_SWIGLU ? 32 : 64;
 #pragma unroll
@@ -165,7 +168,11 @@ __device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4
     for (int ii = 0; ii < 2; ++ii) {
       const int i = h2 * 2 + ii;
 #pragma unroll
-      for (int g = 0; g < 4; ++g)
+      for (int g = 0; g < 4; ++g) {
+        int4 p4 = make_int4(0, 0, 0, 0);
+        if (EPI == EPI_QKV_ROPE && !is_v)   // positions of the 4 rows e = 0..3 (buffer padded past M)
+          p4 = *reinterpret_cast<const int4*>(a.pos + mw + i * 32 + g * 8 + hi * 4);
+        const int pe[4] = {p4.x, p4.y, p4.z, p4.w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = ii * 32 + g * 8 + hi * 4 + e;   // row inside the 64-row slab
@@ -173,11 +180,10 @@ __device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4
           if (EPI == EPI_SWIGLU) {
             slice[r * 32 + l32] = f2bf(silu_fast(v0) * v1);
           } else if (EPI == EPI_QKV_ROPE && !is_v) {
-            int64_t m = mw + i * 32 + g * 8 + hi * 4 + e;
-            if (m > M - 1) m = M - 1;   // rows past M are computed but never stored
-            const int dlo = hh * 32 + l32;
-            const int64_t ti = static_cast<int64_t>(a.pos[m]) * half + dlo;
-            const float cs = a.rope_cos[ti], sn = a.rope_sin[ti];
+            // angle pos * theta^(-2i/hd), in revolutions (hardware sin/cos take revolutions)
+            const float rev = static_cast<float>(pe[e]) * rev_per_pos;
+            const float frac = rev - floorf(rev);
+            const float cs = __builtin_amdgcn_cosf(frac), sn = __builtin_amdgcn_sinf(frac);
             slice[r * 64 + l32] = f2bf(v0 * cs - v1 * sn);        // lower half dims
             slice[r * 64 + 32 + l32] = f2bf(v1 * cs + v0 * sn);   // upper half dims
           } else {
@@ -185,6 +191,7 @@ __device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4
             slice[r * 64 + 32 + l32] = f2bf(v1);
           }
         }
+      }
     }
     const int64_t m_first = mw + h2 * 64;
     if (EPI == EPI_SWIGLU) {

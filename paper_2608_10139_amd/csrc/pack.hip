@@ -264,8 +264,14 @@ hipError_t launch_packed_desc(const int32_t* cu32, int32_t n_seq, int64_t n_tok,
 
 // ------------------------------------------------------------------ rotary table
 // cos / sin of pos * theta**(-2i/hd), evaluated in fp64 and rounded to fp32.
-__global__ void k_rope_table(int32_t max_pos, int32_t half, double theta, int32_t hd, float* cos_t, float* sin_t) {
+__global__ void k_rope_table(int32_t max_pos, int32_t half, double theta, int32_t hd, float* cos_t, float* sin_t,
+                             float* rev) {
   const int64_t n = static_cast<int64_t>(max_pos) * half;
+  if (blockIdx.x == 0 && static_cast<int>(threadIdx.x) < half) {
+    const int i = threadIdx.x;
+    rev[i] = static_cast<float>(pow(theta, -2.0 * static_cast<double>(i) / static_cast<double>(hd)) /
+                                6.283185307179586);
+  }
   for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < n; j += (int64_t)gridDim.x * blockDim.x) {
     const int64_t p = j / half;
     const int i = static_cast<int>(j % half);
@@ -277,9 +283,9 @@ __global__ void k_rope_table(int32_t max_pos, int32_t half, double theta, int32_
 }
 
 hipError_t launch_rope_table(int32_t max_pos, int32_t half, double theta, int32_t hd, float* cos_t,
-                             float* sin_t, hipStream_t s) {
+                             float* sin_t, float* rev, hipStream_t s) {
   hipLaunchKernelGGL(k_rope_table, dim3(grid_for(static_cast<int64_t>(max_pos) * half, 256)), dim3(256), 0,
-                     s, max_pos, half, theta, hd, cos_t, sin_t);
+                     s, max_pos, half, theta, hd, cos_t, sin_t, rev);
   return hipGetLastError();
 }
 
