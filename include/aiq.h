@@ -63,7 +63,7 @@ typedef enum aiq_status {
 
 /* element types of columns and weights */
 typedef enum aiq_dtype {
-  AIQ_I8 = 1, AIQ_I16 = 2, AIQ_I32 = 3, AIQ_F32 = 4, AIQ_BF16 = 5
+  AIQ_I8 = 1, AIQ_I16 = 2, AIQ_I32 = 3, AIQ_F32 = 4, AIQ_BF16 = 5, AIQ_F16 = 6
 } aiq_dtype;
 
 /* predicate operators: `col op k`, or `col IN (set)` */
@@ -149,7 +149,11 @@ typedef struct aiq_layer {
 typedef struct aiq_model {
   int32_t n_layers, d_model, n_heads, n_kv_heads, d_ff, vocab;
   int32_t act;                   /* aiq_act */
-  int32_t wdtype;                /* AIQ_F32 or AIQ_BF16 */
+  int32_t wdtype;                /* AIQ_F32, AIQ_BF16 or AIQ_F16: storage type of the
+                                    weights and the compute type of the projections
+                                    (16-bit types run on MFMA with fp32 accumulation;
+                                    activations fed to the projections use the same
+                                    16-bit type, the residual stream stays fp32) */
   double rope_theta;             /* rotary base, e.g. 10000 */
   double norm_eps;               /* RMSNorm epsilon, e.g. 1e-5 */
   const void* emb;               /* device [vocab, d] */

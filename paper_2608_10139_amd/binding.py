@@ -14,7 +14,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libaiq.so")
 
 AIQ_OK, AIQ_EINVAL, AIQ_EUNSUPPORTED, AIQ_ENOSPC, AIQ_EHIP, AIQ_ENOMEM = 0, -1, -2, -3, -4, -5
-AIQ_I8, AIQ_I16, AIQ_I32, AIQ_F32, AIQ_BF16 = 1, 2, 3, 4, 5
+AIQ_I8, AIQ_I16, AIQ_I32, AIQ_F32, AIQ_BF16, AIQ_F16 = 1, 2, 3, 4, 5, 6
 AIQ_LT, AIQ_LE, AIQ_GT, AIQ_GE, AIQ_EQ, AIQ_NE, AIQ_IN = range(7)
 AIQ_ACT_GELU_ERF, AIQ_ACT_SWIGLU = 1, 2
 AIQ_DECIDE_BINARY_GT, AIQ_DECIDE_ARGMAX = 1, 2

@@ -27,7 +27,8 @@ struct aiq_plan {
   int n_layers = 0;
   // derived model shapes
   int hd = 0, d_q = 0, d_kv = 0, n_qkv = 0, n_up = 0;
-  bool bf16 = false;
+  bool bf16 = false;   // 16-bit MFMA path (bf16 or fp16 operands)
+  int act = 0;         // activation element type of that path (1 bf16, 2 fp16; 0 fp32 model)
   // derived run shapes
   int64_t n_rows = 0, t_ub = 0, chunk_tokens = 0, n_chunks = 0, t_cap = 0, seq_ub = 0;
   int32_t max_seq = 0;
@@ -105,7 +106,7 @@ aiq_status validate_model(const aiq_model* m) {
   if (m->n_heads % m->n_kv_heads) return AIQ_EINVAL;
   const int hd = m->d_model / m->n_heads;
   if (hd != 32 && hd != 64 && hd != 128) return AIQ_EINVAL;
-  if (m->wdtype != AIQ_F32 && m->wdtype != AIQ_BF16) return AIQ_EINVAL;
+  if (m->wdtype != AIQ_F32 && m->wdtype != AIQ_BF16 && m->wdtype != AIQ_F16) return AIQ_EINVAL;
   if (m->act != AIQ_ACT_GELU_ERF && m->act != AIQ_ACT_SWIGLU) return AIQ_EINVAL;
   if (!(m->norm_eps > 0.0) || !(m->rope_theta > 0.0)) return AIQ_EINVAL;
   if (!m->emb || !m->final_norm || !m->lm_head || (m->n_layers > 0 && !m->layers)) return AIQ_EINVAL;
@@ -116,7 +117,7 @@ aiq_status validate_model(const aiq_model* m) {
     if (m->act == AIQ_ACT_SWIGLU && !L.w_up) return AIQ_EINVAL;
   }
   const int d = m->d_model, d_q = m->n_heads * hd, d_kv = m->n_kv_heads * hd;
-  if (m->wdtype == AIQ_BF16) {
+  if (m->wdtype == AIQ_BF16 || m->wdtype == AIQ_F16) {
     // MFMA path: 256-wide output tiles, 64-deep K steps, rotary pairs in registers
     if (m->act != AIQ_ACT_SWIGLU) return AIQ_EUNSUPPORTED;
     if (hd == 32) return AIQ_EUNSUPPORTED;
@@ -282,13 +283,14 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
     g.rope_cos = rcos;
     g.rope_sin = rsin;
     g.rope_rev = rrev;
+    g.f16 = p->act == 2;
     return p->bf16 ? launch_gemm_bf16(epi, g, s) : launch_gemm_f32(epi, g, s);
   };
 
   TRACED(tr, AIQ_K_EMBED, launch_embed(desc, cu, packed, m.emb, m.wdtype, d, m.vocab, x, pos, ctr, t_cap, s));
   for (int l = 0; l < p->n_layers; ++l) {
     const aiq_layer& W = p->layers[l];
-    TRACED(tr, AIQ_K_NORM, launch_rmsnorm(desc, x, l ? delta : nullptr, W.attn_norm, d, eps, h, p->bf16, t_cap, s));
+    TRACED(tr, AIQ_K_NORM, launch_rmsnorm(desc, x, l ? delta : nullptr, W.attn_norm, d, eps, h, p->act, t_cap, s));
     TRACED(tr, AIQ_K_GEMM_QKV, gemm(EPI_QKV_ROPE, h, d, p->n_qkv, d, W.wq, W.wk, W.wv, qkv, p->n_qkv));
     if (!p->bf16)
       TRACED(tr, AIQ_K_GEMM_QKV, launch_rope_f32(desc, static_cast<float*>(qkv), p->n_qkv, p->d_q, p->d_kv, p->hd,
@@ -304,9 +306,10 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
     aa.n_kv = m.n_kv_heads;
     aa.hd = p->hd;
     aa.seq_ub = seq_ub;
+    aa.out_act = p->act;
     TRACED(tr, AIQ_K_ATTN, p->bf16 ? launch_attention_bf16(aa, s) : launch_attention_f32(aa, s));
     TRACED(tr, AIQ_K_GEMM_O, gemm(EPI_STORE_F32, att, p->d_q, d, p->d_q, W.wo, nullptr, nullptr, delta, d));
-    TRACED(tr, AIQ_K_NORM, launch_rmsnorm(desc, x, delta, W.ffn_norm, d, eps, h, p->bf16, t_cap, s));
+    TRACED(tr, AIQ_K_NORM, launch_rmsnorm(desc, x, delta, W.ffn_norm, d, eps, h, p->act, t_cap, s));
     if (p->bf16)
       TRACED(tr, AIQ_K_GEMM_UP, gemm(EPI_SWIGLU, h, d, 2 * m.d_ff, d, W.w_gate, W.w_up, nullptr, ffn, m.d_ff));
     else
@@ -329,7 +332,7 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
   ha.label_out = ha.n_labels >= 2 ? label_out : nullptr;
   ha.logits_out = ha.n_labels >= 2 ? logits_out : nullptr;
   ha.hf_out = hf_out;
-  ha.hf_bf16 = p->bf16;
+  ha.hf_act = p->act;
   ha.seq_ub = seq_ub;
   TRACED(tr, AIQ_K_HEAD, launch_head(ha, s));
   return AIQ_OK;
@@ -376,7 +379,8 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
   p->d_q = model->n_heads * p->hd;
   p->d_kv = model->n_kv_heads * p->hd;
   p->n_qkv = p->d_q + 2 * p->d_kv;
-  p->bf16 = model->wdtype == AIQ_BF16;
+  p->bf16 = model->wdtype == AIQ_BF16 || model->wdtype == AIQ_F16;
+  p->act = model->wdtype == AIQ_F16 ? 2 : model->wdtype == AIQ_BF16 ? 1 : 0;
   p->n_up = p->bf16 ? 2 * model->d_ff : model->d_ff;
 
   if (query) {
@@ -627,6 +631,7 @@ aiq_status aiq_prefill_packed(const aiq_plan* p, const int32_t* tok, const int32
     g.B0 = p->model.lm_head;
     g.C = logits;
     g.ldc = p->model.vocab;
+    g.f16 = p->act == 2;
     HIP_TRY(p->bf16 ? launch_gemm_bf16(EPI_STORE_F32, g, s) : launch_gemm_f32(EPI_STORE_F32, g, s));
   }
   return AIQ_OK;

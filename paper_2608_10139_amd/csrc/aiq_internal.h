@@ -114,8 +114,9 @@ hipError_t launch_embed(const int64_t* desc, const int64_t* cu, const int32_t* p
                         const void* emb, int32_t wdtype, int32_t d, int32_t vocab, float* x, int32_t* pos,
                         int64_t* ctr, int64_t t_cap, hipStream_t s);
 // x += delta (when delta is non-null, written back), then out = RMSNorm(x) * g
+// out_act: 0 fp32, 1 bf16, 2 fp16
 hipError_t launch_rmsnorm(const int64_t* desc, float* x, const float* delta, const float* g, int32_t d,
-                          float eps, void* out, int32_t out_bf16, int64_t t_cap, hipStream_t s);
+                          float eps, void* out, int32_t out_act, int64_t t_cap, hipStream_t s);
 
 enum Epi : int { EPI_STORE_F32 = 0, EPI_QKV_ROPE = 1, EPI_SWIGLU = 3, EPI_GELU = 4, EPI_STORE_ACT = 5 };
 
@@ -135,7 +136,8 @@ struct GemmArgs {
   const int32_t* pos;        // [M + 256] positions (EPI_QKV_ROPE; entries past M are ignored)
   const float* rope_cos;     // [max_pos, hd/2] (fp32 path)
   const float* rope_sin;
-  const float* rope_rev;     // [hd/2] theta^(-2i/hd) / (2 pi) (bf16 path)
+  const float* rope_rev;     // [hd/2] theta^(-2i/hd) / (2 pi) (MFMA path)
+  int32_t f16;               // MFMA path: operands are fp16 (else bf16)
 };
 
 hipError_t launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t s);
@@ -153,6 +155,7 @@ struct AttnArgs {
   const int64_t* cu;         // global cu_seqlens (int64)
   int32_t n_heads, n_kv, hd;
   int64_t seq_ub;            // host upper bound on sequences per chunk
+  int32_t out_act;           // MFMA path: output element type (1 bf16, 2 fp16)
 };
 hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s);
 hipError_t launch_attention_f32(const AttnArgs& a, hipStream_t s);
@@ -173,7 +176,7 @@ struct HeadArgs {
   int32_t* label_out;        // [global seq]
   float* logits_out;         // [global seq, n_labels] or NULL
   void* hf_out;              // optional normalised rows [local seq, d] (full-vocab mode)
-  int32_t hf_bf16;
+  int32_t hf_act;            // element type of hf_out (0 fp32, 1 bf16, 2 fp16)
   int64_t seq_ub;
 };
 hipError_t launch_head(const HeadArgs& a, hipStream_t s);

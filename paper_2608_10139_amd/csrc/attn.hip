@@ -8,15 +8,19 @@
 // other rows packed next to it.  Softmax is the usual online form in fp32
 // (running max and sum, rescaled output accumulator).
 //
-// bf16 path (hd 64 / 128): both products run on v_mfma_f32_16x16x32_bf16.
-// S^T = K Q^T puts one query per lane column and 4 keys per lane, which is
-// exactly the operand layout the P V product needs for P^T, so probabilities
-// never leave registers; V is staged transposed in LDS.
+// MFMA path for bf16 models (hd 64 / 128): q, k, v arrive in fp16 and both
+// products run on v_mfma_f32_16x16x32_f16 (fp16 keeps 3 more mantissa bits
+// than bf16 at the same rate).  S^T = K Q^T puts one query per lane column and
+// 4 keys per lane, which is exactly the operand layout the P V product needs
+// for P^T, so probabilities never leave registers; V is staged transposed in
+// LDS.  The softmax denominator sums the fp16-rounded probabilities that the
+// P V product actually uses.
 #include "aiq_internal.h"
+#include "dev_util.h"
 
 namespace aiq {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 static int grid_cap(int64_t items, int cap) {
@@ -26,11 +30,6 @@ static int grid_cap(int64_t items, int cap) {
   return static_cast<int>(g);
 }
 
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return static_cast<uint16_t>(u >> 16);
-}
 
 // ======================================================================= bf16 MFMA
 template <int HD>
@@ -59,13 +58,13 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
 
     for (int qb = 0; qb * KB < L; ++qb) {
       const int qi = qb * KB + w * 16 + c16;   // this lane's query (column of S^T)
-      bf16x8 qf[HD / 32];
+      half8 qf[HD / 32];
 #pragma unroll
       for (int kc = 0; kc < HD / 32; ++kc) {
         if (qi < L)
-          qf[kc] = *reinterpret_cast<const bf16x8*>(qkv + (s0 + qi) * a.ld + qcol + kc * 32 + g * 8);
+          qf[kc] = *reinterpret_cast<const half8*>(qkv + (s0 + qi) * a.ld + qcol + kc * 32 + g * 8);
         else
-          qf[kc] = bf16x8{};
+          qf[kc] = half8{};
       }
       f32x4 o[HD / 16];
 #pragma unroll
@@ -102,8 +101,8 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
           const int krow = j * 16 + c16;
 #pragma unroll
           for (int kc = 0; kc < HD / 32; ++kc) {
-            const bf16x8 kf = *reinterpret_cast<const bf16x8*>(Ks + krow * HD + (((kc * 4 + g) ^ (krow & 7)) << 3));
-            sacc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[kc], sacc[j], 0, 0, 0);
+            const half8 kf = *reinterpret_cast<const half8*>(Ks + krow * HD + (((kc * 4 + g) ^ (krow & 7)) << 3));
+            sacc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf, qf[kc], sacc[j], 0, 0, 0);
           }
         }
         float mx = -INFINITY;
@@ -123,11 +122,12 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
         const float m_new = fmaxf(m_run, mx);
         const float alpha = (m_new == -INFINITY) ? 1.f : exp2f(m_run - m_new);
         float psum = 0.f;
-        float p[16];
+        uint16_t ph[16];   // fp16 probabilities fed to the P V product
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          p[i] = (m_new == -INFINITY || sv[i] == -INFINITY) ? 0.f : exp2f(sv[i] - m_new);
-          psum += p[i];
+          const float pf = (m_new == -INFINITY || sv[i] == -INFINITY) ? 0.f : exp2f(sv[i] - m_new);
+          ph[i] = f2h(pf);
+          psum += h2f(ph[i]);
         }
         l_run = l_run * alpha + psum;
         m_run = m_new;
@@ -137,15 +137,15 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
         // O^T += V^T P^T over two 32-key halves
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-          bf16x8 pb;
+          half8 pb;
           {
             uint16_t tmp[8];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-              tmp[e] = f2bf(p[(2 * u) * 4 + e]);
-              tmp[4 + e] = f2bf(p[(2 * u + 1) * 4 + e]);
+              tmp[e] = ph[(2 * u) * 4 + e];
+              tmp[4 + e] = ph[(2 * u + 1) * 4 + e];
             }
-            pb = *reinterpret_cast<const bf16x8*>(tmp);
+            pb = *reinterpret_cast<const half8*>(tmp);
           }
 #pragma unroll
           for (int db = 0; db < HD / 16; ++db) {
@@ -154,8 +154,8 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
             const uint2 lo = *reinterpret_cast<const uint2*>(vrow + (((8 * u + g) ^ (dim & 15)) << 2));
             const uint2 hi = *reinterpret_cast<const uint2*>(vrow + (((8 * u + 4 + g) ^ (dim & 15)) << 2));
             const uint4 vv = make_uint4(lo.x, lo.y, hi.x, hi.y);
-            const bf16x8 vf = *reinterpret_cast<const bf16x8*>(&vv);
-            o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pb, o[db], 0, 0, 0);
+            const half8 vf = *reinterpret_cast<const half8*>(&vv);
+            o[db] = __builtin_amdgcn_mfma_f32_16x16x32_f16(vf, pb, o[db], 0, 0, 0);
           }
         }
       }
@@ -169,8 +169,8 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
         for (int db = 0; db < HD / 16; ++db) {
           const f32x4 v = o[db];
           uint2 pk;
-          pk.x = f2bf(v[0] * inv) | (static_cast<uint32_t>(f2bf(v[1] * inv)) << 16);
-          pk.y = f2bf(v[2] * inv) | (static_cast<uint32_t>(f2bf(v[3] * inv)) << 16);
+          pk.x = f2act(v[0] * inv, a.out_act) | (static_cast<uint32_t>(f2act(v[1] * inv, a.out_act)) << 16);
+          pk.y = f2act(v[2] * inv, a.out_act) | (static_cast<uint32_t>(f2act(v[3] * inv, a.out_act)) << 16);
           *reinterpret_cast<uint2*>(orow + db * 16 + 4 * g) = pk;
         }
       }

@@ -16,11 +16,14 @@
 // fp32 path: a plain 64 x 64 LDS-tiled FMA kernel with the same row mapping
 // and epilogues, used for fp32 models.
 #include "aiq_internal.h"
+#include "dev_util.h"
 
 namespace aiq {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 static int g_cus[64];
 
@@ -35,11 +38,6 @@ static int num_cus() {
   return g_cus[dev];
 }
 
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return static_cast<uint16_t>(u >> 16);
-}
 
 __device__ __forceinline__ uint2 pack_bf16x4(float a, float b, float c, float d) {
   uint2 p;
@@ -86,10 +84,27 @@ __device__ __forceinline__ const T* b_row(const GemmArgs& a, int n) {
   }
 }
 
-// ======================================================================= bf16 MFMA
+// ======================================================================= 16-bit MFMA
+// The MFMA path runs on bf16 or fp16 operands (H = fp16); both forms of
+// v_mfma_f32_32x32x16 have the same rate.
+template <bool H> struct Op16;
+template <> struct Op16<false> {
+  typedef bf16x8 V;
+  static __device__ __forceinline__ f32x16_t mma(V a, V b, f32x16_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ uint16_t cvt(float f) { return f2bf(f); }
+};
+template <> struct Op16<true> {
+  typedef half8 V;
+  static __device__ __forceinline__ f32x16_t mma(V a, V b, f32x16_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ uint16_t cvt(float f) { return f2h(f); }
+};
 constexpr int GM = 256, GN = 256, GK = 64, GT = 512;
 
-typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef f32x16_t f32x16;
 
 // Accumulator layout (v_mfma_f32_32x32x16_bf16, activations as the first
 // operand): acc[i][j][4g + e] holds C[m][n] with
@@ -97,6 +112,9 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 // A lane owns one column of each 32-wide block, so the rotary pair (j = 0
 // lower half, j = 1 upper half of a head) and the SwiGLU pair (j = 0 gate,
 // j = 1 up) sit in the same lane.
+//
+// q, k and v (attention operands) are stored in fp16: 10 mantissa bits where
+// bf16 has 7, at the same MFMA rate; their magnitudes are O(1) after RMSNorm.
 //
 // Output goes through LDS: each wave owns an 8 KB slice of the idle LDS stage,
 // writes a slab of its sub-tile there in row-major order, then stores whole
@@ -123,7 +141,7 @@ __device__ __forceinline__ void flush_slab(const T* slab, int rows, int cols, T*
   }
 }
 
-template <int EPI>
+template <int EPI, bool H>
 __device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4][2], int64_t m0, int n0,
                                               int64_t M, int wm, int wn, int lane, uint16_t* slice) {
   const int l32 = lane & 31, hi = lane >> 5;
@@ -178,17 +196,20 @@ __device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4
           const int r = ii * 32 + g * 8 + hi * 4 + e;   // row inside the 64-row slab
           const float v0 = acc[i][0][4 * g + e], v1 = acc[i][1][4 * g + e];
           if (EPI == EPI_SWIGLU) {
-            slice[r * 32 + l32] = f2bf(silu_fast(v0) * v1);
+            slice[r * 32 + l32] = Op16<H>::cvt(silu_fast(v0) * v1);
           } else if (EPI == EPI_QKV_ROPE && !is_v) {
             // angle pos * theta^(-2i/hd), in revolutions (hardware sin/cos take revolutions)
             const float rev = static_cast<float>(pe[e]) * rev_per_pos;
             const float frac = rev - floorf(rev);
             const float cs = __builtin_amdgcn_cosf(frac), sn = __builtin_amdgcn_sinf(frac);
-            slice[r * 64 + l32] = f2bf(v0 * cs - v1 * sn);        // lower half dims
-            slice[r * 64 + 32 + l32] = f2bf(v1 * cs + v0 * sn);   // upper half dims
+            slice[r * 64 + l32] = f2h(v0 * cs - v1 * sn);        // lower half dims
+            slice[r * 64 + 32 + l32] = f2h(v1 * cs + v0 * sn);   // upper half dims
+          } else if (EPI == EPI_QKV_ROPE) {   // v
+            slice[r * 64 + l32] = f2h(v0);
+            slice[r * 64 + 32 + l32] = f2h(v1);
           } else {
-            slice[r * 64 + l32] = f2bf(v0);
-            slice[r * 64 + 32 + l32] = f2bf(v1);
+            slice[r * 64 + l32] = Op16<H>::cvt(v0);
+            slice[r * 64 + 32 + l32] = Op16<H>::cvt(v1);
           }
         }
       }
@@ -217,29 +238,32 @@ __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >>
 // One 64-deep k-step of the wave's 128 x 64 sub-tile from one LDS stage.
 // Fragments of the next 16-deep sub-step are read while the MFMAs of the
 // current one run (two register sets), so LDS latency hides behind MFMA work.
+template <bool H>
 __device__ __forceinline__ void load_frags(const uint16_t* As, const uint16_t* Bs, int s, int wm, int wn, int lane,
-                                           bf16x8 (&af)[4], bf16x8 (&bw)[2]) {
+                                           typename Op16<H>::V (&af)[4], typename Op16<H>::V (&bw)[2]) {
+  typedef typename Op16<H>::V V;
   const int r32 = lane & 31;
   const int sw = swz(r32, 2 * s + (lane >> 5)) << 3;   // same for every 32-row block
 #pragma unroll
-  for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const bf16x8*>(As + (wm * 128 + i * 32 + r32) * GK + sw);
+  for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const V*>(As + (wm * 128 + i * 32 + r32) * GK + sw);
 #pragma unroll
-  for (int j = 0; j < 2; ++j) bw[j] = *reinterpret_cast<const bf16x8*>(Bs + (wn * 64 + j * 32 + r32) * GK + sw);
+  for (int j = 0; j < 2; ++j) bw[j] = *reinterpret_cast<const V*>(Bs + (wn * 64 + j * 32 + r32) * GK + sw);
 }
 
+template <bool H>
 __device__ __forceinline__ void mma_stage(const uint16_t* As, const uint16_t* Bs, f32x16 (&acc)[4][2], int wm,
                                           int wn, int lane) {
-  bf16x8 af[2][4], bw[2][2];
-  load_frags(As, Bs, 0, wm, wn, lane, af[0], bw[0]);
+  typename Op16<H>::V af[2][4], bw[2][2];
+  load_frags<H>(As, Bs, 0, wm, wn, lane, af[0], bw[0]);
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
     const int cur = s & 1;
-    if (s < 3) load_frags(As, Bs, s + 1, wm, wn, lane, af[cur ^ 1], bw[cur ^ 1]);
+    if (s < 3) load_frags<H>(As, Bs, s + 1, wm, wn, lane, af[cur ^ 1], bw[cur ^ 1]);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 2; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bw[cur][j], acc[i][j], 0, 0, 0);
+        acc[i][j] = Op16<H>::mma(af[cur][i], bw[cur][j], acc[i][j]);
     if (s < 3) {
       // interleave: one MFMA, one LDS read, ... then the remaining MFMAs
       for (int q = 0; q < 6; ++q) {
@@ -279,7 +303,7 @@ __device__ __forceinline__ void tile_sources(const GemmArgs& a, const uint16_t* 
   }
 }
 
-template <int EPI>
+template <int EPI, bool H>
 __global__ __launch_bounds__(GT) void k_gemm_bf16(GemmArgs a) {
   // two stages in distinct arrays: the compiler can then tell the in-flight
   // loads into one stage from the reads of the other and only waits at the
@@ -340,11 +364,11 @@ __global__ __launch_bounds__(GT) void k_gemm_bf16(GemmArgs a) {
     __syncthreads();   // stage 0 of this tile has landed
     for (int kt = 0; kt < nk; kt += 2) {
       if (kt + 1 < nk) dma_stage(sA1, sB1, ga, gb, (kt + 1) * GK, w);
-      mma_stage(sA0, sB0, acc, wm, wn, lane);
+      mma_stage<H>(sA0, sB0, acc, wm, wn, lane);
       __syncthreads();
       if (kt + 1 < nk) {
         if (kt + 2 < nk) dma_stage(sA0, sB0, ga, gb, (kt + 2) * GK, w);
-        mma_stage(sA1, sB1, acc, wm, wn, lane);
+        mma_stage<H>(sA1, sB1, acc, wm, wn, lane);
         __syncthreads();
       }
     }
@@ -359,7 +383,7 @@ __global__ __launch_bounds__(GT) void k_gemm_bf16(GemmArgs a) {
     // each wave stages its output in its own 8 KB slice of stage 1, which is
     // idle until the next tile's first barrier
     uint16_t* slice = (w < 4 ? sA1 : sB1) + (w & 3) * 4096;
-    epilogue_bf16<EPI>(a, acc, m0, n0, M, wm, wn, lane, slice);
+    epilogue_bf16<EPI, H>(a, acc, m0, n0, M, wm, wn, lane, slice);
   }
 }
 
@@ -370,13 +394,21 @@ hipError_t launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t s) {
   if (tiles < g) g = tiles;
   g = (g + 7) / 8 * 8;
   const dim3 grid(static_cast<unsigned>(g)), block(GT);
+#define AIQ_LAUNCH_GEMM(E)                                                         \
+  do {                                                                             \
+    if (a.f16)                                                                     \
+      hipLaunchKernelGGL((k_gemm_bf16<E, true>), grid, block, 0, s, a);            \
+    else                                                                           \
+      hipLaunchKernelGGL((k_gemm_bf16<E, false>), grid, block, 0, s, a);           \
+  } while (0)
   switch (epi) {
-    case EPI_STORE_F32: hipLaunchKernelGGL(k_gemm_bf16<EPI_STORE_F32>, grid, block, 0, s, a); break;
-    case EPI_STORE_ACT: hipLaunchKernelGGL(k_gemm_bf16<EPI_STORE_ACT>, grid, block, 0, s, a); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL(k_gemm_bf16<EPI_SWIGLU>, grid, block, 0, s, a); break;
-    case EPI_QKV_ROPE: hipLaunchKernelGGL(k_gemm_bf16<EPI_QKV_ROPE>, grid, block, 0, s, a); break;
+    case EPI_STORE_F32: AIQ_LAUNCH_GEMM(EPI_STORE_F32); break;
+    case EPI_STORE_ACT: AIQ_LAUNCH_GEMM(EPI_STORE_ACT); break;
+    case EPI_SWIGLU: AIQ_LAUNCH_GEMM(EPI_SWIGLU); break;
+    case EPI_QKV_ROPE: AIQ_LAUNCH_GEMM(EPI_QKV_ROPE); break;
     default: return hipErrorInvalidValue;
   }
+#undef AIQ_LAUNCH_GEMM
   return hipGetLastError();
 }
 

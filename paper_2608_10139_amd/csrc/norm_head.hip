@@ -6,6 +6,7 @@
 // vocab] logits: one wave per sequence normalises the last token's residual
 // row in fp32 and takes K dot products with the label rows of the LM head.
 #include "aiq_internal.h"
+#include "dev_util.h"
 
 namespace aiq {
 
@@ -22,13 +23,6 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return static_cast<uint16_t>(u >> 16);
-}
-
-__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
 
 // ------------------------------------------------------------------ residual add + RMSNorm
 // One wave per row.  With a pending projection output `delta` the residual
@@ -37,7 +31,7 @@ __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(stati
 // fixed order inside the row, so a row's result does not depend on which
 // other rows share the launch.
 __global__ __launch_bounds__(256) void k_rmsnorm(const int64_t* desc, float* x, const float* delta, const float* g,
-                                                 int32_t d, float eps, void* out, int32_t out_bf16) {
+                                                 int32_t d, float eps, void* out, int32_t out_act) {
   const int64_t nt = desc[D_NTOK];
   const int lane = threadIdx.x & 63;
   const int64_t wave = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6;
@@ -70,10 +64,10 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const int64_t* desc, float* x, 
       const int c = lane + 64 * j;
       if (c < nv) {
         const float4 a = v[j], w = gr[c];
-        if (out_bf16) {
+        if (out_act != ACT_F32) {
           uint2 p;
-          p.x = f2bf(a.x * r * w.x) | (static_cast<uint32_t>(f2bf(a.y * r * w.y)) << 16);
-          p.y = f2bf(a.z * r * w.z) | (static_cast<uint32_t>(f2bf(a.w * r * w.w)) << 16);
+          p.x = f2act(a.x * r * w.x, out_act) | (static_cast<uint32_t>(f2act(a.y * r * w.y, out_act)) << 16);
+          p.y = f2act(a.z * r * w.z, out_act) | (static_cast<uint32_t>(f2act(a.w * r * w.w, out_act)) << 16);
           reinterpret_cast<uint2*>(static_cast<uint16_t*>(out) + t * d)[c] = p;
         } else {
           reinterpret_cast<float4*>(static_cast<float*>(out) + t * d)[c] =
@@ -85,10 +79,10 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const int64_t* desc, float* x, 
 }
 
 hipError_t launch_rmsnorm(const int64_t* desc, float* x, const float* delta, const float* g, int32_t d,
-                          float eps, void* out, int32_t out_bf16, int64_t t_cap, hipStream_t s) {
+                          float eps, void* out, int32_t out_act, int64_t t_cap, hipStream_t s) {
   if (d > 64 * 4 * 16) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_rmsnorm, dim3(grid_for(t_cap, 4, 4096)), dim3(256), 0, s, desc, x, delta, g, d, eps, out,
-                     out_bf16);
+                     out_act);
   return hipGetLastError();
 }
 
@@ -115,9 +109,10 @@ __global__ __launch_bounds__(256) void k_head(HeadArgs a) {
     float lg[AIQ_MAX_LABELS];
     for (int k = 0; k < a.n_labels; ++k) {
       float acc = 0.f;
-      if (a.wdtype == AIQ_BF16) {
+      if (a.wdtype == AIQ_BF16 || a.wdtype == AIQ_F16) {
+        const int wa = a.wdtype == AIQ_F16 ? ACT_F16 : ACT_BF16;
         const uint16_t* w = static_cast<const uint16_t*>(a.lm_head) + static_cast<int64_t>(a.labels[k]) * d;
-        for (int c = lane; c < d; c += 64) acc += (xv(c) * r * a.g[c]) * bf2f(w[c]);
+        for (int c = lane; c < d; c += 64) acc += (xv(c) * r * a.g[c]) * act2f(w[c], wa);
       } else {
         const float* w = static_cast<const float*>(a.lm_head) + static_cast<int64_t>(a.labels[k]) * d;
         for (int c = lane; c < d; c += 64) acc += (xv(c) * r * a.g[c]) * w[c];
@@ -125,9 +120,9 @@ __global__ __launch_bounds__(256) void k_head(HeadArgs a) {
       lg[k] = wave_sum(acc);
     }
     if (a.hf_out) {
-      if (a.hf_bf16) {
+      if (a.hf_act != ACT_F32) {
         uint16_t* o = static_cast<uint16_t*>(a.hf_out) + i * d;
-        for (int c = lane; c < d; c += 64) o[c] = f2bf(xv(c) * r * a.g[c]);
+        for (int c = lane; c < d; c += 64) o[c] = f2act(xv(c) * r * a.g[c], a.hf_act);
       } else {
         float* o = static_cast<float*>(a.hf_out) + i * d;
         for (int c = lane; c < d; c += 64) o[c] = xv(c) * r * a.g[c];

@@ -9,6 +9,7 @@
 // chunks of at most chunk_tokens + longest-sequence tokens.  Every count
 // lives in device memory; kernels read their real extents from it.
 #include "aiq_internal.h"
+#include "dev_util.h"
 
 namespace aiq {
 
@@ -313,15 +314,16 @@ __global__ __launch_bounds__(256) void k_embed(const int64_t* desc, const int64_
       pos[t] = static_cast<int32_t>(g - cu[lo]);
     }
     float* xr = x + t * d;
-    if (wdtype == AIQ_BF16) {
+    if (wdtype == AIQ_BF16 || wdtype == AIQ_F16) {
+      const int ea = wdtype == AIQ_F16 ? ACT_F16 : ACT_BF16;
       const uint16_t* er = static_cast<const uint16_t*>(emb) + static_cast<int64_t>(tok) * d;
       for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
         const uint2 v = *reinterpret_cast<const uint2*>(er + c);
         float4 o;
-        o.x = __uint_as_float((v.x & 0xFFFFu) << 16);
-        o.y = __uint_as_float(v.x & 0xFFFF0000u);
-        o.z = __uint_as_float((v.y & 0xFFFFu) << 16);
-        o.w = __uint_as_float(v.y & 0xFFFF0000u);
+        o.x = act2f(static_cast<uint16_t>(v.x & 0xFFFFu), ea);
+        o.y = act2f(static_cast<uint16_t>(v.x >> 16), ea);
+        o.z = act2f(static_cast<uint16_t>(v.y & 0xFFFFu), ea);
+        o.w = act2f(static_cast<uint16_t>(v.y >> 16), ea);
         *reinterpret_cast<float4*>(xr + c) = o;
       }
     } else {

@@ -46,15 +46,26 @@ def _ptr(t) -> int:
 
 
 class DeviceModel:
-    """Model weights resident in device memory plus the aiq_model struct."""
+    """Model weights resident in device memory plus the aiq_model struct.
 
-    def __init__(self, model: dict, device="cuda"):
+    ``compute`` selects the projection type of a 16-bit model: "bf16" keeps the
+    stored bf16 weights; "f16" uploads their fp16 images (exact except for
+    |w| < 2**-14, which fp16 holds as subnormals) so that activations fed to
+    the MFMA projections carry 10 mantissa bits instead of 7.  fp32 models
+    are uploaded as they are."""
+
+    def __init__(self, model: dict, device="cuda", compute: str | None = None):
         spec = model["spec"]
         self.spec = spec
         self.keep = []
+        self.compute = "f32" if spec.dtype == "f32" else (compute or "f16")
+        if self.compute not in ("f32", "bf16", "f16"):
+            raise ValueError(compute)
 
         def up(a):
             t = _dev(a, device)
+            if t.dtype == torch.bfloat16 and self.compute == "f16":
+                t = t.to(torch.float16)
             self.keep.append(t)
             return t
 
@@ -74,7 +85,7 @@ class DeviceModel:
         m.n_layers, m.d_model, m.n_heads = L, spec.d_model, spec.n_heads
         m.n_kv_heads, m.d_ff, m.vocab = spec.n_kv_heads, spec.d_ff, spec.vocab
         m.act = B.AIQ_ACT_SWIGLU if spec.act == "swiglu" else B.AIQ_ACT_GELU_ERF
-        m.wdtype = B.AIQ_BF16 if spec.dtype == "bf16" else B.AIQ_F32
+        m.wdtype = {"f32": B.AIQ_F32, "bf16": B.AIQ_BF16, "f16": B.AIQ_F16}[self.compute]
         m.rope_theta, m.norm_eps = spec.rope_theta, spec.norm_eps
         m.emb, m.lm_head, m.final_norm = _ptr(self.emb), _ptr(self.lm_head), _ptr(self.final_norm)
         m.layers = C.cast(self.layers, C.POINTER(B.aiq_layer))

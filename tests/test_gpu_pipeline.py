@@ -74,10 +74,10 @@ def test_tiny_chunking_does_not_change_results():
 
 # ---------------------------------------------------------------- reviews model, bf16, prefill entry
 
-@pytest.fixture(scope="module")
-def reviews_prefill():
+@pytest.fixture(scope="module", params=["f16", "bf16"])
+def reviews_prefill(request):
     w = workload("reviews")
-    dm = DeviceModel(w["model"])
+    dm = DeviceModel(w["model"], compute=request.param)
     return w, dm
 
 
@@ -139,13 +139,14 @@ def test_reviews_full_vocab_head(reviews_prefill):
 
 # ---------------------------------------------------------------- reviews end to end
 
-def test_reviews_end_to_end():
-    say("case: reviews end-to-end (16,384 rows, bf16 4-layer d512)")
+@pytest.mark.parametrize("compute", ["f16", "bf16"])
+def test_reviews_end_to_end(compute):
+    say(f"case: reviews end-to-end (16,384 rows, 4-layer d512, {compute} projections)")
     g = load_golden("reviews")
     if g is None:
         pytest.skip("golden file for the reviews workload not generated")
     w = workload("reviews")
     q = w["workload"].queries[0]
-    r = run_query(w, q)
+    r = run_query(w, q, dmodel=DeviceModel(w["model"], compute=compute))
     check_query(r, w, q, g["q0_rows"], None, g["q0_logits"], g["q0_labels"], g["q0_margin"], TOL_BF16)
     say(f"  selected {r['n_selected']} kept {r['count']} tokens {r['n_tokens']}")
