@@ -134,10 +134,36 @@ aiq_status validate_model(const aiq_model* m) {
 
 struct Layout {
   size_t ctr, mask, blk_cnt, blk_off, sel, payload, lens, label, logits, cu, scan_tmp, packed, hkeys, hvals,
-      bins, desc, rcos, rsin, rrev, x, delta, h, qkv, att, ffn, pos, hf, total;
+      bins, desc, rcos, rsin, rrev, x, delta, h, qkv, att, ffn, pos, hf, ssp, rs, total;
 };
 
 size_t act_bytes(const aiq_plan* p) { return p->bf16 ? 2 : 4; }
+
+// Per-token residual-stream bytes: x (fp32) plus, on the fp32 path, the
+// pending projection output `delta`, or on the MFMA path the per-slice sums
+// of squares (one float per 64 columns) and the row scale.
+size_t resid_bytes(const aiq_plan* p) {
+  const size_t d = static_cast<size_t>(p->model.d_model);
+  return d * 4 + (p->bf16 ? d / 16 + 4 : d * 4);
+}
+
+// x, delta / ssp / rs and the 16-bit or fp32 activations of one chunk of T tokens
+void take_resid(const aiq_plan* p, Carver& c, Layout& L, size_t T) {
+  const size_t d = static_cast<size_t>(p->model.d_model);
+  const size_t ab = act_bytes(p);
+  L.x = c.take(T * d * 4);
+  if (p->bf16) {
+    L.ssp = c.take(T * (d / 64) * 4);
+    L.rs = c.take((T + 256) * 4);   // GEMMs read row scales in 256-row tiles up to the tile edge
+  } else {
+    L.delta = c.take(T * d * 4);
+  }
+  L.h = c.take(T * d * ab);
+  L.qkv = c.take(T * p->n_qkv * ab);
+  L.att = c.take(T * p->d_q * ab);
+  L.ffn = c.take(T * p->model.d_ff * ab);
+  L.pos = c.take((T + 256) * 4);   // GEMM tiles read positions up to the tile edge
+}
 
 Layout run_layout(const aiq_plan* p) {
   Layout L{};
@@ -166,14 +192,7 @@ Layout run_layout(const aiq_plan* p) {
   L.rcos = c.take(static_cast<size_t>(p->max_seq) * (p->hd / 2) * 4);
   L.rsin = c.take(static_cast<size_t>(p->max_seq) * (p->hd / 2) * 4);
   L.rrev = c.take(static_cast<size_t>(p->hd / 2) * 4);
-  const size_t T = static_cast<size_t>(p->t_cap);
-  L.x = c.take(T * d * 4);
-  L.delta = c.take(T * d * 4);
-  L.h = c.take(T * d * ab);
-  L.qkv = c.take(T * p->n_qkv * ab);
-  L.att = c.take(T * p->d_q * ab);
-  L.ffn = c.take(T * p->model.d_ff * ab);
-  L.pos = c.take((T + 256) * 4);   // GEMM epilogues read positions in 4-row groups up to the tile edge
+  take_resid(p, c, L, static_cast<size_t>(p->t_cap));
   L.hf = 0;
   L.total = c.off;
   return L;
@@ -193,13 +212,7 @@ Layout prefill_layout(const aiq_plan* p, int64_t max_tokens) {
   L.rcos = c.take(T * (p->hd / 2) * 4);
   L.rsin = c.take(T * (p->hd / 2) * 4);
   L.rrev = c.take(static_cast<size_t>(p->hd / 2) * 4);
-  L.x = c.take(T * d * 4);
-  L.delta = c.take(T * d * 4);
-  L.h = c.take(T * d * ab);
-  L.qkv = c.take(T * p->n_qkv * ab);
-  L.att = c.take(T * p->d_q * ab);
-  L.ffn = c.take(T * p->model.d_ff * ab);
-  L.pos = c.take((T + 256) * 4);
+  take_resid(p, c, L, T);
   L.hf = c.take(T * d * ab);
   L.total = c.off;
   return L;
@@ -252,7 +265,11 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
   const int d = m.d_model;
   const int64_t* m_ptr = desc + D_NTOK;
   float* x = at<float>(ws, L.x);
-  float* delta = at<float>(ws, L.delta);   // output of the last O / down projection, added by the next norm
+  // fp32 path: output of the last O / down projection, added by the next norm
+  float* delta = p->bf16 ? nullptr : at<float>(ws, L.delta);
+  // MFMA path: per-slice sums of squares and row scales of the norm folded into the next projection
+  float* ssp = p->bf16 ? at<float>(ws, L.ssp) : nullptr;
+  float* rs = p->bf16 ? at<float>(ws, L.rs) : nullptr;
   void* h = at<void>(ws, L.h);
   void* qkv = at<void>(ws, L.qkv);
   void* att = at<void>(ws, L.att);
@@ -263,7 +280,7 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
   const float* rrev = at<float>(ws, L.rrev);
   const float eps = static_cast<float>(m.norm_eps);
   auto gemm = [&](int epi, const void* A, int64_t lda, int N, int K, const void* B0, const void* B1, const void* B2,
-                  void* C, int64_t ldc) {
+                  void* C, int64_t ldc, const float* gnext = nullptr) {
     GemmArgs g{};
     g.A = A;
     g.lda = lda;
@@ -284,9 +301,53 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
     g.rope_sin = rsin;
     g.rope_rev = rrev;
     g.f16 = p->act == 2;
+    g.rs = rs;
+    if (epi == EPI_RESID) {
+      g.x = x;
+      g.gnext = gnext;
+      g.hout = h;
+      g.ssp = ssp;
+      g.n_part = d / 64;
+    }
     return p->bf16 ? launch_gemm_bf16(epi, g, s) : launch_gemm_f32(epi, g, s);
   };
 
+  if (p->bf16) {
+    // MFMA path: each RMSNorm is split between the producer of its input and
+    // the projection that consumes it.  h = x * g (16-bit) and the row sums of
+    // x^2 come from the embedding or from the residual projection's epilogue;
+    // the consuming projection scales its rows by 1/rms, since
+    // (x / rms * g) . W^T = ((x * g) . W^T) / rms.
+    const float* g0 = p->n_layers > 0 ? p->layers[0].attn_norm : m.final_norm;
+    TRACED(tr, AIQ_K_EMBED, launch_embed_norm(desc, cu, packed, m.emb, m.wdtype, d, m.vocab, x, pos, ctr, g0, eps,
+                                              h, p->act, rs, t_cap, s));
+    for (int l = 0; l < p->n_layers; ++l) {
+      const aiq_layer& W = p->layers[l];
+      const bool last = l + 1 == p->n_layers;
+      TRACED(tr, AIQ_K_GEMM_QKV, gemm(EPI_QKV_ROPE, h, d, p->n_qkv, d, W.wq, W.wk, W.wv, qkv, p->n_qkv));
+      AttnArgs aa{};
+      aa.qkv = qkv;
+      aa.ld = p->n_qkv;
+      aa.out = att;
+      aa.ldo = p->d_q;
+      aa.desc = desc;
+      aa.cu = cu;
+      aa.n_heads = m.n_heads;
+      aa.n_kv = m.n_kv_heads;
+      aa.hd = p->hd;
+      aa.seq_ub = seq_ub;
+      aa.out_act = p->act;
+      TRACED(tr, AIQ_K_ATTN, launch_attention_bf16(aa, s));
+      TRACED(tr, AIQ_K_GEMM_O, gemm(EPI_RESID, att, p->d_q, d, p->d_q, W.wo, nullptr, nullptr, nullptr, d,
+                                    W.ffn_norm));
+      TRACED(tr, AIQ_K_NORM, launch_row_scale(desc, ssp, d / 64, d, eps, rs, t_cap, s));
+      TRACED(tr, AIQ_K_GEMM_UP, gemm(EPI_SWIGLU, h, d, 2 * m.d_ff, d, W.w_gate, W.w_up, nullptr, ffn, m.d_ff));
+      // the head normalises the last position itself: after the last layer only x is needed
+      TRACED(tr, AIQ_K_GEMM_DOWN, gemm(EPI_RESID, ffn, m.d_ff, d, m.d_ff, W.w_down, nullptr, nullptr, nullptr, d,
+                                       last ? nullptr : p->layers[l + 1].attn_norm));
+      if (!last) TRACED(tr, AIQ_K_NORM, launch_row_scale(desc, ssp, d / 64, d, eps, rs, t_cap, s));
+    }
+  } else {
   TRACED(tr, AIQ_K_EMBED, launch_embed(desc, cu, packed, m.emb, m.wdtype, d, m.vocab, x, pos, ctr, t_cap, s));
   for (int l = 0; l < p->n_layers; ++l) {
     const aiq_layer& W = p->layers[l];
@@ -316,11 +377,12 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
       TRACED(tr, AIQ_K_GEMM_UP, gemm(EPI_GELU, h, d, m.d_ff, d, W.w_gate, nullptr, nullptr, ffn, m.d_ff));
     TRACED(tr, AIQ_K_GEMM_DOWN, gemm(EPI_STORE_F32, ffn, m.d_ff, d, m.d_ff, W.w_down, nullptr, nullptr, delta, d));
   }
+  }
   HeadArgs ha{};
   ha.desc = desc;
   ha.cu = cu;
   ha.x = x;
-  ha.delta = p->n_layers > 0 ? delta : nullptr;
+  ha.delta = p->n_layers > 0 ? delta : nullptr;   // null on the MFMA path: x is complete
   ha.g = m.final_norm;
   ha.eps = eps;
   ha.d = d;
@@ -440,7 +502,7 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
     p->max_seq = p->probe.max_list_len + q.n_prefix;
     // default chunk: about 48 GB of per-token activations (a fraction of one
     // MI355X's 288 GB), at most 4M tokens
-    const int64_t per_tok = static_cast<int64_t>(model->d_model) * 8 +   // x and delta (fp32)
+    const int64_t per_tok = static_cast<int64_t>(resid_bytes(p)) +
                             static_cast<int64_t>(model->d_model + p->n_qkv + p->d_q + model->d_ff) *
                                 (p->bf16 ? 2 : 4) + 4;
     const int64_t def_chunk = std::min<int64_t>((int64_t(48) << 30) / per_tok, int64_t(4) << 20);

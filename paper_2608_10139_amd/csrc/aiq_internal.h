@@ -113,12 +113,22 @@ hipError_t launch_rope_table(int32_t max_pos, int32_t half, double theta, int32_
 hipError_t launch_embed(const int64_t* desc, const int64_t* cu, const int32_t* packed,
                         const void* emb, int32_t wdtype, int32_t d, int32_t vocab, float* x, int32_t* pos,
                         int64_t* ctr, int64_t t_cap, hipStream_t s);
+// MFMA path: the embedding also writes the first projection's operand
+// h = x * g (16-bit) and the row scale rs = 1 / sqrt(mean(x^2) + eps).
+hipError_t launch_embed_norm(const int64_t* desc, const int64_t* cu, const int32_t* packed, const void* emb,
+                             int32_t wdtype, int32_t d, int32_t vocab, float* x, int32_t* pos, int64_t* ctr,
+                             const float* g, float eps, void* h, int32_t h_act, float* rs, int64_t t_cap,
+                             hipStream_t s);
+// rs[t] = 1 / sqrt(sum_p ssp[t, p] / d + eps) for the chunk's tokens, the
+// partial sums added in order p = 0, 1, ...
+hipError_t launch_row_scale(const int64_t* desc, const float* ssp, int32_t n_part, int32_t d, float eps,
+                            float* rs, int64_t t_cap, hipStream_t s);
 // x += delta (when delta is non-null, written back), then out = RMSNorm(x) * g
 // out_act: 0 fp32, 1 bf16, 2 fp16
 hipError_t launch_rmsnorm(const int64_t* desc, float* x, const float* delta, const float* g, int32_t d,
                           float eps, void* out, int32_t out_act, int64_t t_cap, hipStream_t s);
 
-enum Epi : int { EPI_STORE_F32 = 0, EPI_QKV_ROPE = 1, EPI_SWIGLU = 3, EPI_GELU = 4, EPI_STORE_ACT = 5 };
+enum Epi : int { EPI_STORE_F32 = 0, EPI_QKV_ROPE = 1, EPI_SWIGLU = 3, EPI_GELU = 4, EPI_STORE_ACT = 5, EPI_RESID = 6 };
 
 struct GemmArgs {
   const void* A;             // [M, K] activations (bf16 or f32), row stride lda
@@ -138,6 +148,13 @@ struct GemmArgs {
   const float* rope_sin;
   const float* rope_rev;     // [hd/2] theta^(-2i/hd) / (2 pi) (MFMA path)
   int32_t f16;               // MFMA path: operands are fp16 (else bf16)
+  // Residual stream with the RMSNorm folded into the projections (MFMA path):
+  const float* rs;           // EPI_QKV_ROPE / EPI_SWIGLU: per-row scale 1/rms (rows padded by 256), or null
+  float* x;                  // EPI_RESID: residual [M, ldc] fp32, x += A.W^T in place
+  const float* gnext;        // EPI_RESID: gain of the RMSNorm that follows (null: only x is written)
+  void* hout;                // EPI_RESID: [M, ldc] 16-bit, x * gnext (the next projection's operand)
+  float* ssp;                // EPI_RESID: [M, n_part] sums of x^2 over each 64-column slice
+  int32_t n_part;            // ldc / 64
 };
 
 hipError_t launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t s);

@@ -141,12 +141,70 @@ __device__ __forceinline__ void flush_slab(const T* slab, int rows, int cols, T*
   }
 }
 
+// `rl` and `pl` are the tile's row scales and positions in LDS (tile-relative
+// rows; unused for other epilogues).
 template <int EPI, bool H>
 __device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4][2], int64_t m0, int n0,
-                                              int64_t M, int wm, int wn, int lane, uint16_t* slice) {
+                                              int64_t M, int wm, int wn, int lane, uint16_t* slice,
+                                              const float* rl, const int32_t* pl) {
   const int l32 = lane & 31, hi = lane >> 5;
   const int nw = n0 + wn * 64;   // first GEMM column of this wave
   const int64_t mw = m0 + wm * 128;   // first row of this wave's sub-tile
+  if (EPI == EPI_RESID) {
+    // x += acc in place; with a following norm also h = x * g and, per row,
+    // the sum of x^2 over this wave's 64 columns.  A slab of 32 rows x 64
+    // columns goes through LDS; each lane then owns 4 columns of 8 rows, and
+    // the 16 lanes of a row add their squares in a fixed butterfly order.
+    float* slab = reinterpret_cast<float*>(slice);
+    const int cg = (lane & 15) * 4;
+    const bool norm = a.gnext != nullptr;
+    float4 gv = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (norm) gv = *reinterpret_cast<const float4*>(a.gnext + nw + cg);
+    uint16_t* hout = static_cast<uint16_t*>(a.hout);
+    const int part = nw >> 6;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = g * 8 + hi * 4 + e;
+          slab[r * 64 + l32] = acc[i][0][4 * g + e];
+          slab[r * 64 + 32 + l32] = acc[i][1][4 * g + e];
+        }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int r = (lane >> 4) + 4 * k;
+        const int64_t m = mw + i * 32 + r;
+        float ssq = 0.f;
+        if (m < M) {
+          float4* xp = reinterpret_cast<float4*>(a.x + m * a.ldc + nw + cg);
+          const float4 sv = *reinterpret_cast<const float4*>(slab + r * 64 + cg);
+          float4 xn = *xp;
+          xn.x += sv.x;
+          xn.y += sv.y;
+          xn.z += sv.z;
+          xn.w += sv.w;
+          *xp = xn;
+          if (norm) {
+            uint2 hv;
+            hv.x = Op16<H>::cvt(xn.x * gv.x) | (static_cast<uint32_t>(Op16<H>::cvt(xn.y * gv.y)) << 16);
+            hv.y = Op16<H>::cvt(xn.z * gv.z) | (static_cast<uint32_t>(Op16<H>::cvt(xn.w * gv.w)) << 16);
+            *reinterpret_cast<uint2*>(hout + m * a.ldc + nw + cg) = hv;
+            ssq = (xn.x * xn.x + xn.y * xn.y) + (xn.z * xn.z + xn.w * xn.w);
+          }
+        }
+        if (norm) {
+          ssq += __shfl_xor(ssq, 1);
+          ssq += __shfl_xor(ssq, 2);
+          ssq += __shfl_xor(ssq, 4);
+          ssq += __shfl_xor(ssq, 8);
+          if ((lane & 15) == 0 && m < M) a.ssp[m * a.n_part + part] = ssq;
+        }
+      }
+    }
+    return;
+  }
   if (EPI == EPI_STORE_F32) {
     // fp32: four slabs of 32 rows x 64 columns (8 KB each)
     float* slab = reinterpret_cast<float*>(slice);
@@ -187,14 +245,18 @@ __device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4
       const int i = h2 * 2 + ii;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
+        const int tr = wm * 128 + i * 32 + g * 8 + hi * 4;   // tile row of e = 0
         int4 p4 = make_int4(0, 0, 0, 0);
-        if (EPI == EPI_QKV_ROPE && !is_v)   // positions of the 4 rows e = 0..3 (buffer padded past M)
-          p4 = *reinterpret_cast<const int4*>(a.pos + mw + i * 32 + g * 8 + hi * 4);
+        if (EPI == EPI_QKV_ROPE && !is_v)   // positions of the 4 rows e = 0..3
+          p4 = *reinterpret_cast<const int4*>(pl + tr);
         const int pe[4] = {p4.x, p4.y, p4.z, p4.w};
+        float4 r4 = make_float4(1.f, 1.f, 1.f, 1.f);
+        if (a.rs) r4 = *reinterpret_cast<const float4*>(rl + tr);   // RMSNorm row scales
+        const float re[4] = {r4.x, r4.y, r4.z, r4.w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = ii * 32 + g * 8 + hi * 4 + e;   // row inside the 64-row slab
-          const float v0 = acc[i][0][4 * g + e], v1 = acc[i][1][4 * g + e];
+          const float v0 = acc[i][0][4 * g + e] * re[e], v1 = acc[i][1][4 * g + e] * re[e];
           if (EPI == EPI_SWIGLU) {
             slice[r * 32 + l32] = Op16<H>::cvt(silu_fast(v0) * v1);
           } else if (EPI == EPI_QKV_ROPE && !is_v) {
@@ -312,6 +374,8 @@ __global__ __launch_bounds__(GT) void k_gemm_bf16(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t sB0[GN * GK];
   __shared__ __attribute__((aligned(16))) uint16_t sA1[GM * GK];
   __shared__ __attribute__((aligned(16))) uint16_t sB1[GN * GK];
+  __shared__ __attribute__((aligned(16))) float rbuf[GM];     // the tile's RMSNorm row scales
+  __shared__ __attribute__((aligned(16))) int32_t pbuf[GM];   // the tile's token positions (QKV)
   const int64_t M = *a.m_ptr;
   if (M <= 0) return;
   const int tiles_n = a.N / GN;
@@ -361,7 +425,15 @@ __global__ __launch_bounds__(GT) void k_gemm_bf16(GemmArgs a) {
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
-    __syncthreads();   // stage 0 of this tile has landed
+    __syncthreads();   // stage 0 of this tile has landed; the last epilogue is done with rbuf / pbuf
+    // the tile's row scales and positions go to LDS now, so that the epilogue
+    // reads no global memory behind the next tile's prefetch
+    if (w == 0 && (EPI == EPI_QKV_ROPE || EPI == EPI_SWIGLU) && a.rs)
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(a.rs + m0 + lane * 4), (lds_ptr_t)(rbuf + lane * 4),
+                                       16, 0, 0);
+    if (w == 1 && EPI == EPI_QKV_ROPE)
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(a.pos + m0 + lane * 4), (lds_ptr_t)(pbuf + lane * 4),
+                                       16, 0, 0);
     for (int kt = 0; kt < nk; kt += 2) {
       if (kt + 1 < nk) dma_stage(sA1, sB1, ga, gb, (kt + 1) * GK, w);
       mma_stage<H>(sA0, sB0, acc, wm, wn, lane);
@@ -383,7 +455,7 @@ __global__ __launch_bounds__(GT) void k_gemm_bf16(GemmArgs a) {
     // each wave stages its output in its own 8 KB slice of stage 1, which is
     // idle until the next tile's first barrier
     uint16_t* slice = (w < 4 ? sA1 : sB1) + (w & 3) * 4096;
-    epilogue_bf16<EPI, H>(a, acc, m0, n0, M, wm, wn, lane, slice);
+    epilogue_bf16<EPI, H>(a, acc, m0, n0, M, wm, wn, lane, slice, rbuf, pbuf);
   }
 }
 
@@ -406,6 +478,11 @@ hipError_t launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t s) {
     case EPI_STORE_ACT: AIQ_LAUNCH_GEMM(EPI_STORE_ACT); break;
     case EPI_SWIGLU: AIQ_LAUNCH_GEMM(EPI_SWIGLU); break;
     case EPI_QKV_ROPE: AIQ_LAUNCH_GEMM(EPI_QKV_ROPE); break;
+    case EPI_RESID:
+      if (a.ldc != a.N || a.N % 64 || (a.gnext && (!a.hout || !a.ssp || a.n_part != a.N / 64)))
+        return hipErrorInvalidValue;
+      AIQ_LAUNCH_GEMM(EPI_RESID);
+      break;
     default: return hipErrorInvalidValue;
   }
 #undef AIQ_LAUNCH_GEMM

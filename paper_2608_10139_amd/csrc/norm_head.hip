@@ -86,6 +86,26 @@ hipError_t launch_rmsnorm(const int64_t* desc, float* x, const float* delta, con
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ row scale
+// Thread per token: the RMSNorm scale from the per-slice sums of squares that
+// the residual projection wrote, added in slice order.
+__global__ __launch_bounds__(256) void k_row_scale(const int64_t* desc, const float* ssp, int32_t n_part, int32_t d,
+                                                   float eps, float* rs) {
+  const int64_t nt = desc[D_NTOK];
+  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < nt; t += (int64_t)gridDim.x * blockDim.x) {
+    const float* p = ssp + t * n_part;
+    float ss = 0.f;
+    for (int k = 0; k < n_part; ++k) ss += p[k];
+    rs[t] = 1.0f / sqrtf(ss / static_cast<float>(d) + eps);
+  }
+}
+
+hipError_t launch_row_scale(const int64_t* desc, const float* ssp, int32_t n_part, int32_t d, float eps,
+                            float* rs, int64_t t_cap, hipStream_t s) {
+  hipLaunchKernelGGL(k_row_scale, dim3(grid_for(t_cap, 256, 4096)), dim3(256), 0, s, desc, ssp, n_part, d, eps, rs);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ label head + decision
 // Wave per sequence of the chunk.  label_out / logits_out are indexed by the
 // global sequence number (seq_begin + local index).

@@ -292,44 +292,67 @@ hipError_t launch_rope_table(int32_t max_pos, int32_t half, double theta, int32_
 
 // ------------------------------------------------------------------ embedding
 // One workgroup per chunk token (grid-stride): x[t, :] = E[tok, :] in fp32 and
-// pos[t] = position of the token inside its own sequence.
+// pos[t] = position of the token inside its own sequence.  With a norm gain
+// `g` (MFMA path) the workgroup also writes h[t, :] = x * g in 16 bits and
+// rs[t] = 1 / sqrt(mean(x^2) + eps): the first RMSNorm, applied by the first
+// projection.
+template <bool NORM>
 __global__ __launch_bounds__(256) void k_embed(const int64_t* desc, const int64_t* cu, const int32_t* packed,
                                                const void* emb, int32_t wdtype, int32_t d, int32_t vocab,
-                                               float* x, int32_t* pos, int64_t* ctr) {
+                                               float* x, int32_t* pos, int64_t* ctr, const float* g, float eps,
+                                               void* h, int32_t h_act, float* rs) {
+  __shared__ float part[4];
   const int64_t tb = desc[D_TOK_BEGIN], nt = desc[D_NTOK], sb = desc[D_SEQ_BEGIN], ns = desc[D_NSEQ];
   for (int64_t t = blockIdx.x; t < nt; t += gridDim.x) {
-    const int64_t g = tb + t;
-    int32_t tok = packed[g];
+    const int64_t gt = tb + t;
+    int32_t tok = packed[gt];
     if (tok < 0 || tok >= vocab) {   // only reachable through caller-packed batches
       if (threadIdx.x == 0) set_status(ctr, AIQ_DEV_TOKEN_RANGE);
       tok = 0;
     }
     if (threadIdx.x == 0) {
-      int64_t lo = sb, hi = sb + ns - 1;   // last i with cu[i] <= g
+      int64_t lo = sb, hi = sb + ns - 1;   // last i with cu[i] <= gt
       while (lo < hi) {
         const int64_t mid = (lo + hi + 1) >> 1;
-        if (cu[mid] <= g) lo = mid;
+        if (cu[mid] <= gt) lo = mid;
         else hi = mid - 1;
       }
-      pos[t] = static_cast<int32_t>(g - cu[lo]);
+      pos[t] = static_cast<int32_t>(gt - cu[lo]);
     }
     float* xr = x + t * d;
-    if (wdtype == AIQ_BF16 || wdtype == AIQ_F16) {
-      const int ea = wdtype == AIQ_F16 ? ACT_F16 : ACT_BF16;
-      const uint16_t* er = static_cast<const uint16_t*>(emb) + static_cast<int64_t>(tok) * d;
-      for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
+    float ssq = 0.f;
+    for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
+      float4 o;
+      if (wdtype == AIQ_BF16 || wdtype == AIQ_F16) {
+        const int ea = wdtype == AIQ_F16 ? ACT_F16 : ACT_BF16;
+        const uint16_t* er = static_cast<const uint16_t*>(emb) + static_cast<int64_t>(tok) * d;
         const uint2 v = *reinterpret_cast<const uint2*>(er + c);
-        float4 o;
         o.x = act2f(static_cast<uint16_t>(v.x & 0xFFFFu), ea);
         o.y = act2f(static_cast<uint16_t>(v.x >> 16), ea);
         o.z = act2f(static_cast<uint16_t>(v.y & 0xFFFFu), ea);
         o.w = act2f(static_cast<uint16_t>(v.y >> 16), ea);
-        *reinterpret_cast<float4*>(xr + c) = o;
+      } else {
+        o = *reinterpret_cast<const float4*>(static_cast<const float*>(emb) + static_cast<int64_t>(tok) * d + c);
       }
-    } else {
-      const float* er = static_cast<const float*>(emb) + static_cast<int64_t>(tok) * d;
-      for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4)
-        *reinterpret_cast<float4*>(xr + c) = *reinterpret_cast<const float4*>(er + c);
+      *reinterpret_cast<float4*>(xr + c) = o;
+      if (NORM) {
+        const float4 gv = *reinterpret_cast<const float4*>(g + c);
+        uint2 hv;
+        hv.x = f2act(o.x * gv.x, h_act) | (static_cast<uint32_t>(f2act(o.y * gv.y, h_act)) << 16);
+        hv.y = f2act(o.z * gv.z, h_act) | (static_cast<uint32_t>(f2act(o.w * gv.w, h_act)) << 16);
+        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(h) + t * d + c) = hv;
+        ssq += (o.x * o.x + o.y * o.y) + (o.z * o.z + o.w * o.w);
+      }
+    }
+    if (NORM) {
+      // fixed-order block reduction: waves, then the 4 wave sums in order
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) ssq += __shfl_xor(ssq, o);
+      if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ssq;
+      __syncthreads();
+      if (threadIdx.x == 0)
+        rs[t] = 1.0f / sqrtf(((part[0] + part[1]) + (part[2] + part[3])) / static_cast<float>(d) + eps);
+      __syncthreads();
     }
   }
 }
@@ -337,8 +360,18 @@ __global__ __launch_bounds__(256) void k_embed(const int64_t* desc, const int64_
 hipError_t launch_embed(const int64_t* desc, const int64_t* cu, const int32_t* packed,
                         const void* emb, int32_t wdtype, int32_t d, int32_t vocab, float* x, int32_t* pos,
                         int64_t* ctr, int64_t t_cap, hipStream_t s) {
-  hipLaunchKernelGGL(k_embed, dim3(grid_for(t_cap, 1, 8192)), dim3(256), 0, s, desc, cu, packed, emb, wdtype,
-                     d, vocab, x, pos, ctr);
+  hipLaunchKernelGGL(k_embed<false>, dim3(grid_for(t_cap, 1, 8192)), dim3(256), 0, s, desc, cu, packed, emb,
+                     wdtype, d, vocab, x, pos, ctr, nullptr, 0.f, nullptr, 0, nullptr);
+  return hipGetLastError();
+}
+
+hipError_t launch_embed_norm(const int64_t* desc, const int64_t* cu, const int32_t* packed, const void* emb,
+                             int32_t wdtype, int32_t d, int32_t vocab, float* x, int32_t* pos, int64_t* ctr,
+                             const float* g, float eps, void* h, int32_t h_act, float* rs, int64_t t_cap,
+                             hipStream_t s) {
+  if (h_act == ACT_F32) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_embed<true>, dim3(grid_for(t_cap, 1, 8192)), dim3(256), 0, s, desc, cu, packed, emb,
+                     wdtype, d, vocab, x, pos, ctr, g, eps, h, h_act, rs);
   return hipGetLastError();
 }
 
