@@ -141,12 +141,16 @@ __device__ __forceinline__ void flush_slab(const T* slab, int rows, int cols, T*
   }
 }
 
-// `rl` and `pl` are the tile's row scales and positions in LDS (tile-relative
-// rows; unused for other epilogues).
-template <int EPI, bool H>
+// `rl` holds the tile's row scales (QKV, SwiGLU) or the following norm's gain
+// for the tile's columns (residual), `pl` the tile's positions, both in LDS;
+// `rev` the rotary frequencies of this lane's dims (revolutions per position)
+// for the first and second 64-dim half of a head.  `prefetch` issues the next
+// tile's first loads: the residual epilogue calls it after its first loads of
+// x, so that those do not queue behind it; the others call it first.
+template <int EPI, bool H, typename Prefetch>
 __device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4][2], int64_t m0, int n0,
                                               int64_t M, int wm, int wn, int lane, uint16_t* slice,
-                                              const float* rl, const int32_t* pl) {
+                                              const float* rl, const int32_t* pl, float2 rev, Prefetch prefetch) {
   const int l32 = lane & 31, hi = lane >> 5;
   const int nw = n0 + wn * 64;   // first GEMM column of this wave
   const int64_t mw = m0 + wm * 128;   // first row of this wave's sub-tile
@@ -154,14 +158,28 @@ __device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4
     // x += acc in place; with a following norm also h = x * g and, per row,
     // the sum of x^2 over this wave's 64 columns.  A slab of 32 rows x 64
     // columns goes through LDS; each lane then owns 4 columns of 8 rows, and
-    // the 16 lanes of a row add their squares in a fixed butterfly order.
+    // the 16 lanes of a row add their squares in a fixed butterfly order.  A
+    // row's x for the next slab is read as soon as its slot is free, so those
+    // reads are in flight while the rest of the slab is processed.
     float* slab = reinterpret_cast<float*>(slice);
     const int cg = (lane & 15) * 4;
     const bool norm = a.gnext != nullptr;
-    float4 gv = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (norm) gv = *reinterpret_cast<const float4*>(a.gnext + nw + cg);
     uint16_t* hout = static_cast<uint16_t*>(a.hout);
     const int part = nw >> 6;
+    auto row_of = [&](int i, int k) { return mw + i * 32 + (lane >> 4) + 4 * k; };
+    auto load_x = [&](int i, float4 (&v)[8]) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        int64_t m = row_of(i, k);
+        if (m > M - 1) m = M - 1;   // in bounds; the value is not used
+        v[k] = *reinterpret_cast<const float4*>(a.x + m * a.ldc + nw + cg);
+      }
+    };
+    float4 xo[8];
+    load_x(0, xo);
+    prefetch();
+    float4 gv = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (norm) gv = *reinterpret_cast<const float4*>(rl + (nw - n0) + cg);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
 #pragma unroll
@@ -175,17 +193,16 @@ __device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
         const int r = (lane >> 4) + 4 * k;
-        const int64_t m = mw + i * 32 + r;
+        const int64_t m = row_of(i, k);
         float ssq = 0.f;
         if (m < M) {
-          float4* xp = reinterpret_cast<float4*>(a.x + m * a.ldc + nw + cg);
           const float4 sv = *reinterpret_cast<const float4*>(slab + r * 64 + cg);
-          float4 xn = *xp;
+          float4 xn = xo[k];
           xn.x += sv.x;
           xn.y += sv.y;
           xn.z += sv.z;
           xn.w += sv.w;
-          *xp = xn;
+          *reinterpret_cast<float4*>(a.x + m * a.ldc + nw + cg) = xn;
           if (norm) {
             uint2 hv;
             hv.x = Op16<H>::cvt(xn.x * gv.x) | (static_cast<uint32_t>(Op16<H>::cvt(xn.y * gv.y)) << 16);
@@ -201,10 +218,16 @@ __device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4
           ssq += __shfl_xor(ssq, 8);
           if ((lane & 15) == 0 && m < M) a.ssp[m * a.n_part + part] = ssq;
         }
+        if (i < 3) {   // the same row slot of the next slab
+          int64_t mn = row_of(i + 1, k);
+          if (mn > M - 1) mn = M - 1;
+          xo[k] = *reinterpret_cast<const float4*>(a.x + mn * a.ldc + nw + cg);
+        }
       }
     }
     return;
   }
+  prefetch();
   if (EPI == EPI_STORE_F32) {
     // fp32: four slabs of 32 rows x 64 columns (8 KB each)
     float* slab = reinterpret_cast<float*>(slice);
@@ -235,7 +258,7 @@ __device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4
     hh = (c % a.hd) >> 6;   // 0 except the second half-wave of a 128-dim head
     half = a.hd >> 1;
     // rotary frequency of this lane's lower-half dim, in revolutions per position
-    rev_per_pos = a.rope_rev[hh * 32 + l32];
+    rev_per_pos = hh ? rev.y : rev.x;
   }
   constexpr int COLS = EPI == EPI_SWIGLU ? 32 : 64;
 #pragma unroll
@@ -405,6 +428,12 @@ __global__ __launch_bounds__(GT) void k_gemm_bf16(GemmArgs a) {
   };
   int64_t q = blockIdx.x >> 3;
   if (q >= count_x) return;
+  float2 rev = make_float2(0.f, 0.f);
+  if (EPI == EPI_QKV_ROPE) {
+    const int l32 = lane & 31;
+    rev.x = a.rope_rev[l32];
+    if (a.hd == 128) rev.y = a.rope_rev[32 + l32];
+  }
   const uint16_t* ga[4];
   const uint16_t* gb[4];
   {
@@ -431,6 +460,9 @@ __global__ __launch_bounds__(GT) void k_gemm_bf16(GemmArgs a) {
     if (w == 0 && (EPI == EPI_QKV_ROPE || EPI == EPI_SWIGLU) && a.rs)
       __builtin_amdgcn_global_load_lds(static_cast<const void*>(a.rs + m0 + lane * 4), (lds_ptr_t)(rbuf + lane * 4),
                                        16, 0, 0);
+    if (w == 0 && EPI == EPI_RESID && a.gnext)   // the following norm's gain for the tile's columns
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(a.gnext + n0 + lane * 4),
+                                       (lds_ptr_t)(rbuf + lane * 4), 16, 0, 0);
     if (w == 1 && EPI == EPI_QKV_ROPE)
       __builtin_amdgcn_global_load_lds(static_cast<const void*>(a.pos + m0 + lane * 4), (lds_ptr_t)(pbuf + lane * 4),
                                        16, 0, 0);
@@ -444,18 +476,21 @@ __global__ __launch_bounds__(GT) void k_gemm_bf16(GemmArgs a) {
         __syncthreads();
       }
     }
-    // stage 0 is free: start the next tile's first k-step under the epilogue
-    if (q + per_xcd < count_x) {
-      int64_t m1;
-      int n1;
-      tile_mn(q + per_xcd, m1, n1);
-      tile_sources<EPI>(a, A, M, m1, n1, w, lane, ga, gb);
-      dma_stage(sA0, sB0, ga, gb, 0, w);
-    }
+    // stage 0 is free: the next tile's first k-step loads under the epilogue
+    const bool more = q + per_xcd < count_x;
+    auto prefetch = [&]() {
+      if (more) {
+        int64_t m1;
+        int n1;
+        tile_mn(q + per_xcd, m1, n1);
+        tile_sources<EPI>(a, A, M, m1, n1, w, lane, ga, gb);
+        dma_stage(sA0, sB0, ga, gb, 0, w);
+      }
+    };
     // each wave stages its output in its own 8 KB slice of stage 1, which is
     // idle until the next tile's first barrier
     uint16_t* slice = (w < 4 ? sA1 : sB1) + (w & 3) * 4096;
-    epilogue_bf16<EPI, H>(a, acc, m0, n0, M, wm, wn, lane, slice, rbuf, pbuf);
+    epilogue_bf16<EPI, H>(a, acc, m0, n0, M, wm, wn, lane, slice, rbuf, pbuf, rev, prefetch);
   }
 }
 

@@ -291,37 +291,49 @@ hipError_t launch_rope_table(int32_t max_pos, int32_t half, double theta, int32_
 }
 
 // ------------------------------------------------------------------ embedding
-// One workgroup per chunk token (grid-stride): x[t, :] = E[tok, :] in fp32 and
-// pos[t] = position of the token inside its own sequence.  With a norm gain
-// `g` (MFMA path) the workgroup also writes h[t, :] = x * g in 16 bits and
-// rs[t] = 1 / sqrt(mean(x^2) + eps): the first RMSNorm, applied by the first
-// projection.
+// One wave per chunk token (grid-stride): x[t, :] = E[tok, :] in fp32 and
+// pos[t] = position of the token inside its own sequence, found by a 64-way
+// search of the chunk's sequence offsets (each round narrows the range 64x).
+// With a norm gain `g` (MFMA path) the wave also writes h[t, :] = x * g in 16
+// bits and rs[t] = 1 / sqrt(mean(x^2) + eps): the first RMSNorm, applied by
+// the first projection.
+__device__ __forceinline__ int64_t seq_of(const int64_t* cu, int64_t sb, int64_t ns, int64_t gt, int lane) {
+  int64_t lo = sb, n = ns;   // answer in [lo, lo + n): the last i with cu[i] <= gt
+  while (n > 1) {
+    const int64_t step = (n + 63) / 64;
+    const int64_t i = lo + lane * step;
+    const bool le = i < lo + n && cu[i] <= gt;
+    const uint64_t b = __ballot(le);
+    if (b == 0) break;   // cannot happen (cu[lo] <= gt holds throughout); keeps the index in range
+    const int last = 63 - __builtin_clzll(b);
+    lo += static_cast<int64_t>(last) * step;
+    const int64_t rem = n - static_cast<int64_t>(last) * step;
+    n = rem < step ? rem : step;
+  }
+  return lo;
+}
+
 template <bool NORM>
 __global__ __launch_bounds__(256) void k_embed(const int64_t* desc, const int64_t* cu, const int32_t* packed,
                                                const void* emb, int32_t wdtype, int32_t d, int32_t vocab,
                                                float* x, int32_t* pos, int64_t* ctr, const float* g, float eps,
                                                void* h, int32_t h_act, float* rs) {
-  __shared__ float part[4];
   const int64_t tb = desc[D_TOK_BEGIN], nt = desc[D_NTOK], sb = desc[D_SEQ_BEGIN], ns = desc[D_NSEQ];
-  for (int64_t t = blockIdx.x; t < nt; t += gridDim.x) {
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6;
+  const int64_t n_waves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t t = wave; t < nt; t += n_waves) {
     const int64_t gt = tb + t;
     int32_t tok = packed[gt];
     if (tok < 0 || tok >= vocab) {   // only reachable through caller-packed batches
-      if (threadIdx.x == 0) set_status(ctr, AIQ_DEV_TOKEN_RANGE);
+      if (lane == 0) set_status(ctr, AIQ_DEV_TOKEN_RANGE);
       tok = 0;
     }
-    if (threadIdx.x == 0) {
-      int64_t lo = sb, hi = sb + ns - 1;   // last i with cu[i] <= gt
-      while (lo < hi) {
-        const int64_t mid = (lo + hi + 1) >> 1;
-        if (cu[mid] <= gt) lo = mid;
-        else hi = mid - 1;
-      }
-      pos[t] = static_cast<int32_t>(gt - cu[lo]);
-    }
+    const int64_t sq = seq_of(cu, sb, ns, gt, lane);
+    if (lane == 0) pos[t] = static_cast<int32_t>(gt - cu[sq]);
     float* xr = x + t * d;
     float ssq = 0.f;
-    for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
+    for (int c = lane * 4; c < d; c += 256) {
       float4 o;
       if (wdtype == AIQ_BF16 || wdtype == AIQ_F16) {
         const int ea = wdtype == AIQ_F16 ? ACT_F16 : ACT_BF16;
@@ -345,14 +357,9 @@ __global__ __launch_bounds__(256) void k_embed(const int64_t* desc, const int64_
       }
     }
     if (NORM) {
-      // fixed-order block reduction: waves, then the 4 wave sums in order
 #pragma unroll
       for (int o = 32; o > 0; o >>= 1) ssq += __shfl_xor(ssq, o);
-      if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ssq;
-      __syncthreads();
-      if (threadIdx.x == 0)
-        rs[t] = 1.0f / sqrtf(((part[0] + part[1]) + (part[2] + part[3])) / static_cast<float>(d) + eps);
-      __syncthreads();
+      if (lane == 0) rs[t] = 1.0f / sqrtf(ssq / static_cast<float>(d) + eps);
     }
   }
 }
@@ -360,7 +367,7 @@ __global__ __launch_bounds__(256) void k_embed(const int64_t* desc, const int64_
 hipError_t launch_embed(const int64_t* desc, const int64_t* cu, const int32_t* packed,
                         const void* emb, int32_t wdtype, int32_t d, int32_t vocab, float* x, int32_t* pos,
                         int64_t* ctr, int64_t t_cap, hipStream_t s) {
-  hipLaunchKernelGGL(k_embed<false>, dim3(grid_for(t_cap, 1, 8192)), dim3(256), 0, s, desc, cu, packed, emb,
+  hipLaunchKernelGGL(k_embed<false>, dim3(grid_for(t_cap, 4, 8192)), dim3(256), 0, s, desc, cu, packed, emb,
                      wdtype, d, vocab, x, pos, ctr, nullptr, 0.f, nullptr, 0, nullptr);
   return hipGetLastError();
 }
@@ -370,7 +377,7 @@ hipError_t launch_embed_norm(const int64_t* desc, const int64_t* cu, const int32
                              const float* g, float eps, void* h, int32_t h_act, float* rs, int64_t t_cap,
                              hipStream_t s) {
   if (h_act == ACT_F32) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_embed<true>, dim3(grid_for(t_cap, 1, 8192)), dim3(256), 0, s, desc, cu, packed, emb,
+  hipLaunchKernelGGL(k_embed<true>, dim3(grid_for(t_cap, 4, 8192)), dim3(256), 0, s, desc, cu, packed, emb,
                      wdtype, d, vocab, x, pos, ctr, g, eps, h, h_act, rs);
   return hipGetLastError();
 }
