@@ -37,6 +37,24 @@ PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3
 PEAK_HBM_GBPS = 8000.0
 
+# HBM bytes per launch of the gate/up GEMM on the reviews workload (472,953
+# tokens), from rocprofv3 FETCH_SIZE and WRITE_SIZE runs scaled by a plain
+# 1 GiB copy (x2.000 and x1.000); summary and commands in
+# profiles/reviews_pipeline_hbm_traffic.md.  Valid only for the kernel source
+# it was measured on: reported as null once gemm.hip, dev_util.h or the
+# GemmArgs declaration change.
+GATE_UP_TRAFFIC = {"workload": "reviews", "tokens": 472953, "bytes": 4844238511,
+                   "source_sha256": "d2801c7fd2ba1f0f892e625666cd9c89f86237fa717c812ae04512cdd7cb2ea8"}
+
+
+def gemm_source_sha256() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("gemm.hip", "aiq_internal.h", "dev_util.h"):
+        with open(os.path.join(ROOT, "paper_2608_10139_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
@@ -296,6 +314,10 @@ def main(argv=None) -> int:
     rel_bytes = n_rows * col_bytes + 4 * len(sel)
     rel_ms = float(np.sum(kinds.get(B.AIQ_K_REL, [0.0])))
 
+    traffic = None
+    if (a.workload == GATE_UP_TRAFFIC["workload"] and T == GATE_UP_TRAFFIC["tokens"]
+            and gemm_source_sha256() == GATE_UP_TRAFFIC["source_sha256"]):
+        traffic = GATE_UP_TRAFFIC["bytes"]
     result = {
         "metric": METRIC, "value": round(n_rows / (ms_step * 1e-3), 2), "unit": "rows/s",
         "n_gpus": 1, "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_step, 4),
@@ -314,7 +336,7 @@ def main(argv=None) -> int:
         "relational_gbps": round(rel_bytes / (rel_ms * 1e-3) / 1e9, 2) if rel_ms > 0 else None,
         "roofline": {"bound": "mfma", "kernel": "k_gemm_bf16<EPI_SWIGLU> (gate/up projection + SwiGLU)",
                      "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
-                     "frac": round(achieved / peak, 4), "traffic": None,
+                     "frac": round(achieved / peak, 4), "traffic": traffic,
                      "launches": n_up, "avg_launch_ms": round(up_avg_ms, 5),
                      "flops_per_launch": up_flops_per_launch},
     }
