@@ -207,6 +207,63 @@ def split_baseline_leg(tables, model, q, dm, B, torch, micro=128) -> dict:
             "micro_batch": micro, "logits": f"fp32 [{micro}, {V}] per micro-batch, D2H"}
 
 
+def relational_scale_leg(B, torch, sizes, thresholds, steps: int = 5) -> list:
+    """The relational part alone (WHERE c < k, stable compaction, per-row
+    token counts) on the 1M-row sweep table's generator scaled to `sizes` rows
+    (columns c and offsets; no token list), through a relational-only plan.
+    Algorithmic bytes per run: 4 B of c per row + per selected row 4 B id
+    written, 16 B of offsets read, 8 B of cu_seqlens written.  The counts are
+    checked against numpy on the host."""
+    import dataclasses
+    from paper_2608_10139_amd.device import DeviceModel, DeviceQuery
+    from synth import WORKLOADS
+    from synth.configs import Pred, Query
+    from synth.gen import make_model, make_probe
+
+    tiny = make_model(WORKLOADS["tiny"].model)
+    dm = DeviceModel(tiny)
+    out = []
+    for n in sizes:
+        log(f"[bench] relational scale: generating {n} rows (sweep-table generator, c and lengths)")
+        spec = dataclasses.replace(WORKLOADS["sweep3b"].table, n_rows=n)
+        probe = make_probe(spec, with_tokens=False)
+        tables = {"probe": probe, "build": None, "prefix": np.zeros(0, np.int32)}
+        for k in thresholds:
+            q = Query(preds=(Pred("c", "lt", k),), labels=(1, 2), decision="binary_gt", agg="count")
+            dq = DeviceQuery(tables, tiny, q, dmodel=dm, relational_only=True, want_sel=False)
+            dq.run()
+            torch.cuda.synchronize()
+            res = dq.results()
+            want = probe["c"] < k
+            n_sel = int(np.count_nonzero(want))
+            if res["status"] != 0 or res["n_selected"] != n_sel or res["n_tokens"] != int(probe["len"][want].sum()):
+                raise RuntimeError(f"relational scale run disagrees with numpy at n={n}, c < {k}")
+            ev = HipEvents(2 * 8 * steps)
+            tr = make_trace(B, ev, (1 << B.AIQ_K_REL) | (1 << B.AIQ_K_PACK) | (1 << B.AIQ_K_AGG))
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(steps):
+                dq.run(trace=tr)
+            torch.cuda.synchronize()
+            wall = (time.perf_counter() - t0) / steps * 1e3
+            kinds = per_kind_ms(B, tr, ev)
+            ev.close()
+            rel = float(np.sum(kinds.get(B.AIQ_K_REL, []))) / steps
+            pack = float(np.sum(kinds.get(B.AIQ_K_PACK, []))) / steps
+            agg = float(np.sum(kinds.get(B.AIQ_K_AGG, []))) / steps
+            nbytes = 4 * n + 28 * n_sel
+            gbps = nbytes / ((rel + pack) * 1e-3) / 1e9
+            out.append({"rows": n, "predicate": f"c < {k}", "selected": n_sel, "tokens": res["n_tokens"],
+                        "where_compact_ms": round(rel, 4), "token_counts_ms": round(pack, 4),
+                        "ids_out_ms": round(agg, 4), "run_ms": round(wall, 4),
+                        "algorithmic_bytes": nbytes, "gbps": round(gbps, 1),
+                        "hbm_frac": round(gbps / PEAK_HBM_GBPS, 4)})
+            log(f"[bench]   n={n} c<{k}: {out[-1]}")
+            dq.close()
+        del probe, tables
+    return out
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -218,6 +275,10 @@ def main(argv=None) -> int:
     ap.add_argument("--cpu-rows", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-split", action="store_true")
+    ap.add_argument("--relational-scale", action="store_true",
+                    help="only the relational part at 2^26 and 2^28 rows (relational-only plans); one JSON line")
+    ap.add_argument("--no-relational-scale", action="store_true",
+                    help="skip the 2^26-row relational run of the default line")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (3 times): the reference "
                          "for scaling HBM traffic counters")
@@ -239,6 +300,19 @@ def main(argv=None) -> int:
         return 0
     from paper_2608_10139_amd import binding as B
     from paper_2608_10139_amd.device import DeviceModel, DeviceQuery
+    if a.relational_scale:
+        torch.cuda.set_device(0)
+        runs = relational_scale_leg(B, torch, [1 << 26, 1 << 28], [10, 1000], steps=a.steps)
+        best = max(runs, key=lambda r: r["gbps"])
+        print(json.dumps({"metric": "relational stages (WHERE + stable compaction + token counts) HBM GB/s",
+                          "value": best["gbps"], "unit": "GB/s", "n_gpus": 1, "steps": a.steps, "warmup": 1,
+                          "higher_is_better": True, "dtype": "int32", "data": "synthetic",
+                          "config": {"workload": "sweep-table generator scaled to 2^26 and 2^28 rows, "
+                                                 "c and offsets only, relational-only plans"},
+                          "roofline": {"bound": "hbm", "achieved": best["gbps"], "peak": PEAK_HBM_GBPS,
+                                       "unit": "GB/s", "frac": best["hbm_frac"], "traffic": None},
+                          "runs": runs}), flush=True)
+        return 0
     from synth import WORKLOADS
     from synth.gen import make_model, make_tables
 
@@ -340,6 +414,8 @@ def main(argv=None) -> int:
                      "launches": n_up, "avg_launch_ms": round(up_avg_ms, 5),
                      "flops_per_launch": up_flops_per_launch},
     }
+    if not a.no_relational_scale:
+        result["relational_scale"] = relational_scale_leg(B, torch, [1 << 26], [10, 1000], steps=5)
     if not a.no_cpu_baseline:
         log("[bench] cpu baseline (oracle on a sample)")
         result["cpu_baseline"] = cpu_baseline_leg(tables, model, q, a.cpu_rows)

@@ -102,7 +102,9 @@ typedef enum aiq_logits_mode { AIQ_LOGITS_LABELS = 1, AIQ_LOGITS_FULL_VOCAB = 2 
 #define AIQ_MAX_PREFIX 64
 #define AIQ_MAX_LABELS 8
 
-/* One fixed-width column: `data` is a device array of n_rows elements. */
+/* One fixed-width column: `data` is a device array of n_rows elements,
+ * 16-byte aligned (predicates read it in 16-byte vectors; a misaligned
+ * column is rejected with AIQ_EINVAL at plan creation). */
 typedef struct aiq_col {
   const void* data;
   int32_t dtype;          /* AIQ_I8, AIQ_I16 or AIQ_I32 */
@@ -187,8 +189,22 @@ typedef struct aiq_plan_opts {
   int64_t chunk_tokens;                /* prefill chunk size in tokens; 0 = default */
   int32_t n_layers_override;           /* diagnostics: 0 = every layer, n > 0 = the first n
                                           layers, negative = no layer (embedding -> head) */
-  int32_t reserved[5];
+  int32_t flags;                       /* AIQ_PLAN_* bits */
+  int32_t reserved[4];
 } aiq_plan_opts;
+
+/*
+ * AIQ_PLAN_RELATIONAL_ONLY: aiq_run executes only the relational part of the
+ * query (Table 1: the FROM and WHERE clauses, and the join of Section 4): the
+ * predicate (+ join), the stable compaction and each selected row's token
+ * count (list length + prefix).  out->ids receives every selected row id
+ * ascending; scalars SELECTED = KEPT = their count, TOKENS = their total
+ * tokens.  No model, decision or aggregate runs (the model must still be a
+ * valid one); the query's agg must be AIQ_AGG_COUNT (else AIQ_EINVAL at plan
+ * creation); the probe table's token column is not read and may be NULL
+ * (its offsets are required).
+ */
+#define AIQ_PLAN_RELATIONAL_ONLY 1
 
 /*
  * Outputs, all device buffers owned by the caller.  Optional buffers may be

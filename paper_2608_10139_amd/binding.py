@@ -20,6 +20,7 @@ AIQ_ACT_GELU_ERF, AIQ_ACT_SWIGLU = 1, 2
 AIQ_DECIDE_BINARY_GT, AIQ_DECIDE_ARGMAX = 1, 2
 AIQ_AGG_COUNT, AIQ_AGG_AVG_LABEL_COUNT_BY, AIQ_AGG_COUNT_BY_PAYLOAD = 1, 2, 3
 AIQ_LOGITS_LABELS, AIQ_LOGITS_FULL_VOCAB = 1, 2
+AIQ_PLAN_RELATIONAL_ONLY = 1
 
 AIQ_DEV_TOKEN_RANGE, AIQ_DEV_DUP_KEY, AIQ_DEV_HASH_FULL, AIQ_DEV_IDS_CAP = 0x01, 0x02, 0x04, 0x08
 AIQ_DEV_GROUP_RANGE, AIQ_DEV_LIST_LEN, AIQ_DEV_GROUP_CAP = 0x10, 0x20, 0x40
@@ -73,8 +74,8 @@ class aiq_query(C.Structure):
 
 
 class aiq_plan_opts(C.Structure):
-    _fields_ = [("chunk_tokens", C.c_int64), ("n_layers_override", C.c_int32),
-                ("reserved", C.c_int32 * 5)]
+    _fields_ = [("chunk_tokens", C.c_int64), ("n_layers_override", C.c_int32), ("flags", C.c_int32),
+                ("reserved", C.c_int32 * 4)]
 
 
 class aiq_out(C.Structure):

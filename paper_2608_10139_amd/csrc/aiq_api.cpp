@@ -21,6 +21,7 @@ struct aiq_plan {
   aiq_model model;
   std::vector<aiq_layer> layers;
   bool has_probe = false, has_build = false, has_query = false;
+  bool rel_only = false;   // AIQ_PLAN_RELATIONAL_ONLY
   aiq_table probe{}, build{};
   std::vector<aiq_col> probe_cols, build_cols;
   aiq_query q{};
@@ -81,16 +82,18 @@ aiq_status make_preds(const aiq_pred* src, int n, const std::vector<aiq_col>& co
   return AIQ_OK;
 }
 
-aiq_status copy_table(const aiq_table* t, aiq_table* dst, std::vector<aiq_col>* cols, bool need_list) {
+// need_list: 0 no list column, 1 offsets (tokens optional), 2 offsets and tokens
+aiq_status copy_table(const aiq_table* t, aiq_table* dst, std::vector<aiq_col>* cols, int need_list) {
   if (t->n_rows < 0 || t->n_rows > INT32_MAX) return AIQ_EINVAL;
   if (t->n_cols < 0 || (t->n_cols > 0 && !t->cols)) return AIQ_EINVAL;
   cols->assign(t->cols, t->cols + t->n_cols);
   for (const aiq_col& c : *cols) {
     if (!int_dtype(c.dtype) && c.dtype != AIQ_F32) return AIQ_EINVAL;
     if (!c.data && t->n_rows > 0) return AIQ_EINVAL;
+    if (reinterpret_cast<uintptr_t>(c.data) % 16) return AIQ_EINVAL;   // columns are read in 16-byte vectors
   }
   if (need_list) {
-    if (!t->list_offsets || !t->list_tokens) return AIQ_EINVAL;
+    if (!t->list_offsets || (need_list == 2 && !t->list_tokens)) return AIQ_EINVAL;
     if (t->n_list_tokens < 0 || t->max_list_len < 1) return AIQ_EINVAL;
   }
   *dst = *t;
@@ -133,7 +136,7 @@ aiq_status validate_model(const aiq_model* m) {
 }
 
 struct Layout {
-  size_t ctr, mask, blk_cnt, blk_off, sel, payload, lens, label, logits, cu, scan_tmp, packed, hkeys, hvals,
+  size_t ctr, mask, blk_cnt, blk_off, sel, payload, lens, label, logits, cu, blk_tok, tok_off, packed, hkeys, hvals,
       bins, desc, rcos, rsin, rrev, x, delta, h, qkv, att, ffn, pos, hf, ssp, rs, total;
 };
 
@@ -178,15 +181,20 @@ Layout run_layout(const aiq_plan* p) {
   L.blk_off = c.take(static_cast<size_t>(nb + 1) * 8);
   L.sel = c.take(static_cast<size_t>(n + 1) * 4);
   L.payload = c.take(static_cast<size_t>(n + 1) * 4);
-  L.lens = c.take(static_cast<size_t>(n + 1) * 4);
+  L.lens = c.take(static_cast<size_t>(n + 24) * 4);   // read in 16-entry groups from an 8-aligned start
   L.label = c.take(static_cast<size_t>(n + 1) * 4);
   L.logits = c.take(static_cast<size_t>(n + 1) * p->q.n_labels * 4);
   L.cu = c.take(static_cast<size_t>(n + 1) * 8);
-  L.scan_tmp = c.take(static_cast<size_t>(n / 4096 + 2) * 8);
-  L.packed = c.take(static_cast<size_t>(p->t_ub + 1) * 4);
+  L.blk_tok = c.take(static_cast<size_t>(nb) * 8);
+  L.tok_off = c.take(static_cast<size_t>(nb + 1) * 8);
   const size_t hcap = p->hash_log2 ? (size_t(1) << p->hash_log2) : 1;
   L.hkeys = c.take(hcap * 4);
   L.hvals = c.take(hcap * 4);
+  if (p->rel_only) {   // no packed batch, model activations or groups
+    L.total = c.off;
+    return L;
+  }
+  L.packed = c.take(static_cast<size_t>(p->t_ub + 1) * 4);
   L.bins = c.take(static_cast<size_t>(std::max(p->q.n_group_keys, 1)) * 16);
   L.desc = c.take(static_cast<size_t>(p->n_chunks) * D_STRIDE * 8);
   L.rcos = c.take(static_cast<size_t>(p->max_seq) * (p->hd / 2) * 4);
@@ -460,7 +468,9 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
   if (probe) {
     if (!query) return fail(AIQ_EINVAL);
     p->has_probe = true;
-    st = copy_table(probe, &p->probe, &p->probe_cols, true);
+    p->rel_only = opts && (opts->flags & AIQ_PLAN_RELATIONAL_ONLY);
+    if (opts && (opts->flags & ~AIQ_PLAN_RELATIONAL_ONLY)) return fail(AIQ_EINVAL);
+    st = copy_table(probe, &p->probe, &p->probe_cols, p->rel_only ? 1 : 2);
     if (st != AIQ_OK) return fail(st);
     const aiq_query& q = p->q;
     st = make_preds(q.preds, q.n_pred, p->probe_cols, &p->probe_preds);
@@ -469,7 +479,7 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
     if ((q.join == 1) != (build != nullptr)) return fail(AIQ_EINVAL);
     if (q.join) {
       p->has_build = true;
-      st = copy_table(build, &p->build, &p->build_cols, false);
+      st = copy_table(build, &p->build, &p->build_cols, 0);
       if (st != AIQ_OK) return fail(st);
       const int nc = static_cast<int>(p->build_cols.size());
       if (q.build_key_col < 0 || q.build_key_col >= nc || q.build_payload_col < 0 || q.build_payload_col >= nc)
@@ -485,6 +495,7 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
       if (lg > 30) return fail(AIQ_EUNSUPPORTED);
       p->hash_log2 = lg;
     }
+    if (p->rel_only && q.agg != AIQ_AGG_COUNT) return fail(AIQ_EINVAL);
     switch (q.agg) {
       case AIQ_AGG_COUNT: break;
       case AIQ_AGG_AVG_LABEL_COUNT_BY:
@@ -561,7 +572,8 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
   int32_t* label = at<int32_t>(ws, L.label);
   float* logits = at<float>(ws, L.logits);
   int64_t* cu = at<int64_t>(ws, L.cu);
-  int64_t* scan_tmp = at<int64_t>(ws, L.scan_tmp);
+  int64_t* blk_tok = at<int64_t>(ws, L.blk_tok);
+  int64_t* tok_off = at<int64_t>(ws, L.tok_off);
   int32_t* packed = at<int32_t>(ws, L.packed);
   int64_t* desc = at<int64_t>(ws, L.desc);
   const int64_t n = p->n_rows;
@@ -586,14 +598,31 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
   }
   HIP_TRY(launch_row_mask(p->probe_preds, n, pkey, pkey_dt, h, p->has_build, mask, blk_cnt, s));
   HIP_TRY(launch_scan_blocks(blk_cnt, nullptr, n, blk_off, ctr + C_SEL, s));
-  HIP_TRY(launch_scatter_rows(mask, blk_off, nullptr, n, nullptr, sel, n, pkey, pkey_dt, h, p->has_build,
-                              payload, ctr, s));
+  // compaction: selected ids (straight into the caller's ids when nothing
+  // else follows), join payloads, token counts and per-block token sums
+  ScatterLens sl{p->probe.list_offsets, p->probe.max_list_len, q.n_prefix, lens, blk_tok};
+  if (p->rel_only)
+    HIP_TRY(launch_scatter_rows(mask, blk_off, nullptr, n, nullptr, out->ids, out->ids_cap, pkey, pkey_dt, h,
+                                p->has_build, payload, ctr, s,
+                                out->sel_cap > 0 ? out->sel_ids : nullptr, out->sel_cap, sl));
+  else
+    HIP_TRY(launch_scatter_rows(mask, blk_off, nullptr, n, nullptr, sel, n, pkey, pkey_dt, h, p->has_build,
+                                payload, ctr, s, nullptr, 0, sl));
   tr.end();
-  // ---- pack: lengths, offsets, tokens, chunk descriptors
+  // ---- token offsets of the selected rows
   tr.begin(AIQ_K_PACK);
-  HIP_TRY(launch_seq_lengths(sel, ctr + C_SEL, n, p->probe.list_offsets, p->probe.max_list_len, q.n_prefix, lens,
-                             ctr, s));
-  HIP_TRY(launch_scan_lengths(lens, ctr + C_SEL, n, scan_tmp, cu, ctr + C_TOK, s));
+  HIP_TRY(launch_scan_blocks64(blk_tok, nullptr, n, tok_off, ctr + C_TOK, s));
+  HIP_TRY(launch_cu_from_blocks(lens, blk_off, tok_off, n, cu, s));
+  if (p->rel_only) {
+    // relational part only: every selected id is kept
+    tr.end();
+    tr.begin(AIQ_K_AGG);
+    HIP_TRY(launch_keep_selected(ctr, out->ids_cap, s));
+    HIP_TRY(launch_finalize(ctr, out->scalars, s));
+    tr.end();
+    return AIQ_OK;
+  }
+  // ---- pack: tokens, chunk descriptors
   HIP_TRY(launch_gather_tokens(sel, ctr + C_SEL, n, p->probe.list_offsets, p->probe.list_tokens, cu, p->prefix,
                                p->model.vocab, p->t_ub, packed, ctr, s));
   HIP_TRY(launch_chunk_desc(cu, ctr + C_SEL, p->chunk_tokens, p->n_chunks, p->t_ub, desc, s));

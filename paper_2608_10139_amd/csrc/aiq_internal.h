@@ -46,11 +46,11 @@ struct HashArgs {
 
 constexpr int32_t HASH_EMPTY = INT32_MIN;
 
-// relational block geometry: 256 threads x 8 rows
+// relational block geometry: 256 threads x 32 rows
 constexpr int REL_THREADS = 256;
-constexpr int REL_ROWS_PER_THREAD = 8;
-constexpr int REL_ROWS_PER_BLOCK = REL_THREADS * REL_ROWS_PER_THREAD;   // 2048
-constexpr int REL_WORDS_PER_BLOCK = REL_ROWS_PER_BLOCK / 64;             // 32
+constexpr int REL_ROWS_PER_THREAD = 32;
+constexpr int REL_ROWS_PER_BLOCK = REL_THREADS * REL_ROWS_PER_THREAD;   // 8192
+constexpr int REL_WORDS_PER_BLOCK = REL_ROWS_PER_BLOCK / 64;             // 128
 
 // ---------------------------------------------------------------- launchers
 // Every launcher enqueues on `s` and returns hipGetLastError().
@@ -66,13 +66,37 @@ hipError_t launch_row_mask(const DPredList& preds, int64_t n_rows, const void* p
                            int32_t* blk_cnt, hipStream_t s);
 hipError_t launch_label_mask(const int32_t* label, const int64_t* n_ptr, int64_t n_ub,
                              uint64_t* mask, int32_t* blk_cnt, hipStream_t s);
+// Exclusive scan of per-block values (one per REL_ROWS_PER_BLOCK rows of n):
+// off[b] = sum of v[< b], off[nb] = *total_out = the sum of all.
 hipError_t launch_scan_blocks(const int32_t* blk_cnt, const int64_t* n_ptr, int64_t n_ub,
                               int64_t* blk_off, int64_t* total_out, hipStream_t s);
+hipError_t launch_scan_blocks64(const int64_t* blk_val, const int64_t* n_ptr, int64_t n_ub,
+                                int64_t* blk_off, int64_t* total_out, hipStream_t s);
+// Token counts of the selected rows, produced while compacting them: for
+// output position i of row r, lens[i] = min(off[r+1] - off[r], max_len) +
+// n_prefix (a list longer than max_len, or negative, flags AIQ_DEV_LIST_LEN),
+// and blk_tok[b] = sum of lens over the rows of input block b.
+struct ScatterLens {
+  const int64_t* off;        // null: no lengths
+  int32_t max_len, n_prefix;
+  int32_t* lens;             // [n] by output position
+  int64_t* blk_tok;          // [n_blocks]
+};
+// Stable compaction of the mask: out_ids[pos] = src_ids ? src_ids[r] : r for
+// every set bit r, in row order (positions >= out_cap dropped and flagged);
+// optionally a second copy (out_ids2, cap2), the join payload and lengths.
 hipError_t launch_scatter_rows(const uint64_t* mask, const int64_t* blk_off, const int64_t* n_ptr,
                                int64_t n_ub, const int32_t* src_ids, int32_t* out_ids,
                                int64_t out_cap, const void* probe_key, int32_t probe_key_dtype,
                                HashArgs h, int join, int32_t* out_payload, int64_t* ctr,
-                               hipStream_t s);
+                               hipStream_t s, int32_t* out_ids2 = nullptr, int64_t out_cap2 = 0,
+                               ScatterLens lens = ScatterLens{});
+// cu[0] = 0 and cu[i + 1] = cu[i] + lens[i] for the selected rows, from the
+// per-block token offsets of the compaction (tok_off = scan of blk_tok).
+hipError_t launch_cu_from_blocks(const int32_t* lens, const int64_t* blk_off, const int64_t* tok_off,
+                                 int64_t n_ub, int64_t* cu, hipStream_t s);
+// ctr[C_KEPT] = ctr[C_SEL] (every selected row kept), flagged if above cap.
+hipError_t launch_keep_selected(int64_t* ctr, int64_t cap, hipStream_t s);
 hipError_t launch_group_accumulate(const int32_t* sel, const int32_t* label, const int32_t* payload,
                                    const uint8_t* keep_by_label, const int64_t* n_ptr, int64_t n_ub,
                                    const void* key_col, int32_t key_dtype, int mode,
@@ -87,12 +111,6 @@ hipError_t launch_copy_f32(const float* src, const int64_t* n_ptr, int64_t n_ub,
 hipError_t launch_finalize(const int64_t* ctr, int64_t* scalars, hipStream_t s);
 
 // packing / chunking
-hipError_t launch_seq_lengths(const int32_t* sel, const int64_t* n_ptr, int64_t n_ub,
-                              const int64_t* offsets, int32_t max_len, int32_t n_prefix,
-                              int32_t* lens, int64_t* ctr, hipStream_t s);
-hipError_t launch_scan_lengths(const int32_t* lens, const int64_t* n_ptr, int64_t n_ub,
-                               int64_t* block_tmp, int64_t* cu, int64_t* total_out,
-                               hipStream_t s);
 struct Prefix {
   int32_t n;
   int32_t tok[AIQ_MAX_PREFIX];

@@ -24,126 +24,6 @@ __device__ __forceinline__ void set_status(int64_t* ctr, int64_t bits) {
   atomicOr(reinterpret_cast<unsigned long long*>(ctr + C_STATUS), static_cast<unsigned long long>(bits));
 }
 
-// ------------------------------------------------------------------ lengths
-__global__ void k_seq_lengths(const int32_t* sel, const int64_t* n_ptr, const int64_t* off, int32_t max_len,
-                              int32_t n_prefix, int32_t* lens, int64_t* ctr) {
-  const int64_t n = *n_ptr;
-  bool bad = false;
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t r = sel[i];
-    int64_t len = off[r + 1] - off[r];
-    if (len < 0 || len > max_len) {
-      bad = true;
-      len = len < 0 ? 0 : max_len;
-    }
-    lens[i] = static_cast<int32_t>(len) + n_prefix;
-  }
-  if (bad) set_status(ctr, AIQ_DEV_LIST_LEN);
-}
-
-hipError_t launch_seq_lengths(const int32_t* sel, const int64_t* n_ptr, int64_t n_ub,
-                              const int64_t* offsets, int32_t max_len, int32_t n_prefix,
-                              int32_t* lens, int64_t* ctr, hipStream_t s) {
-  hipLaunchKernelGGL(k_seq_lengths, dim3(grid_for(n_ub, 256)), dim3(256), 0, s, sel, n_ptr, offsets,
-                     max_len, n_prefix, lens, ctr);
-  return hipGetLastError();
-}
-
-// ------------------------------------------------------------------ scan of lengths -> cu (int64)
-// Three phases over tiles of 4096 lengths: tile sums, one-workgroup scan of
-// the tile sums, then per-tile inclusive scan plus the tile offset.
-
-constexpr int SCAN_T = 1024;
-constexpr int SCAN_PER = 4;
-constexpr int SCAN_TILE = SCAN_T * SCAN_PER;
-
-__device__ __forceinline__ int64_t wg_exclusive_scan(int64_t v, int64_t* total) {
-  __shared__ int64_t wsum[SCAN_T / 64];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  int64_t x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int64_t y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
-  if (lane == 63) wsum[w] = x;
-  __syncthreads();
-  int64_t before = 0, all = 0;
-  for (int i = 0; i < SCAN_T / 64; ++i) {
-    const int64_t ws = wsum[i];
-    if (i < w) before += ws;
-    all += ws;
-  }
-  __syncthreads();
-  *total = all;
-  return before + x - v;
-}
-
-__global__ __launch_bounds__(SCAN_T) void k_scan_tile_sums(const int32_t* lens, const int64_t* n_ptr,
-                                                           int64_t* tile_sum) {
-  const int64_t n = *n_ptr;
-  const int64_t base = static_cast<int64_t>(blockIdx.x) * SCAN_TILE;
-  if (base >= n) return;
-  int64_t v = 0;
-  for (int j = 0; j < SCAN_PER; ++j) {
-    const int64_t i = base + threadIdx.x * SCAN_PER + j;
-    if (i < n) v += lens[i];
-  }
-  int64_t tot;
-  wg_exclusive_scan(v, &tot);
-  if (threadIdx.x == 0) tile_sum[blockIdx.x] = tot;
-}
-
-__global__ __launch_bounds__(SCAN_T) void k_scan_tile_offsets(int64_t* tile_sum, const int64_t* n_ptr,
-                                                              int64_t* total_out, int64_t* cu) {
-  const int64_t n = *n_ptr;
-  const int64_t nt = (n + SCAN_TILE - 1) / SCAN_TILE;
-  int64_t carry = 0;
-  for (int64_t t0 = 0; t0 < nt; t0 += SCAN_T) {
-    const int64_t t = t0 + threadIdx.x;
-    const int64_t v = t < nt ? tile_sum[t] : 0;
-    int64_t tot;
-    const int64_t ex = wg_exclusive_scan(v, &tot);
-    if (t < nt) tile_sum[t] = carry + ex;   // becomes the tile's exclusive offset
-    carry += tot;
-  }
-  if (threadIdx.x == 0) {
-    *total_out = carry;
-    cu[0] = 0;
-  }
-}
-
-__global__ __launch_bounds__(SCAN_T) void k_scan_tile_apply(const int32_t* lens, const int64_t* n_ptr,
-                                                            const int64_t* tile_off, int64_t* cu) {
-  const int64_t n = *n_ptr;
-  const int64_t base = static_cast<int64_t>(blockIdx.x) * SCAN_TILE;
-  if (base >= n) return;
-  int64_t v[SCAN_PER];
-  int64_t s = 0;
-  for (int j = 0; j < SCAN_PER; ++j) {
-    const int64_t i = base + threadIdx.x * SCAN_PER + j;
-    v[j] = i < n ? lens[i] : 0;
-    s += v[j];
-  }
-  int64_t tot;
-  int64_t run = tile_off[blockIdx.x] + wg_exclusive_scan(s, &tot);
-  for (int j = 0; j < SCAN_PER; ++j) {
-    const int64_t i = base + threadIdx.x * SCAN_PER + j;
-    run += v[j];
-    if (i < n) cu[i + 1] = run;
-  }
-}
-
-hipError_t launch_scan_lengths(const int32_t* lens, const int64_t* n_ptr, int64_t n_ub,
-                               int64_t* block_tmp, int64_t* cu, int64_t* total_out,
-                               hipStream_t s) {
-  const int64_t nt = (n_ub + SCAN_TILE - 1) / SCAN_TILE;
-  const unsigned g = static_cast<unsigned>(nt < 1 ? 1 : nt);
-  hipLaunchKernelGGL(k_scan_tile_sums, dim3(g), dim3(SCAN_T), 0, s, lens, n_ptr, block_tmp);
-  hipLaunchKernelGGL(k_scan_tile_offsets, dim3(1), dim3(SCAN_T), 0, s, block_tmp, n_ptr, total_out, cu);
-  hipLaunchKernelGGL(k_scan_tile_apply, dim3(g), dim3(SCAN_T), 0, s, lens, n_ptr, block_tmp, cu);
-  return hipGetLastError();
-}
 
 // ------------------------------------------------------------------ gather
 // One wave per sequence: the prompt prefix, then the row's tokens.  Token ids

@@ -154,8 +154,78 @@ __device__ __forceinline__ void finish_block_count(int count_wave, int32_t* blk_
   }
 }
 
-// Row r = base + j*256 + threadIdx.x for j in [0, 8): each (j, wave) pair
-// yields the ballot word index block*32 + j*4 + wave.
+// Predicate masks.  A block covers 8192 rows in two passes of 4096; in a pass
+// lane l of wave w owns the 16 consecutive rows starting at
+// base + pass*4096 + w*1024 + 16l, read with 16-byte loads (one for int8, two
+// for int16, four for int32 columns).  The predicates are evaluated column by
+// column into a 16-bit result per lane; four neighbouring lanes form one
+// 64-row mask word (bit b = row 64*word + b of the block, the natural order
+// the compaction reads).  Column data must be 16-byte aligned (the plan
+// checks this).
+
+template <typename T>
+__device__ __forceinline__ void load16(const T* col, int64_t r0, int64_t n_rows, int32_t (&v)[16]) {
+  if (r0 + 16 <= n_rows) {
+    constexpr int PER = 16 / sizeof(T);   // values per 16-byte load
+#pragma unroll
+    for (int q = 0; q < 16 / PER; ++q) {
+      const int4 raw = *reinterpret_cast<const int4*>(col + r0 + q * PER);
+      const T* e = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+      for (int k = 0; k < PER; ++k) v[q * PER + k] = static_cast<int32_t>(e[k]);
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) v[k] = r0 + k < n_rows ? static_cast<int32_t>(col[r0 + k]) : 0;
+  }
+}
+
+template <typename T, typename Cmp>
+__device__ __forceinline__ uint32_t atom16_op(const T* col, int64_t r0, int64_t n_rows, Cmp cmp) {
+  int32_t v[16];
+  load16<T>(col, r0, n_rows, v);
+  uint32_t bits = 0;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) bits |= static_cast<uint32_t>(cmp(v[k])) << k;
+  return bits;
+}
+
+// Column values are at most 32-bit; a constant outside the int32 range
+// decides every row alike, so the per-row compare runs in 32 bits.
+template <typename T>
+__device__ __forceinline__ uint32_t atom16(const DPred& P, int64_t r0, int64_t n_rows) {
+  const T* col = static_cast<const T*>(P.data);
+  const int64_t k = P.k;
+  const bool hi = k > INT32_MAX, lo = k < INT32_MIN;
+  const int32_t k32 = hi ? INT32_MAX : (lo ? INT32_MIN : static_cast<int32_t>(k));
+  switch (P.op) {
+    case AIQ_LT:
+      if (hi || lo) return hi ? 0xFFFFu : 0u;
+      return atom16_op(col, r0, n_rows, [=](int32_t x) { return x < k32; });
+    case AIQ_LE:
+      if (hi || lo) return hi ? 0xFFFFu : 0u;
+      return atom16_op(col, r0, n_rows, [=](int32_t x) { return x <= k32; });
+    case AIQ_GT:
+      if (hi || lo) return lo ? 0xFFFFu : 0u;
+      return atom16_op(col, r0, n_rows, [=](int32_t x) { return x > k32; });
+    case AIQ_GE:
+      if (hi || lo) return lo ? 0xFFFFu : 0u;
+      return atom16_op(col, r0, n_rows, [=](int32_t x) { return x >= k32; });
+    case AIQ_EQ:
+      if (hi || lo) return 0u;
+      return atom16_op(col, r0, n_rows, [=](int32_t x) { return x == k32; });
+    case AIQ_NE:
+      if (hi || lo) return 0xFFFFu;
+      return atom16_op(col, r0, n_rows, [=](int32_t x) { return x != k32; });
+    default:   // IN: set values outside the column's type never match (dropped at plan time)
+      return atom16_op(col, r0, n_rows, [&](int32_t x) {
+        bool m = false;
+        for (int i = 0; i < P.n_set; ++i) m |= (x == P.set[i]);
+        return m;
+      });
+  }
+}
+
 __global__ __launch_bounds__(REL_THREADS) void k_row_mask(DPredList preds, int64_t n_rows,
                                                           const void* probe_key, int32_t pk_dt,
                                                           HashArgs h, int join, uint64_t* mask,
@@ -164,14 +234,32 @@ __global__ __launch_bounds__(REL_THREADS) void k_row_mask(DPredList preds, int64
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   int cnt = 0;
 #pragma unroll
-  for (int j = 0; j < REL_ROWS_PER_THREAD; ++j) {
-    const int64_t r = base + j * REL_THREADS + threadIdx.x;
-    bool ok = r < n_rows && eval_all(preds, r);
-    if (ok && join) ok = hash_find(h, static_cast<int32_t>(load_int(probe_key, pk_dt, r))) >= 0;
-    const uint64_t word = __ballot(ok);
-    if (lane == 0) mask[blockIdx.x * REL_WORDS_PER_BLOCK + j * 4 + w] = word;
-    cnt += __popcll(word);
+  for (int pass = 0; pass < 2; ++pass) {
+    const int64_t r0 = base + pass * 4096 + w * 1024 + lane * 16;
+    uint32_t keep = 0;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) keep |= static_cast<uint32_t>(r0 + k < n_rows) << k;
+    for (int i = 0; i < preds.n; ++i) {   // uniform over the grid
+      const DPred& P = preds.p[i];
+      if (P.dtype == AIQ_I8) keep &= atom16<int8_t>(P, r0, n_rows);
+      else if (P.dtype == AIQ_I16) keep &= atom16<int16_t>(P, r0, n_rows);
+      else keep &= atom16<int32_t>(P, r0, n_rows);
+    }
+    if (join) {
+      for (int k = 0; k < 16; ++k)
+        if ((keep >> k) & 1u)
+          if (hash_find(h, static_cast<int32_t>(load_int(probe_key, pk_dt, r0 + k))) < 0) keep &= ~(1u << k);
+    }
+    const uint32_t k1 = __shfl_down(keep, 1), k2 = __shfl_down(keep, 2), k3 = __shfl_down(keep, 3);
+    if ((lane & 3) == 0) {
+      const uint64_t word = static_cast<uint64_t>(keep) | (static_cast<uint64_t>(k1) << 16) |
+                            (static_cast<uint64_t>(k2) << 32) | (static_cast<uint64_t>(k3) << 48);
+      mask[blockIdx.x * REL_WORDS_PER_BLOCK + pass * 64 + w * 16 + (lane >> 2)] = word;
+      cnt += __popcll(word);
+    }
   }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o);
   finish_block_count(cnt, blk_cnt);
 }
 
@@ -216,9 +304,11 @@ hipError_t launch_label_mask(const int32_t* label, const int64_t* n_ptr, int64_t
   return hipGetLastError();
 }
 
-// ------------------------------------------------------------------ scan of block counts
-// One workgroup of 1024 threads walks the block counts in tiles of 1024 with a
-// running carry.  blk_off[b] = sum of counts of blocks < b; blk_off[nb] = total.
+// ------------------------------------------------------------------ scan of per-block values
+// One workgroup of 1024 threads; each thread sums 32 consecutive block values,
+// the workgroup scans those sums, so one pass covers 32768 blocks (268M rows)
+// with a running carry across passes.  off[b] = sum of values of blocks < b,
+// off[nb] = total.
 
 __device__ __forceinline__ int64_t block_exclusive_scan_1024(int64_t v, int64_t* total) {
   __shared__ int64_t wsum[16];
@@ -242,89 +332,276 @@ __device__ __forceinline__ int64_t block_exclusive_scan_1024(int64_t v, int64_t*
   return before + x - v;
 }
 
-__global__ __launch_bounds__(1024) void k_scan_blocks(const int32_t* blk_cnt, const int64_t* n_ptr,
-                                                      int64_t n_ub, int64_t* blk_off,
-                                                      int64_t* total_out) {
+template <typename T>
+__global__ __launch_bounds__(1024) void k_scan_blocks(const T* val, const int64_t* n_ptr, int64_t n_ub,
+                                                      int64_t* off, int64_t* total_out) {
+  constexpr int PER = 32;
   const int64_t n = n_ptr ? *n_ptr : n_ub;
   const int64_t nb = (n + REL_ROWS_PER_BLOCK - 1) / REL_ROWS_PER_BLOCK;
   int64_t carry = 0;
-  for (int64_t b0 = 0; b0 < nb; b0 += 1024) {
-    const int64_t b = b0 + threadIdx.x;
-    const int64_t v = b < nb ? blk_cnt[b] : 0;
+  for (int64_t b0 = 0; b0 < nb; b0 += 1024 * PER) {
+    const int64_t first = b0 + static_cast<int64_t>(threadIdx.x) * PER;
+    int64_t v[PER];
+    int64_t sum = 0;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      v[k] = first + k < nb ? static_cast<int64_t>(val[first + k]) : 0;
+      sum += v[k];
+    }
     int64_t tot;
-    const int64_t ex = block_exclusive_scan_1024(v, &tot);
-    if (b < nb) blk_off[b] = carry + ex;
+    int64_t run = carry + block_exclusive_scan_1024(sum, &tot);
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      if (first + k < nb) off[first + k] = run;
+      run += v[k];
+    }
     carry += tot;
   }
   if (threadIdx.x == 0) {
-    blk_off[nb] = carry;
+    off[nb] = carry;
     *total_out = carry;
   }
 }
 
 hipError_t launch_scan_blocks(const int32_t* blk_cnt, const int64_t* n_ptr, int64_t n_ub,
                               int64_t* blk_off, int64_t* total_out, hipStream_t s) {
-  hipLaunchKernelGGL(k_scan_blocks, dim3(1), dim3(1024), 0, s, blk_cnt, n_ptr, n_ub, blk_off, total_out);
+  hipLaunchKernelGGL(k_scan_blocks<int32_t>, dim3(1), dim3(1024), 0, s, blk_cnt, n_ptr, n_ub, blk_off, total_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_scan_blocks64(const int64_t* blk_val, const int64_t* n_ptr, int64_t n_ub,
+                                int64_t* blk_off, int64_t* total_out, hipStream_t s) {
+  hipLaunchKernelGGL(k_scan_blocks<int64_t>, dim3(1), dim3(1024), 0, s, blk_val, n_ptr, n_ub, blk_off, total_out);
   return hipGetLastError();
 }
 
 // ------------------------------------------------------------------ scatter
 // out_ids[pos] = src_ids ? src_ids[r] : r for every set bit r, in row order.
-// With a join the build payload of the row's match is written alongside.
+// With a join the build payload of the row's match is written alongside;
+// with lengths each row's token count too, and the block's token sum.
+//
+// Two levels: each thread drops the row numbers of its set bits into the
+// block's dense list in LDS (slot = popcount prefix of the block's mask),
+// then the whole block walks that list with consecutive threads on
+// consecutive entries, so every read of ids / offsets and every write of
+// ids / lengths is coalesced, and a block with few survivors costs one
+// round trip.
 
 __global__ __launch_bounds__(REL_THREADS) void k_scatter_rows(
     const uint64_t* mask, const int64_t* blk_off, const int64_t* n_ptr, int64_t n_ub,
-    const int32_t* src_ids, int32_t* out_ids, int64_t out_cap, const void* probe_key, int32_t pk_dt,
-    HashArgs h, int join, int32_t* out_payload, int64_t* ctr) {
+    const int32_t* src_ids, int32_t* out_ids, int64_t out_cap, int32_t* out_ids2, int64_t out_cap2,
+    const void* probe_key, int32_t pk_dt, HashArgs h, int join, int32_t* out_payload, ScatterLens ln,
+    int64_t* ctr) {
   const int64_t n = n_ptr ? *n_ptr : n_ub;
   const int64_t base = static_cast<int64_t>(blockIdx.x) * REL_ROWS_PER_BLOCK;
-  if (base >= n) return;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (base >= n) {
+    if (ln.off && threadIdx.x == 0) ln.blk_tok[blockIdx.x] = 0;
+    return;
+  }
   __shared__ uint64_t words[REL_WORDS_PER_BLOCK];
-  __shared__ int32_t wpre[REL_WORDS_PER_BLOCK];
-  if (threadIdx.x < REL_WORDS_PER_BLOCK) words[threadIdx.x] = mask[blockIdx.x * REL_WORDS_PER_BLOCK + threadIdx.x];
+  __shared__ int32_t wpre[REL_WORDS_PER_BLOCK + 1];
+  __shared__ int32_t wtot;
+  __shared__ uint16_t rows[REL_ROWS_PER_BLOCK];   // block-relative row of each survivor, in order
+  __shared__ int64_t tsum[REL_THREADS / 64];
+  const int64_t boff = blk_off[blockIdx.x];   // issued together with the mask load
+  // the block's 128 words and their exclusive popcount prefix (two waves)
+  int32_t pc = 0;
+  if (threadIdx.x < REL_WORDS_PER_BLOCK) {
+    const uint64_t wd = mask[blockIdx.x * REL_WORDS_PER_BLOCK + threadIdx.x];
+    words[threadIdx.x] = wd;
+    pc = __popcll(wd);
+  }
+  int32_t x = pc;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int32_t y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (threadIdx.x == 63) wtot = x;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    int32_t acc = 0;
-    for (int i = 0; i < REL_WORDS_PER_BLOCK; ++i) {
-      wpre[i] = acc;
-      acc += __popcll(words[i]);
-    }
+  if (threadIdx.x < REL_WORDS_PER_BLOCK) {
+    const int32_t incl = x + (threadIdx.x >= 64 ? wtot : 0);
+    wpre[threadIdx.x] = incl - pc;
+    if (threadIdx.x == REL_WORDS_PER_BLOCK - 1) wpre[REL_WORDS_PER_BLOCK] = incl;
   }
   __syncthreads();
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int64_t boff = blk_off[blockIdx.x];
   const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  bool overflow = false;
 #pragma unroll
   for (int j = 0; j < REL_ROWS_PER_THREAD; ++j) {
     const int wi = j * 4 + w;
     const uint64_t word = words[wi];
-    if (!((word >> lane) & 1ull)) continue;
-    const int64_t r = base + j * REL_THREADS + threadIdx.x;
-    const int64_t pos = boff + wpre[wi] + __popcll(word & below);
-    if (pos >= out_cap) {
-      overflow = true;
-      continue;
+    if ((word >> lane) & 1ull)
+      rows[wpre[wi] + __popcll(word & below)] = static_cast<uint16_t>(j * REL_THREADS + threadIdx.x);
+  }
+  __syncthreads();
+  const int32_t cnt = wpre[REL_WORDS_PER_BLOCK];
+  bool overflow = false, bad_len = false;
+  int64_t tok = 0;
+  constexpr int U = 8;   // entries per thread and round, their loads issued together
+  for (int i0 = 0; i0 < cnt; i0 += REL_THREADS * U) {
+    int32_t id[U];
+    uint32_t lo0[U], lo1[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = i0 + u * REL_THREADS + threadIdx.x;
+      id[u] = 0;
+      lo0[u] = lo1[u] = 0;
+      if (i < cnt) {
+        const int64_t r = base + rows[i];
+        id[u] = src_ids ? src_ids[r] : static_cast<int32_t>(r);
+        if (ln.off) {
+          // list length from the low 32 bits of both offsets (exact below 2^31)
+          const uint32_t* off32 = reinterpret_cast<const uint32_t*>(ln.off);
+          lo0[u] = off32[2 * r];
+          lo1[u] = off32[2 * r + 2];
+        }
+      }
     }
-    out_ids[pos] = src_ids ? src_ids[r] : static_cast<int32_t>(r);
-    if (join && out_payload) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = i0 + u * REL_THREADS + threadIdx.x;
+      if (i >= cnt) continue;
+      const int64_t pos = boff + i;
+      if (pos < out_cap) out_ids[pos] = id[u];
+      else overflow = true;
+      if (out_ids2) {
+        if (pos < out_cap2) out_ids2[pos] = id[u];
+        else overflow = true;
+      }
+      if (ln.off) {
+        int32_t len = static_cast<int32_t>(lo1[u] - lo0[u]);
+        if (len < 0 || len > ln.max_len) {
+          bad_len = true;
+          len = len < 0 ? 0 : ln.max_len;
+        }
+        const int32_t l = len + ln.n_prefix;
+        ln.lens[pos] = l;
+        tok += l;
+      }
+    }
+  }
+  if (join && out_payload) {   // the build payload of each survivor's match
+    for (int i = threadIdx.x; i < cnt; i += REL_THREADS) {
+      const int64_t r = base + rows[i];
       const int32_t slot = hash_find(h, static_cast<int32_t>(load_int(probe_key, pk_dt, r)));
-      out_payload[pos] = slot >= 0 ? h.vals[slot] : 0;
+      out_payload[boff + i] = slot >= 0 ? h.vals[slot] : 0;
     }
   }
   if (overflow) set_status(ctr, AIQ_DEV_IDS_CAP);
+  if (ln.off) {
+    if (bad_len) set_status(ctr, AIQ_DEV_LIST_LEN);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) tok += __shfl_xor(tok, o);
+    if (lane == 0) tsum[w] = tok;
+    __syncthreads();
+    if (threadIdx.x == 0) ln.blk_tok[blockIdx.x] = (tsum[0] + tsum[1]) + (tsum[2] + tsum[3]);
+  }
 }
 
 hipError_t launch_scatter_rows(const uint64_t* mask, const int64_t* blk_off, const int64_t* n_ptr,
                                int64_t n_ub, const int32_t* src_ids, int32_t* out_ids,
                                int64_t out_cap, const void* probe_key, int32_t probe_key_dtype,
                                HashArgs h, int join, int32_t* out_payload, int64_t* ctr,
-                               hipStream_t s) {
+                               hipStream_t s, int32_t* out_ids2, int64_t out_cap2, ScatterLens lens) {
   const int64_t nb = (n_ub + REL_ROWS_PER_BLOCK - 1) / REL_ROWS_PER_BLOCK;
   if (nb == 0) return hipSuccess;
   hipLaunchKernelGGL(k_scatter_rows, dim3(static_cast<unsigned>(nb)), dim3(REL_THREADS), 0, s, mask,
-                     blk_off, n_ptr, n_ub, src_ids, out_ids, out_cap, probe_key, probe_key_dtype, h,
-                     join, out_payload, ctr);
+                     blk_off, n_ptr, n_ub, src_ids, out_ids, out_cap, out_ids2, out_cap2, probe_key,
+                     probe_key_dtype, h, join, out_payload, lens, ctr);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ cu_seqlens
+// Block b of the compaction owns output positions [blk_off[b], blk_off[b+1]);
+// its tokens start at tok_off[b].  Each workgroup writes the exclusive prefix
+// cu[i] for its positions, scanning in steps of 4096 (16 per thread, read as
+// four 16-byte vectors from an 8-aligned start, written as eight 16-byte
+// vectors) with a running carry; the last block also writes cu[n] = total.
+// `lens` must be readable up to 23 entries past the last position.
+__global__ __launch_bounds__(256) void k_cu_from_blocks(const int32_t* lens, const int64_t* blk_off,
+                                                        const int64_t* tok_off, int64_t* cu) {
+  constexpr int E = 16;   // entries per thread and step
+  __shared__ int64_t wsum[4];
+  const int64_t o0 = blk_off[blockIdx.x], o1 = blk_off[blockIdx.x + 1];
+  if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) cu[o1] = tok_off[gridDim.x];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int64_t carry = tok_off[blockIdx.x];
+  for (int64_t c0 = o0 & ~int64_t(7); c0 < o1; c0 += 256 * E) {
+    const int64_t i0 = c0 + static_cast<int64_t>(threadIdx.x) * E;
+    int32_t v[E];
+    int64_t sum = 0;
+    if (i0 < o1) {
+#pragma unroll
+      for (int q = 0; q < E / 4; ++q) {
+        const int4 a = *reinterpret_cast<const int4*>(lens + i0 + 4 * q);
+        v[4 * q] = a.x;
+        v[4 * q + 1] = a.y;
+        v[4 * q + 2] = a.z;
+        v[4 * q + 3] = a.w;
+      }
+#pragma unroll
+      for (int k = 0; k < E; ++k) {
+        if (!(i0 + k >= o0 && i0 + k < o1)) v[k] = 0;
+        sum += v[k];
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < E; ++k) v[k] = 0;
+    }
+    int64_t x = sum;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int64_t y = __shfl_up(x, o);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) wsum[w] = x;
+    __syncthreads();
+    int64_t before = 0, all = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (i < w) before += wsum[i];
+      all += wsum[i];
+    }
+    __syncthreads();
+    int64_t run = carry + before + x - sum;
+    if (i0 >= o0 && i0 + E <= o1) {
+#pragma unroll
+      for (int k = 0; k < E; k += 2) {
+        const int64_t a = run;
+        run += v[k];
+        const int64_t b = run;
+        run += v[k + 1];
+        *reinterpret_cast<longlong2*>(cu + i0 + k) = make_longlong2(a, b);
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < E; ++k) {
+        if (i0 + k >= o0 && i0 + k < o1) cu[i0 + k] = run;
+        run += v[k];
+      }
+    }
+    carry += all;
+  }
+}
+
+hipError_t launch_cu_from_blocks(const int32_t* lens, const int64_t* blk_off, const int64_t* tok_off,
+                                 int64_t n_ub, int64_t* cu, hipStream_t s) {
+  const int64_t nb = (n_ub + REL_ROWS_PER_BLOCK - 1) / REL_ROWS_PER_BLOCK;
+  if (nb == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_cu_from_blocks, dim3(static_cast<unsigned>(nb)), dim3(256), 0, s, lens, blk_off, tok_off,
+                     cu);
+  return hipGetLastError();
+}
+
+__global__ void k_keep_selected(int64_t* ctr, int64_t cap) {
+  const int64_t n = ctr[C_SEL];
+  ctr[C_KEPT] = n;
+  if (n > cap) set_status(ctr, AIQ_DEV_IDS_CAP);
+}
+
+hipError_t launch_keep_selected(int64_t* ctr, int64_t cap, hipStream_t s) {
+  hipLaunchKernelGGL(k_keep_selected, dim3(1), dim3(1), 0, s, ctr, cap);
   return hipGetLastError();
 }
 

@@ -110,9 +110,11 @@ class DeviceTable:
         if with_list:
             off = np.asarray(cols["offsets"], dtype=np.int64)
             self.offsets = _dev(off, device)
-            tok = np.asarray(cols["tokens"], dtype=np.int32)
-            self.tokens = _dev(tok if len(tok) else np.zeros(1, np.int32), device)
-            t.list_offsets, t.list_tokens = _ptr(self.offsets), _ptr(self.tokens)
+            t.list_offsets = _ptr(self.offsets)
+            if "tokens" in cols:   # absent: offsets only (relational-only plans)
+                tok = np.asarray(cols["tokens"], dtype=np.int32)
+                self.tokens = _dev(tok if len(tok) else np.zeros(1, np.int32), device)
+                t.list_tokens = _ptr(self.tokens)
             t.n_list_tokens = int(off[-1] - off[0])
             lens = np.diff(off)
             t.max_list_len = int(max_list_len if max_list_len is not None else max(1, lens.max(initial=1)))
@@ -165,7 +167,8 @@ class DeviceQuery:
     """A planned query over device-resident tables and weights."""
 
     def __init__(self, tables: dict, model, query, device="cuda", chunk_tokens: int = 0,
-                 n_layers: int | None = None, dmodel: DeviceModel | None = None):
+                 n_layers: int | None = None, dmodel: DeviceModel | None = None, relational_only: bool = False,
+                 want_sel: bool = True):
         self.device = torch.device(device)
         self.query = query
         self.dm = dmodel if dmodel is not None else DeviceModel(model, device)
@@ -175,6 +178,7 @@ class DeviceQuery:
         opts = B.aiq_plan_opts()
         opts.chunk_tokens = int(chunk_tokens)
         opts.n_layers_override = _layers_opt(n_layers)
+        opts.flags = B.AIQ_PLAN_RELATIONAL_ONLY if relational_only else 0
         self.plan = B.aiq_plan_create(self.dm.struct, self.probe.struct,
                                       self.build.struct if self.build else None, self.q, opts)
         self.ws_bytes = B.aiq_workspace_size(self.plan)
@@ -197,7 +201,7 @@ class DeviceQuery:
         o = B.aiq_out()
         o.scalars, o.ids, o.ids_cap = _ptr(self.scalars), _ptr(self.ids), n
         o.sel_ids, o.sel_labels, o.sel_logits, o.sel_cap = (_ptr(self.sel_ids), _ptr(self.sel_labels),
-                                                            _ptr(self.sel_logits), n)
+                                                            _ptr(self.sel_logits), n if want_sel else 0)
         o.grp_key, o.grp_count, o.grp_sum, o.grp_avg = (_ptr(self.grp_key), _ptr(self.grp_count),
                                                         _ptr(self.grp_sum), _ptr(self.grp_avg))
         o.grp_cap = G

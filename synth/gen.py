@@ -97,13 +97,16 @@ def _tokens(spec: TableSpec, nnz: int) -> np.ndarray:
     return out
 
 
-def make_probe(spec: TableSpec, movie_ids: np.ndarray | None = None) -> dict:
+def make_probe(spec: TableSpec, movie_ids: np.ndarray | None = None, with_tokens: bool = True) -> dict:
+    """Probe-table columns; with_tokens=False leaves out the token list (its
+    offsets and lengths are still drawn, from the same streams)."""
     n = spec.n_rows
     lens = _lengths(spec)
     offsets = np.zeros(n + 1, dtype=np.int64)
     np.cumsum(lens, out=offsets[1:])
     t = {"id": np.arange(n, dtype=np.int32), "len": lens, "offsets": offsets}
-    t["tokens"] = _tokens(spec, int(offsets[-1]))
+    if with_tokens:
+        t["tokens"] = _tokens(spec, int(offsets[-1]))
     if spec.rating is not None:
         rng = _rng(spec.seed, S_RATING)
         if spec.rating[0] == "uniform":

@@ -113,12 +113,47 @@ def test_null_model_and_bad_query():
 
 
 def test_table_validation():
+    t = table(); t.cols[1].data = FAKE + 4   # columns must be 16-byte aligned
+    assert B.aiq_plan_create_status(model(), t, None, query()) == B.AIQ_EINVAL
     t = table(); t.list_offsets = 0
     assert B.aiq_plan_create_status(model(), t, None, query()) == B.AIQ_EINVAL
     t = table(); t.max_list_len = 0
     assert B.aiq_plan_create_status(model(), t, None, query()) == B.AIQ_EINVAL
     t = table(); t.n_rows = -1
     assert B.aiq_plan_create_status(model(), t, None, query()) == B.AIQ_EINVAL
+
+
+def _opts(flags):
+    o = B.aiq_plan_opts()
+    o.flags = flags
+    return o
+
+
+def test_relational_only_plan_validation():
+    # the token column is optional only when the plan stops after the relational part
+    t = table(); t.list_tokens = 0
+    assert B.aiq_plan_create_status(model(), t, None, query()) == B.AIQ_EINVAL
+    assert B.aiq_plan_create_status(model(), t, None, query(), _opts(B.AIQ_PLAN_RELATIONAL_ONLY)) == B.AIQ_OK
+    # offsets stay required (token counts come from them)
+    t = table(); t.list_offsets = 0
+    assert B.aiq_plan_create_status(model(), t, None, query(), _opts(B.AIQ_PLAN_RELATIONAL_ONLY)) == B.AIQ_EINVAL
+    # only COUNT: there are no labels to aggregate
+    q = query(agg=B.AIQ_AGG_AVG_LABEL_COUNT_BY, group_col=1, n_group_keys=4)
+    assert B.aiq_plan_create_status(model(), table(), None, q) == B.AIQ_OK
+    assert B.aiq_plan_create_status(model(), table(), None, q, _opts(B.AIQ_PLAN_RELATIONAL_ONLY)) == B.AIQ_EINVAL
+    # unknown flag bits
+    assert B.aiq_plan_create_status(model(), table(), None, query(), _opts(2)) == B.AIQ_EINVAL
+
+
+def test_relational_only_workspace_holds_no_model_activations():
+    full = B.aiq_plan_create(model(), table(), None, query())
+    rel = B.aiq_plan_create(model(), table(), None, query(), _opts(B.AIQ_PLAN_RELATIONAL_ONLY))
+    try:
+        # 1000 rows x 100 tokens: the full plan carries the packed batch and the activations
+        assert B.aiq_workspace_size(rel) < B.aiq_workspace_size(full) // 10
+    finally:
+        B.aiq_plan_destroy(full)
+        B.aiq_plan_destroy(rel)
 
 
 def test_run_rejects_before_enqueue():

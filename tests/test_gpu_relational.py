@@ -147,3 +147,54 @@ def test_status_token_range_and_ids_cap(rel_model):
     r = run(t, m, dm, q, tweak=small_cap)
     assert r["status"] & B.AIQ_DEV_TOKEN_RANGE
     assert r["status"] & B.AIQ_DEV_IDS_CAP
+
+
+def run_relational_only(tables, model, dm, q):
+    dq = DeviceQuery(tables, model, q, dmodel=dm, relational_only=True)
+    dq.run()
+    torch.cuda.synchronize()
+    r = dq.results()
+    dq.close()
+    return r
+
+
+def check_relational_only(r, tables, q):
+    rows, _ = relational(tables, q)
+    assert r["status"] == 0
+    assert r["n_selected"] == r["count"] == len(rows)
+    np.testing.assert_array_equal(r["kept_ids"], rows)
+    np.testing.assert_array_equal(r["sel_ids"], rows)
+    lens = np.diff(tables["probe"]["offsets"])
+    assert r["n_tokens"] == int(lens[rows].sum()) + q.n_prefix * len(rows)
+
+
+@pytest.mark.parametrize("n", [1, 64, 2049, 70000])
+def test_relational_only_mode(rel_model, n):
+    """The plan flag that stops after the relational part: every selected id
+    kept, counts and token totals exact; the token column is never read."""
+    say(f"case: relational-only n={n}")
+    m, dm = rel_model
+    probe = table(n, 100 + n)
+    q = Query(preds=(Pred("c", "lt", 400), Pred("a", "ne", 5)), labels=(1, 2), decision="binary_gt", agg="count")
+    t = {"probe": probe, "build": None, "prefix": np.zeros(0, np.int32)}
+    check_relational_only(run_relational_only(t, m, dm, q), t, q)
+    # without a token column at all
+    t2 = {"probe": {k: v for k, v in probe.items() if k != "tokens"}, "build": None,
+          "prefix": np.zeros(0, np.int32)}
+    check_relational_only(run_relational_only(t2, m, dm, q), t2, q)
+
+
+def test_relational_only_join_with_prefix(rel_model):
+    say("case: relational-only join")
+    m, dm = rel_model
+    r = np.random.default_rng(11)
+    nb = 300
+    build = {"key": r.choice(1 << 30, nb, replace=False).astype(np.int32),
+             "genre": r.integers(0, 7, nb).astype(np.int8), "year": r.integers(1950, 2020, nb).astype(np.int16)}
+    probe = table(4000, 12)
+    probe["fk"] = build["key"][r.integers(0, nb, 4000)]
+    t = {"probe": probe, "build": build, "prefix": np.arange(3, 8, dtype=np.int32)}
+    q = Query(preds=(Pred("a", "gt", -100),), labels=(1, 2), decision="binary_gt", agg="count",
+              join=Join(probe_key="fk", build_key="key", payload="genre",
+                        build_preds=(Pred("year", "gt", 1990),)), n_prefix=5)
+    check_relational_only(run_relational_only(t, m, dm, q), t, q)
