@@ -3,7 +3,8 @@
 //
 // Work items are (sequence, query head) pairs walked by a persistent grid;
 // each item loops over 64-query blocks of its own sequence and, inside, over
-// 64-key blocks from the sequence start up to the diagonal.  Key blocks are
+// 64-key blocks from the sequence start up to the diagonal, the next key
+// block's global reads in flight while the current one is consumed.  Key blocks are
 // aligned to the sequence start, so a row's result does not depend on the
 // other rows packed next to it.  Softmax is the usual online form in fp32
 // (running max and sum, rescaled output accumulator).
@@ -71,19 +72,32 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
       for (int db = 0; db < HD / 16; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
       float m_run = -INFINITY, l_run = 0.f;
 
-      for (int kb = 0; kb <= qb; ++kb) {
-        __syncthreads();   // previous key block fully consumed
-        for (int id = t; id < KB * CH; id += 256) {
-          const int r = id / CH, ch = id % CH;
+      // this thread's K and V chunks of a key block (zeros past L); the next
+      // block's are read into registers while the current block is consumed
+      constexpr int PER = KB * CH / 256;
+      uint4 kr[PER], vr[PER];
+      auto fetch = [&](int kb) {
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+          const int id = t + u * 256, r = id / CH, ch = id % CH;
           const int kk = kb * KB + r;
-          uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+          kr[u] = make_uint4(0, 0, 0, 0);
+          vr[u] = make_uint4(0, 0, 0, 0);
           if (kk < L) {
             const uint16_t* row = qkv + (s0 + kk) * a.ld;
-            kv = *reinterpret_cast<const uint4*>(row + kcol + ch * 8);
-            vv = *reinterpret_cast<const uint4*>(row + vcol + ch * 8);
+            kr[u] = *reinterpret_cast<const uint4*>(row + kcol + ch * 8);
+            vr[u] = *reinterpret_cast<const uint4*>(row + vcol + ch * 8);
           }
-          *reinterpret_cast<uint4*>(Ks + r * HD + ((ch ^ (r & 7)) << 3)) = kv;
-          const uint32_t vw[4] = {vv.x, vv.y, vv.z, vv.w};
+        }
+      };
+      fetch(0);
+      for (int kb = 0; kb <= qb; ++kb) {
+        __syncthreads();   // previous key block fully consumed
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+          const int id = t + u * 256, r = id / CH, ch = id % CH;
+          *reinterpret_cast<uint4*>(Ks + r * HD + ((ch ^ (r & 7)) << 3)) = kr[u];
+          const uint32_t vw[4] = {vr[u].x, vr[u].y, vr[u].z, vr[u].w};
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
             const int dim = ch * 8 + j;
@@ -92,6 +106,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
           }
         }
         __syncthreads();
+        if (kb < qb) fetch(kb + 1);
 
         // S^T block j: keys 16j.., lane holds keys 16j + 4g + e for query c16
         f32x4 sacc[4];
