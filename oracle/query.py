@@ -8,7 +8,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from .relational import select, hash_join, sequences, group_avg_count, count_by
+from .relational import select, hash_join, sequences, group_avg_count, count_by, sum_f32
 from .transformer import label_logits
 
 
@@ -61,6 +61,8 @@ def aggregate(tables: dict, rows: np.ndarray, payload, labels: np.ndarray, query
     elif query.agg == "count_by_payload":
         k, c = count_by(np.asarray(payload, dtype=np.int64)[keep])
         out["groups"] = (k, c, np.zeros_like(c), np.zeros(len(c)))
+    elif query.agg == "sum_f32":
+        out["sum"] = sum_f32(probe[query.group_col][kept])
     return out
 
 

@@ -3,8 +3,9 @@ aggregates.  Test infrastructure only (see the package docstring).
 
 Semantics follow Table 1 of the paper (Section 3.1): a WHERE clause becomes an
 element-wise boolean mask over the column arrays; an aggregate is a reduction
-over the rows the final mask keeps.  Comparisons are exact integer comparisons
-in the column's own type (widened to int64, which is exact).
+over the rows the final mask keeps.  Comparisons are exact: integer columns
+widened to int64, fp32 columns widened to fp64 and compared with the fp64
+constant (IEEE semantics: NaN fails every ordered comparison and EQ, passes NE).
 """
 from __future__ import annotations
 
@@ -18,7 +19,12 @@ _CMP = {
 
 def eval_pred(cols: dict, pred) -> np.ndarray:
     """Boolean mask of one atom ``col op k`` or ``col IN (values)`` (Table 1, WHERE row)."""
-    v = np.asarray(cols[pred.col]).astype(np.int64)
+    col = np.asarray(cols[pred.col])
+    if col.dtype.kind == "f":
+        if pred.op == "in":
+            raise ValueError("IN is defined for integer columns only")
+        return _CMP[pred.op](col.astype(np.float64), np.float64(pred.k))
+    v = col.astype(np.int64)
     if pred.op == "in":
         m = np.zeros(v.shape, dtype=bool)
         for x in pred.values:
@@ -106,3 +112,12 @@ def count_by(keys: np.ndarray):
     """GROUP BY key COUNT(*), ascending key order, present keys only."""
     k, c, _, _ = group_avg_count(keys, np.zeros(len(keys), dtype=np.int64))
     return k, c
+
+
+def sum_f32(values: np.ndarray) -> float:
+    """SUM of an fp32 column over the kept rows (the float aggregate of the
+    paper's running query, Table 1 SUM row and Figure 2): the exact sum of the
+    values, rounded once to fp64 (math.fsum)."""
+    import math
+    return math.fsum(float(x) for x in np.asarray(values, dtype=np.float32))
+

@@ -79,7 +79,8 @@ class TableSpec:
     length: ("uniform", lo, hi) inclusive, or ("lognormal", median, sigma, lo, hi)
     tokens: ("uniform", vocab) or ("zipf", s, vocab)
     rating: None, ("uniform", 1, 5) or ("probs", (p1..p5))
-    extra columns: movie_id ("zipf", s, n_keys) as a key rank, c uniform int range.
+    extra columns: movie_id ("zipf", s, n_keys) as a key rank, c uniform int range,
+    values_a uniform in [lo, hi] rounded to fp32 (the float column the paper's SUM queries add up).
     """
     n_rows: int
     seed: int
@@ -88,6 +89,7 @@ class TableSpec:
     rating: Optional[tuple] = None
     movie_id: Optional[tuple] = None      # ("zipf", s, n_ids)
     c_range: Optional[Tuple[int, int]] = None   # uniform int32 in [lo, hi]
+    values_a: Optional[Tuple[float, float]] = None   # uniform in [lo, hi], rounded to fp32
 
 
 @dataclass(frozen=True)
@@ -110,7 +112,7 @@ OPS = ("lt", "le", "gt", "ge", "eq", "ne", "in")
 class Pred:
     col: str
     op: str
-    k: int = 0
+    k: float = 0   # int for integer columns; a float constant for fp32 columns
     values: Tuple[int, ...] = ()
 
 
@@ -151,21 +153,41 @@ _LOGN_120 = ("lognormal", 120.0, 0.6, 16, 512)
 _ZIPF_TOK = ("zipf", 1.1, 32000)
 _RATING_P = ("probs", (0.1, 0.1, 0.2, 0.3, 0.3))
 
+_TINY_TABLE = TableSpec(n_rows=256, seed=0, length=("uniform", 8, 64), tokens=("uniform", 1024),
+                        rating=("uniform", 1, 5), values_a=(0.0, 100.0))
+_REVIEWS_TABLE = TableSpec(n_rows=16384, seed=1, length=_LOGN_120, tokens=_ZIPF_TOK, rating=_RATING_P,
+                           values_a=(0.0, 100.0))
+
 WORKLOADS = {
     "tiny": Workload(
         name="tiny", description="tiny select + semantic filter, 256 rows, 2-layer fp32 decoder",
-        table=TableSpec(n_rows=256, seed=0, length=("uniform", 8, 64), tokens=("uniform", 1024),
-                        rating=("uniform", 1, 5)),
+        table=_TINY_TABLE,
         model=TINY,
         queries=(Query(preds=(Pred("rating", "ge", 3),), labels=_BINARY, decision="binary_gt",
                        agg="count"),),
     ),
     "reviews": Workload(
         name="reviews", description="reviews-shaped binary filter, 16,384 rows, 4-layer d512 bf16 decoder",
-        table=TableSpec(n_rows=16384, seed=1, length=_LOGN_120, tokens=_ZIPF_TOK, rating=_RATING_P),
+        table=_REVIEWS_TABLE,
         model=SMALL,
         queries=(Query(preds=(Pred("rating", "le", 2), Pred("len", "gt", 32)), labels=_BINARY,
                        decision="binary_gt", agg="count"),),
+    ),
+    # the paper's running query shape: SUM(values_a) WHERE values_a > 70 AND AI_IF(...)
+    "reviews_sum": Workload(
+        name="reviews_sum", description="SUM of a float column over rows passing a float filter and the "
+                                        "semantic filter, 16,384 rows, 4-layer d512 bf16 decoder",
+        table=_REVIEWS_TABLE,
+        model=SMALL,
+        queries=(Query(preds=(Pred("values_a", "gt", 70.0),), labels=_BINARY, decision="binary_gt",
+                       agg="sum_f32", group_col="values_a"),),
+    ),
+    "tiny_sum": Workload(
+        name="tiny_sum", description="tiny SUM of a float column under float and semantic filters, 256 rows",
+        table=_TINY_TABLE,
+        model=TINY,
+        queries=(Query(preds=(Pred("values_a", "ge", 30.0), Pred("rating", "ne", 4)), labels=_BINARY,
+                       decision="binary_gt", agg="sum_f32", group_col="values_a"),),
     ),
     "groupby1b": Workload(
         name="groupby1b", description="1B-class 5-way classify + GROUP BY movie_id, 131,072 rows",

@@ -27,7 +27,7 @@ from .configs import WORKLOADS, ModelSpec, MoviesSpec, TableSpec, Workload
 CHUNK = 1 << 22
 
 # column stream ids
-S_LEN, S_TOK, S_RATING, S_MOVIE, S_C = 1, 2, 3, 4, 5
+S_LEN, S_TOK, S_RATING, S_MOVIE, S_C, S_VALUES = 1, 2, 3, 4, 5, 6
 S_MOVIES_ID, S_GENRE, S_YEAR = 10, 11, 12
 S_PREFIX = 99
 S_WEIGHT_BASE = 1000
@@ -121,6 +121,10 @@ def make_probe(spec: TableSpec, movie_ids: np.ndarray | None = None, with_tokens
     if spec.c_range is not None:
         lo, hi = spec.c_range
         t["c"] = _rng(spec.seed, S_C).integers(lo, hi + 1, size=n).astype(np.int32)
+    if spec.values_a is not None:
+        lo, hi = spec.values_a
+        u = _rng(spec.seed, S_VALUES).random(n)
+        t["values_a"] = np.minimum((lo + (hi - lo) * u).astype(np.float32), np.float32(hi))
     return t
 
 

@@ -5,6 +5,7 @@ import pytest
 
 import oracle
 from oracle.query import aggregate, decide, margin, relational
+from oracle.relational import eval_pred, sum_f32
 from synth.configs import Join, Pred, Query
 
 OPS = {"lt": lambda a, b: a < b, "le": lambda a, b: a <= b, "gt": lambda a, b: a > b,
@@ -178,3 +179,57 @@ def test_relational_with_join_end_to_end():
            if any(movies["movie_id"][m] == reviews["movie_id"][r] and movies["year"][m] > 1990
                   for m in range(40))]
     assert rows.tolist() == exp
+
+
+# ---------------------------------------------------------------- float columns and SUM
+
+def test_float_predicate_matches_python_comparisons():
+    """fp32 columns compare exactly against the fp64 constant, IEEE semantics:
+    values at, just below and just above the threshold, signed zeros, NaN."""
+    k = 70.0
+    up = float(np.nextafter(np.float32(k), np.float32(np.inf)))
+    dn = float(np.nextafter(np.float32(k), np.float32(-np.inf)))
+    vals = np.array([k, up, dn, 0.0, -0.0, np.nan, np.inf, -np.inf, 69.99999, 70.00001, 1e30, -1e-30],
+                    dtype=np.float32)
+    cols = {"v": vals}
+    import operator
+    ops = {"lt": operator.lt, "le": operator.le, "gt": operator.gt, "ge": operator.ge,
+           "eq": operator.eq, "ne": operator.ne}
+    for name, f in ops.items():
+        for kk in (k, 0.0, -0.0, 70.00001, float(np.float32(0.1)), 0.1):
+            got = eval_pred(cols, Pred("v", name, kk))
+            want = np.array([f(float(x), kk) for x in vals])
+            np.testing.assert_array_equal(got, want, err_msg=f"{name} {kk}")
+    # the fp64 constant is not rounded to fp32 first: 0.1 (fp64) > 0.1f32 is False
+    assert not eval_pred({"v": np.float32([0.1])}, Pred("v", "lt", 0.1))[0]
+    with pytest.raises(ValueError):
+        eval_pred(cols, Pred("v", "in", values=(1,)))
+
+
+def test_sum_f32_is_the_exactly_rounded_sum():
+    """SUM equals the rational sum of the fp32 values rounded once to fp64:
+    checked with exact Fraction arithmetic on random values of mixed scale,
+    on cancelling pairs (exactly 0) and on a closed form."""
+    from fractions import Fraction
+    r = np.random.default_rng(3)
+    for n in (1, 2, 17, 500):
+        v = (r.standard_normal(n) * 10.0 ** r.integers(-20, 20, n)).astype(np.float32)
+        exact = sum((Fraction(float(x)) for x in v), Fraction(0))
+        assert sum_f32(v) == float(exact)
+    v = r.standard_normal(999).astype(np.float32)
+    assert sum_f32(np.concatenate([v, -v[::-1]])) == 0.0
+    # closed form: n copies of x sum to n * x exactly while below 2^53 ulps
+    x = np.float32(0.1)
+    assert sum_f32(np.full(1000, x, dtype=np.float32)) == float(Fraction(float(x)) * 1000)
+    assert sum_f32(np.zeros(0, dtype=np.float32)) == 0.0
+
+
+def test_aggregate_sum_over_kept_rows():
+    probe = {"v": np.float32([1.5, 2.25, -4.0, 8.0, 0.125]), "id": np.arange(5, dtype=np.int32)}
+    q = Query(preds=(), labels=(1, 2), decision="binary_gt", agg="sum_f32", group_col="v")
+    rows = np.array([0, 1, 3, 4])
+    labels = np.array([1, 0, 1, 1])
+    out = aggregate({"probe": probe}, rows, None, labels, q)
+    assert out["count"] == 3
+    np.testing.assert_array_equal(out["kept_ids"], [0, 3, 4])
+    assert out["sum"] == 1.5 + 8.0 + 0.125
