@@ -117,7 +117,14 @@ def count_by(keys: np.ndarray):
 def sum_f32(values: np.ndarray) -> float:
     """SUM of an fp32 column over the kept rows (the float aggregate of the
     paper's running query, Table 1 SUM row and Figure 2): the exact sum of the
-    values, rounded once to fp64 (math.fsum)."""
+    values, rounded once to fp64 (math.fsum).  Non-finite values follow IEEE
+    addition, whose result then does not depend on the order: NaN if any
+    value is NaN or both infinities occur, else the infinity."""
     import math
-    return math.fsum(float(x) for x in np.asarray(values, dtype=np.float32))
+    v = np.asarray(values, dtype=np.float32).astype(np.float64)
+    if not np.isfinite(v).all():
+        if np.isnan(v).any() or (np.isposinf(v).any() and np.isneginf(v).any()):
+            return float("nan")
+        return float("inf") if np.isposinf(v).any() else float("-inf")
+    return math.fsum(v.tolist())
 

@@ -224,6 +224,23 @@ def test_sum_f32_is_the_exactly_rounded_sum():
     assert sum_f32(np.zeros(0, dtype=np.float32)) == 0.0
 
 
+def test_sum_f32_non_finite_follows_ieee():
+    inf, nan = np.float32(np.inf), np.float32(np.nan)
+    assert sum_f32(np.float32([1, inf, 2])) == np.inf
+    assert sum_f32(np.float32([-inf, 5])) == -np.inf
+    assert np.isnan(sum_f32(np.float32([inf, -inf])))
+    assert np.isnan(sum_f32(np.float32([1, nan])))
+    # the same as IEEE left-to-right addition in any order
+    for v in ([1, inf, -3], [inf, -inf, 2], [nan, 1], [-inf, -inf]):
+        a = np.float32(v).astype(np.float64)
+        for order in (a, a[::-1]):
+            acc = 0.0
+            for x in order:
+                acc += x
+            got = sum_f32(np.float32(v))
+            assert (np.isnan(acc) and np.isnan(got)) or acc == got
+
+
 def test_aggregate_sum_over_kept_rows():
     probe = {"v": np.float32([1.5, 2.25, -4.0, 8.0, 0.125]), "id": np.arange(5, dtype=np.int32)}
     q = Query(preds=(), labels=(1, 2), decision="binary_gt", agg="sum_f32", group_col="v")
