@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define AIQ_ABI_VERSION 1
+#define AIQ_ABI_VERSION 2
 
 typedef enum aiq_status {
   AIQ_OK = 0,
@@ -76,7 +76,9 @@ typedef enum aiq_decision { AIQ_DECIDE_BINARY_GT = 1, AIQ_DECIDE_ARGMAX = 2 } ai
 typedef enum aiq_agg {
   AIQ_AGG_COUNT = 1,             /* COUNT(*) of kept rows (+ their ids)                  */
   AIQ_AGG_AVG_LABEL_COUNT_BY = 2,/* GROUP BY probe column: COUNT(*), SUM/AVG(label)      */
-  AIQ_AGG_COUNT_BY_PAYLOAD = 3   /* GROUP BY joined build payload: COUNT(*) of kept rows */
+  AIQ_AGG_COUNT_BY_PAYLOAD = 3,  /* GROUP BY joined build payload: COUNT(*) of kept rows */
+  AIQ_AGG_SUM_F32 = 4            /* SUM of an fp32 probe column over the kept rows, in
+                                    fp64 (+ COUNT and ids); Table 1 SUM row, Figure 2     */
 } aiq_agg;
 typedef enum aiq_logits_mode { AIQ_LOGITS_LABELS = 1, AIQ_LOGITS_FULL_VOCAB = 2 } aiq_logits_mode;
 
@@ -125,13 +127,19 @@ typedef struct aiq_table {
   int32_t max_list_len;          /* host: declared bound on any row's list length */
 } aiq_table;
 
-/* one predicate atom: cols[col] op k, or cols[col] IN set[0..n_set) */
+/*
+ * One predicate atom: cols[col] op k, or cols[col] IN set[0..n_set).
+ * Integer columns compare exactly with k; an AIQ_F32 column compares its
+ * value, widened to fp64, with fk under IEEE rules (NaN fails every
+ * comparison but NE); IN on an AIQ_F32 column is AIQ_EUNSUPPORTED.
+ */
 typedef struct aiq_pred {
   int32_t col;
   int32_t op;                    /* aiq_op */
-  int64_t k;
+  int64_t k;                     /* integer columns */
   int32_t n_set;
   int64_t set[AIQ_MAX_IN_SET];
+  double fk;                     /* AIQ_F32 columns */
 } aiq_pred;
 
 /*
@@ -181,7 +189,8 @@ typedef struct aiq_query {
   int32_t decision;                    /* aiq_decision: BINARY_GT keeps a row iff
                                           logit[label_ids[0]] > logit[label_ids[1]] */
   int32_t agg;                         /* aiq_agg */
-  int32_t group_col;                   /* AVG_LABEL_COUNT_BY: probe column (I32) */
+  int32_t group_col;                   /* AVG_LABEL_COUNT_BY: probe key column (integer);
+                                          SUM_F32: the summed probe column (AIQ_F32) */
   int32_t n_group_keys;                /* group keys are codes in [0, n_group_keys) */
 } aiq_query;
 
@@ -224,6 +233,10 @@ typedef struct aiq_out {
   int64_t* grp_sum;          /* SUM(label) (0 for COUNT_BY_PAYLOAD) */
   double* grp_avg;           /* SUM/COUNT in fp64 (0 for COUNT_BY_PAYLOAD) */
   int64_t grp_cap;
+  /* SUM_F32: the sum, accumulated in fp64 in an order fixed by the number of
+     selected rows alone, so repeated runs give the same bits.  Its distance
+     to the exactly rounded sum is at most 2^-52 * (n_kept + 64) * sum|v|. */
+  double* sum_out;
 } aiq_out;
 
 /*

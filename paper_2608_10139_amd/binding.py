@@ -13,12 +13,13 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libaiq.so")
 
+AIQ_ABI_VERSION = 2   # the struct layouts below
 AIQ_OK, AIQ_EINVAL, AIQ_EUNSUPPORTED, AIQ_ENOSPC, AIQ_EHIP, AIQ_ENOMEM = 0, -1, -2, -3, -4, -5
 AIQ_I8, AIQ_I16, AIQ_I32, AIQ_F32, AIQ_BF16, AIQ_F16 = 1, 2, 3, 4, 5, 6
 AIQ_LT, AIQ_LE, AIQ_GT, AIQ_GE, AIQ_EQ, AIQ_NE, AIQ_IN = range(7)
 AIQ_ACT_GELU_ERF, AIQ_ACT_SWIGLU = 1, 2
 AIQ_DECIDE_BINARY_GT, AIQ_DECIDE_ARGMAX = 1, 2
-AIQ_AGG_COUNT, AIQ_AGG_AVG_LABEL_COUNT_BY, AIQ_AGG_COUNT_BY_PAYLOAD = 1, 2, 3
+AIQ_AGG_COUNT, AIQ_AGG_AVG_LABEL_COUNT_BY, AIQ_AGG_COUNT_BY_PAYLOAD, AIQ_AGG_SUM_F32 = 1, 2, 3, 4
 AIQ_LOGITS_LABELS, AIQ_LOGITS_FULL_VOCAB = 1, 2
 AIQ_PLAN_RELATIONAL_ONLY = 1
 
@@ -46,7 +47,7 @@ class aiq_table(C.Structure):
 
 class aiq_pred(C.Structure):
     _fields_ = [("col", C.c_int32), ("op", C.c_int32), ("k", C.c_int64), ("n_set", C.c_int32),
-                ("set", C.c_int64 * AIQ_MAX_IN_SET)]
+                ("set", C.c_int64 * AIQ_MAX_IN_SET), ("fk", C.c_double)]
 
 
 class aiq_layer(C.Structure):
@@ -82,7 +83,8 @@ class aiq_out(C.Structure):
     _fields_ = [("scalars", C.c_void_p), ("ids", C.c_void_p), ("ids_cap", C.c_int64),
                 ("sel_ids", C.c_void_p), ("sel_labels", C.c_void_p), ("sel_logits", C.c_void_p),
                 ("sel_cap", C.c_int64), ("grp_key", C.c_void_p), ("grp_count", C.c_void_p),
-                ("grp_sum", C.c_void_p), ("grp_avg", C.c_void_p), ("grp_cap", C.c_int64)]
+                ("grp_sum", C.c_void_p), ("grp_avg", C.c_void_p), ("grp_cap", C.c_int64),
+                ("sum_out", C.c_void_p)]
 
 
 class aiq_trace(C.Structure):
@@ -129,6 +131,9 @@ def load(path: str = LIB_PATH) -> C.CDLL:
     lib.aiq_status_str.restype = C.c_char_p
     lib.aiq_abi_version.argtypes = []
     lib.aiq_abi_version.restype = C.c_int32
+    if lib.aiq_abi_version() != AIQ_ABI_VERSION:
+        raise RuntimeError(f"{path} has ABI version {lib.aiq_abi_version()}, this binding expects "
+                           f"{AIQ_ABI_VERSION}: rebuild it")
     _lib = lib
     return lib
 

@@ -63,13 +63,15 @@ aiq_status make_preds(const aiq_pred* src, int n, const std::vector<aiq_col>& co
     const aiq_pred& p = src[i];
     if (p.col < 0 || p.col >= static_cast<int>(cols.size())) return AIQ_EINVAL;
     const aiq_col& c = cols[p.col];
-    if (!int_dtype(c.dtype)) return AIQ_EUNSUPPORTED;
+    if (!int_dtype(c.dtype) && c.dtype != AIQ_F32) return AIQ_EUNSUPPORTED;
     if (p.op < AIQ_LT || p.op > AIQ_IN) return AIQ_EINVAL;
+    if (c.dtype == AIQ_F32 && p.op == AIQ_IN) return AIQ_EUNSUPPORTED;
     DPred& d = out->p[i];
     d.data = c.data;
     d.dtype = c.dtype;
     d.op = p.op;
     d.k = p.k;
+    d.fk = p.fk;
     d.n_set = 0;
     if (p.op == AIQ_IN) {
       if (p.n_set < 0 || p.n_set > AIQ_MAX_IN_SET) return AIQ_EINVAL;
@@ -195,7 +197,8 @@ Layout run_layout(const aiq_plan* p) {
     return L;
   }
   L.packed = c.take(static_cast<size_t>(p->t_ub + 1) * 4);
-  L.bins = c.take(static_cast<size_t>(std::max(p->q.n_group_keys, 1)) * 16);
+  L.bins = c.take(std::max<size_t>(static_cast<size_t>(std::max(p->q.n_group_keys, 1)) * 16,
+                                   SUM_BLOCKS * sizeof(double)));   // group bins, or SUM partials
   L.desc = c.take(static_cast<size_t>(p->n_chunks) * D_STRIDE * 8);
   L.rcos = c.take(static_cast<size_t>(p->max_seq) * (p->hd / 2) * 4);
   L.rsin = c.take(static_cast<size_t>(p->max_seq) * (p->hd / 2) * 4);
@@ -506,6 +509,10 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
       case AIQ_AGG_COUNT_BY_PAYLOAD:
         if (!q.join || q.n_group_keys <= 0) return fail(AIQ_EINVAL);
         break;
+      case AIQ_AGG_SUM_F32:
+        if (q.group_col < 0 || q.group_col >= static_cast<int>(p->probe_cols.size())) return fail(AIQ_EINVAL);
+        if (p->probe_cols[q.group_col].dtype != AIQ_F32) return fail(AIQ_EUNSUPPORTED);
+        break;
       default: return fail(AIQ_EINVAL);
     }
     p->n_rows = p->probe.n_rows;
@@ -552,9 +559,10 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
   if (!p->has_probe) return AIQ_EINVAL;
   if (out->ids_cap < 0 || (out->ids_cap > 0 && !out->ids)) return AIQ_EINVAL;
   const aiq_query& q = p->q;
-  if (q.agg != AIQ_AGG_COUNT &&
-      (!out->grp_key || !out->grp_count || !out->grp_sum || !out->grp_avg || out->grp_cap <= 0))
+  const bool grouped = q.agg == AIQ_AGG_AVG_LABEL_COUNT_BY || q.agg == AIQ_AGG_COUNT_BY_PAYLOAD;
+  if (grouped && (!out->grp_key || !out->grp_count || !out->grp_sum || !out->grp_avg || out->grp_cap <= 0))
     return AIQ_EINVAL;
+  if (q.agg == AIQ_AGG_SUM_F32 && !out->sum_out) return AIQ_EINVAL;
   if (out->sel_cap < 0) return AIQ_EINVAL;
   const Layout L = run_layout(p);
   if (ws_bytes < L.total) return AIQ_ENOSPC;
@@ -645,7 +653,7 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
   } else {
     HIP_TRY(launch_copy_ids(sel, ctr + C_SEL, n, out->ids, out->ids_cap, ctr, 1, s));
   }
-  if (q.agg != AIQ_AGG_COUNT) {
+  if (grouped) {
     int64_t* bins = at<int64_t>(ws, L.bins);
     HIP_TRY(launch_fill_i64(bins, 2 * int64_t(q.n_group_keys), 0, s));
     const int mode = q.agg == AIQ_AGG_AVG_LABEL_COUNT_BY ? 1 : 2;
@@ -656,6 +664,9 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
     HIP_TRY(launch_group_emit(bins, q.n_group_keys, out->grp_key, out->grp_count, out->grp_sum, out->grp_avg,
                               out->grp_cap, mode, ctr, s));
   }
+  if (q.agg == AIQ_AGG_SUM_F32)
+    HIP_TRY(launch_sum_f32(sel, label, ctr + C_SEL, static_cast<const float*>(p->probe_cols[q.group_col].data),
+                           q.decision == AIQ_DECIDE_BINARY_GT, at<double>(ws, L.bins), out->sum_out, s));
   if (out->sel_cap > 0) {
     if (out->sel_ids) HIP_TRY(launch_copy_ids(sel, ctr + C_SEL, n, out->sel_ids, out->sel_cap, ctr, 0, s));
     if (out->sel_labels) HIP_TRY(launch_copy_ids(label, ctr + C_SEL, n, out->sel_labels, out->sel_cap, ctr, 0, s));

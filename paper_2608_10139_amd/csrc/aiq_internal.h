@@ -28,7 +28,8 @@ struct DPred {
   const void* data;
   int32_t dtype;
   int32_t op;
-  int64_t k;
+  int64_t k;          // integer columns
+  double fk;          // AIQ_F32 columns
   int32_t n_set;
   int32_t set[AIQ_MAX_IN_SET];
 };
@@ -109,6 +110,13 @@ hipError_t launch_copy_ids(const int32_t* src, const int64_t* n_ptr, int64_t n_u
 hipError_t launch_copy_f32(const float* src, const int64_t* n_ptr, int64_t n_ub, int32_t per_row,
                            float* dst, int64_t cap_rows, hipStream_t s);
 hipError_t launch_finalize(const int64_t* ctr, int64_t* scalars, hipStream_t s);
+// SUM_F32: fp64 sum of col[sel[i]] over the selected rows i < n_sel with
+// label[i] == 1 (binary decision) or all of them (argmax), in a fixed order:
+// SUM_BLOCKS fixed ranges of i, each reduced in a fixed tree, then the block
+// partials in a fixed tree.  partial: [SUM_BLOCKS] scratch.
+constexpr int SUM_BLOCKS = 1024;
+hipError_t launch_sum_f32(const int32_t* sel, const int32_t* label, const int64_t* n_ptr, const float* col,
+                          int binary, double* partial, double* out, hipStream_t s);
 
 // packing / chunking
 struct Prefix {

@@ -226,6 +226,43 @@ __device__ __forceinline__ uint32_t atom16(const DPred& P, int64_t r0, int64_t n
   }
 }
 
+// fp32 columns: each value widened to fp64 and compared with the fp64
+// constant (IEEE: NaN fails every comparison but NE).
+template <typename Cmp>
+__device__ __forceinline__ uint32_t atom16f_op(const float* col, int64_t r0, int64_t n_rows, Cmp cmp) {
+  float v[16];
+  if (r0 + 16 <= n_rows) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float4 f = *reinterpret_cast<const float4*>(col + r0 + 4 * q);
+      v[4 * q] = f.x;
+      v[4 * q + 1] = f.y;
+      v[4 * q + 2] = f.z;
+      v[4 * q + 3] = f.w;
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) v[k] = r0 + k < n_rows ? col[r0 + k] : 0.f;
+  }
+  uint32_t bits = 0;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) bits |= static_cast<uint32_t>(cmp(static_cast<double>(v[k]))) << k;
+  return bits;
+}
+
+__device__ __forceinline__ uint32_t atom16f(const DPred& P, int64_t r0, int64_t n_rows) {
+  const float* col = static_cast<const float*>(P.data);
+  const double k = P.fk;
+  switch (P.op) {
+    case AIQ_LT: return atom16f_op(col, r0, n_rows, [=](double x) { return x < k; });
+    case AIQ_LE: return atom16f_op(col, r0, n_rows, [=](double x) { return x <= k; });
+    case AIQ_GT: return atom16f_op(col, r0, n_rows, [=](double x) { return x > k; });
+    case AIQ_GE: return atom16f_op(col, r0, n_rows, [=](double x) { return x >= k; });
+    case AIQ_EQ: return atom16f_op(col, r0, n_rows, [=](double x) { return x == k; });
+    default: return atom16f_op(col, r0, n_rows, [=](double x) { return x != k; });   // NE (IN rejected at plan)
+  }
+}
+
 __global__ __launch_bounds__(REL_THREADS) void k_row_mask(DPredList preds, int64_t n_rows,
                                                           const void* probe_key, int32_t pk_dt,
                                                           HashArgs h, int join, uint64_t* mask,
@@ -243,6 +280,7 @@ __global__ __launch_bounds__(REL_THREADS) void k_row_mask(DPredList preds, int64
       const DPred& P = preds.p[i];
       if (P.dtype == AIQ_I8) keep &= atom16<int8_t>(P, r0, n_rows);
       else if (P.dtype == AIQ_I16) keep &= atom16<int16_t>(P, r0, n_rows);
+      else if (P.dtype == AIQ_F32) keep &= atom16f(P, r0, n_rows);
       else keep &= atom16<int32_t>(P, r0, n_rows);
     }
     if (join) {
@@ -767,6 +805,50 @@ __global__ void k_finalize(const int64_t* ctr, int64_t* scalars) {
 
 hipError_t launch_finalize(const int64_t* ctr, int64_t* scalars, hipStream_t s) {
   hipLaunchKernelGGL(k_finalize, dim3(1), dim3(64), 0, s, ctr, scalars);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ SUM of an fp32 column
+// Deterministic fp64 sum: SUM_BLOCKS fixed ranges of the selected rows (a
+// function of their count only), each summed by 256 threads in index order
+// and combined by a fixed butterfly and the four wave sums in order; the
+// partials are then combined the same way by one workgroup.
+
+__device__ __forceinline__ double block_sum_fixed(double v, double* wsum, int nw) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  if (lane == 0) wsum[w] = v;
+  __syncthreads();
+  double t = 0.0;
+  for (int i = 0; i < nw; ++i) t += wsum[i];
+  return t;
+}
+
+__global__ __launch_bounds__(256) void k_sum_partial(const int32_t* sel, const int32_t* label, const int64_t* n_ptr,
+                                                     const float* col, int binary, double* partial) {
+  __shared__ double wsum[4];
+  const int64_t n = *n_ptr;
+  const int64_t chunk = (n + SUM_BLOCKS - 1) / SUM_BLOCKS;
+  const int64_t lo = blockIdx.x * chunk;
+  const int64_t hi = lo + chunk < n ? lo + chunk : n;
+  double acc = 0.0;
+  for (int64_t i = lo + threadIdx.x; i < hi; i += 256)
+    if (!binary || label[i] == 1) acc += static_cast<double>(col[sel[i]]);
+  const double t = block_sum_fixed(acc, wsum, 4);
+  if (threadIdx.x == 0) partial[blockIdx.x] = t;
+}
+
+__global__ __launch_bounds__(SUM_BLOCKS) void k_sum_final(const double* partial, double* out) {
+  __shared__ double wsum[SUM_BLOCKS / 64];
+  const double t = block_sum_fixed(partial[threadIdx.x], wsum, SUM_BLOCKS / 64);
+  if (threadIdx.x == 0) out[0] = t;
+}
+
+hipError_t launch_sum_f32(const int32_t* sel, const int32_t* label, const int64_t* n_ptr, const float* col,
+                          int binary, double* partial, double* out, hipStream_t s) {
+  hipLaunchKernelGGL(k_sum_partial, dim3(SUM_BLOCKS), dim3(256), 0, s, sel, label, n_ptr, col, binary, partial);
+  hipLaunchKernelGGL(k_sum_final, dim3(1), dim3(SUM_BLOCKS), 0, s, partial, out);
   return hipGetLastError();
 }
 

@@ -20,10 +20,11 @@ import torch
 
 from . import binding as B
 
-_NP_DTYPE = {np.dtype(np.int8): B.AIQ_I8, np.dtype(np.int16): B.AIQ_I16, np.dtype(np.int32): B.AIQ_I32}
+_NP_DTYPE = {np.dtype(np.int8): B.AIQ_I8, np.dtype(np.int16): B.AIQ_I16, np.dtype(np.int32): B.AIQ_I32,
+             np.dtype(np.float32): B.AIQ_F32}
 _DECISION = {"binary_gt": B.AIQ_DECIDE_BINARY_GT, "argmax": B.AIQ_DECIDE_ARGMAX}
 _AGG = {"count": B.AIQ_AGG_COUNT, "avg_label_count_by": B.AIQ_AGG_AVG_LABEL_COUNT_BY,
-        "count_by_payload": B.AIQ_AGG_COUNT_BY_PAYLOAD}
+        "count_by_payload": B.AIQ_AGG_COUNT_BY_PAYLOAD, "sum_f32": B.AIQ_AGG_SUM_F32}
 _LIST_KEYS = ("offsets", "tokens")
 
 
@@ -121,11 +122,14 @@ class DeviceTable:
         self.struct = t
 
 
-def _pred(p, index: dict) -> B.aiq_pred:
+def _pred(p, table: "DeviceTable") -> B.aiq_pred:
     s = B.aiq_pred()
-    s.col = index[p.col]
+    s.col = table.index[p.col]
     s.op = B.OPS[p.op]
-    s.k = int(p.k)
+    if table.dtypes[p.col].kind == "f":
+        s.fk = float(p.k)
+    else:
+        s.k = int(p.k)
     vals = list(p.values)
     s.n_set = len(vals)
     for i, v in enumerate(vals):
@@ -138,7 +142,7 @@ def make_query(query, probe: DeviceTable | None, build: DeviceTable | None, pref
     preds = list(getattr(query, "preds", ()))
     q.n_pred = len(preds)
     for i, p in enumerate(preds):
-        q.preds[i] = _pred(p, probe.index)
+        q.preds[i] = _pred(p, probe)
     j = getattr(query, "join", None)
     if j is not None:
         q.join = 1
@@ -147,7 +151,7 @@ def make_query(query, probe: DeviceTable | None, build: DeviceTable | None, pref
         q.build_payload_col = build.index[j.payload]
         q.n_build_pred = len(j.build_preds)
         for i, p in enumerate(j.build_preds):
-            q.build_preds[i] = _pred(p, build.index)
+            q.build_preds[i] = _pred(p, build)
     n_prefix = int(getattr(query, "n_prefix", 0))
     q.n_prefix = n_prefix
     for i in range(n_prefix):
@@ -198,6 +202,7 @@ class DeviceQuery:
         self.grp_count = torch.zeros(G, dtype=torch.int64, device=dev)
         self.grp_sum = torch.zeros(G, dtype=torch.int64, device=dev)
         self.grp_avg = torch.zeros(G, dtype=torch.float64, device=dev)
+        self.sum_out = torch.zeros(1, dtype=torch.float64, device=dev)
         o = B.aiq_out()
         o.scalars, o.ids, o.ids_cap = _ptr(self.scalars), _ptr(self.ids), n
         o.sel_ids, o.sel_labels, o.sel_logits, o.sel_cap = (_ptr(self.sel_ids), _ptr(self.sel_labels),
@@ -205,6 +210,7 @@ class DeviceQuery:
         o.grp_key, o.grp_count, o.grp_sum, o.grp_avg = (_ptr(self.grp_key), _ptr(self.grp_count),
                                                         _ptr(self.grp_sum), _ptr(self.grp_avg))
         o.grp_cap = G
+        o.sum_out = _ptr(self.sum_out)
         self.out = o
 
     def run(self, trace=None, stream=None) -> None:
@@ -222,7 +228,9 @@ class DeviceQuery:
              "sel_ids": self.sel_ids[:n_sel].cpu().numpy().astype(np.int64),
              "labels": self.sel_labels[:n_sel].cpu().numpy().astype(np.int64),
              "logits": self.sel_logits[:n_sel * K].cpu().numpy().reshape(n_sel, K)}
-        if self.query.agg != "count":
+        if self.query.agg == "sum_f32":
+            r["sum"] = float(self.sum_out.cpu().item())
+        if self.query.agg in ("avg_label_count_by", "count_by_payload"):
             r["groups"] = (self.grp_key[:n_groups].cpu().numpy().astype(np.int64),
                            self.grp_count[:n_groups].cpu().numpy(), self.grp_sum[:n_groups].cpu().numpy(),
                            self.grp_avg[:n_groups].cpu().numpy())

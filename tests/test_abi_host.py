@@ -25,7 +25,9 @@ def test_library_exports_every_declared_function():
     assert set(declared) == set(B.EXPORTS)
     for fn in declared:
         assert hasattr(lib, fn), fn
-    assert B.aiq_abi_version() == 1
+    header = open(os.path.join(ROOT, "include", "aiq.h")).read()
+    declared_version = int(re.search(r"#define AIQ_ABI_VERSION (\d+)", header).group(1))
+    assert B.aiq_abi_version() == declared_version == B.AIQ_ABI_VERSION
     assert B.aiq_status_str(B.AIQ_ENOSPC) == "workspace or capacity too small"
 
 
@@ -121,6 +123,41 @@ def test_table_validation():
     assert B.aiq_plan_create_status(model(), t, None, query()) == B.AIQ_EINVAL
     t = table(); t.n_rows = -1
     assert B.aiq_plan_create_status(model(), t, None, query()) == B.AIQ_EINVAL
+
+
+def float_table(n=1000):
+    t = table(n)
+    t.cols[1].dtype = B.AIQ_F32
+    return t
+
+
+def test_float_column_rules():
+    q = query()
+    q.preds[0].col, q.preds[0].op, q.preds[0].fk = 1, B.AIQ_GT, 70.0
+    assert B.aiq_plan_create_status(model(), float_table(), None, q) == B.AIQ_OK
+    q.preds[0].op, q.preds[0].n_set = B.AIQ_IN, 1          # IN is integer-only
+    assert B.aiq_plan_create_status(model(), float_table(), None, q) == B.AIQ_EUNSUPPORTED
+    # SUM needs an fp32 column
+    assert B.aiq_plan_create_status(model(), float_table(), None,
+                                    query(agg=B.AIQ_AGG_SUM_F32, group_col=1)) == B.AIQ_OK
+    assert B.aiq_plan_create_status(model(), float_table(), None,
+                                    query(agg=B.AIQ_AGG_SUM_F32, group_col=0)) == B.AIQ_EUNSUPPORTED
+    # a relational-only plan has no labels to sum over
+    o = _opts(B.AIQ_PLAN_RELATIONAL_ONLY)
+    assert B.aiq_plan_create_status(model(), float_table(), None,
+                                    query(agg=B.AIQ_AGG_SUM_F32, group_col=1), o) == B.AIQ_EINVAL
+
+
+def test_sum_run_needs_output():
+    lib = B.load()
+    p = B.aiq_plan_create(model(), float_table(), None, query(agg=B.AIQ_AGG_SUM_F32, group_col=1))
+    try:
+        need = B.aiq_workspace_size(p)
+        out = B.aiq_out()
+        out.scalars, out.ids, out.ids_cap = FAKE, FAKE, 1000
+        assert lib.aiq_run(p, FAKE, need, C.byref(out), None, None) == B.AIQ_EINVAL   # no sum_out
+    finally:
+        B.aiq_plan_destroy(p)
 
 
 def _opts(flags):
