@@ -264,6 +264,56 @@ def relational_scale_leg(B, torch, sizes, thresholds, steps: int = 5) -> list:
     return out
 
 
+def pack_config_leg(B, torch, steps: int = 3) -> list:
+    """The pack stage (token counts -> cu_seqlens, token gather of every
+    selected row, chunk descriptors) at config size: the 1M-row sweep table
+    with every row selected (c < 1000) and the 131k-row group-by table (no
+    predicate).  Runs the whole query with no decoder layer (a 0-layer fp32
+    model: embedding -> head) and reads the pack stage's HIP-event time.
+    Algorithmic bytes: per selected row 8 B of offsets + 4 B of cu_seqlens,
+    per token 4 B read + 4 B written (+ 4 B per prefix token written)."""
+    from paper_2608_10139_amd.device import DeviceModel, DeviceQuery
+    from synth import WORKLOADS
+    from synth.configs import ModelSpec
+    from synth.gen import make_model, make_tables
+
+    # the tables' 32,000-token vocabulary; no layer runs (embedding -> head)
+    tiny = make_model(ModelSpec(n_layers=1, d_model=64, n_heads=2, n_kv_heads=2, d_ff=64, vocab=32000,
+                                act="gelu", dtype="f32", weight_seed=7))
+    dm = DeviceModel(tiny)
+    out = []
+    for name, qi in (("sweep3b", 3), ("groupby1b", 0)):
+        w = WORKLOADS[name]
+        log(f"[bench] pack at config size: generating {name}")
+        tables = make_tables(w)
+        q0 = w.queries[qi]
+        # the tiny model's labels and vocabulary; the selection of the workload's query
+        import dataclasses
+        q = dataclasses.replace(q0, labels=(1, 2), decision="binary_gt", agg="count")
+        probe = tables["probe"]
+        dq = DeviceQuery(tables, tiny, q, dmodel=dm, n_layers=0, want_sel=False)
+        dq.run()
+        torch.cuda.synchronize()
+        res = dq.results()
+        ev = HipEvents(2 * 8 * steps)
+        tr = make_trace(B, ev, 1 << B.AIQ_K_PACK)
+        for _ in range(steps):
+            dq.run(trace=tr)
+        torch.cuda.synchronize()
+        pack = float(np.sum(per_kind_ms(B, tr, ev).get(B.AIQ_K_PACK, []))) / steps
+        ev.close()
+        n_sel, n_tok = res["n_selected"], res["n_tokens"]
+        nbytes = 12 * n_sel + 8 * n_tok
+        gbps = nbytes / (pack * 1e-3) / 1e9
+        out.append({"table": name, "rows": len(probe["id"]), "selected": n_sel, "tokens": n_tok,
+                    "pack_ms": round(pack, 4), "algorithmic_bytes": nbytes, "gbps": round(gbps, 1),
+                    "hbm_frac": round(gbps / PEAK_HBM_GBPS, 4), "status": res["status"]})
+        log(f"[bench]   {out[-1]}")
+        dq.close()
+        del tables
+    return out
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -303,6 +353,7 @@ def main(argv=None) -> int:
     if a.relational_scale:
         torch.cuda.set_device(0)
         runs = relational_scale_leg(B, torch, [1 << 26, 1 << 28], [10, 1000], steps=a.steps)
+        packs = pack_config_leg(B, torch)
         best = max(runs, key=lambda r: r["gbps"])
         print(json.dumps({"metric": "relational stages (WHERE + stable compaction + token counts) HBM GB/s",
                           "value": best["gbps"], "unit": "GB/s", "n_gpus": 1, "steps": a.steps, "warmup": 1,
@@ -311,7 +362,7 @@ def main(argv=None) -> int:
                                                  "c and offsets only, relational-only plans"},
                           "roofline": {"bound": "hbm", "achieved": best["gbps"], "peak": PEAK_HBM_GBPS,
                                        "unit": "GB/s", "frac": best["hbm_frac"], "traffic": None},
-                          "runs": runs}), flush=True)
+                          "runs": runs, "pack_at_config_size": packs}), flush=True)
         return 0
     from synth import WORKLOADS
     from synth.gen import make_model, make_tables

@@ -28,7 +28,8 @@ __device__ __forceinline__ void set_status(int64_t* ctr, int64_t bits) {
 // ------------------------------------------------------------------ gather
 // One wave per sequence: the prompt prefix, then the row's tokens.  Token ids
 // outside [0, vocab) are flagged and replaced by 0 so later gathers stay in
-// bounds.
+// bounds.  The next sequence's extents are read while the current one is
+// copied, and each lane keeps four token loads in flight.
 __global__ __launch_bounds__(256) void k_gather(const int32_t* sel, const int64_t* n_ptr, const int64_t* off,
                                                 const int32_t* tokens, const int64_t* cu, Prefix pre,
                                                 int32_t vocab, int64_t t_ub, int32_t* packed, int64_t* ctr) {
@@ -37,24 +38,54 @@ __global__ __launch_bounds__(256) void k_gather(const int32_t* sel, const int64_
   const int64_t wave = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6;
   const int64_t n_waves = ((int64_t)gridDim.x * blockDim.x) >> 6;
   bool bad = false;
-  for (int64_t i = wave; i < n; i += n_waves) {
-    if (cu[i + 1] > t_ub) {   // more tokens than the table declared: never written
+  // extents of sequence i: packed [c0, c1), source tokens + s0
+  auto extents = [&](int64_t i, int64_t& c0, int64_t& c1, int64_t& s0) {
+    c0 = cu[i];
+    c1 = cu[i + 1];
+    s0 = off[sel[i]];
+  };
+  int64_t i = wave;
+  int64_t c0 = 0, c1 = 0, s0 = 0;
+  if (i < n) extents(i, c0, c1, s0);
+  while (i < n) {
+    const int64_t in = i + n_waves;
+    int64_t d0 = 0, d1 = 0, t0 = 0;
+    if (in < n) extents(in, d0, d1, t0);   // in flight during the copy below
+    if (c1 > t_ub) {   // more tokens than the table declared: never written
       bad = true;
-      continue;
-    }
-    const int64_t r = sel[i];
-    int32_t* dst = packed + cu[i];
-    for (int j = lane; j < pre.n; j += 64) dst[j] = pre.tok[j];
-    const int64_t L = cu[i + 1] - cu[i] - pre.n;
-    const int32_t* src = tokens + off[r];
-    for (int64_t j = lane; j < L; j += 64) {
-      int32_t t = src[j];
-      if (t < 0 || t >= vocab) {
-        bad = true;
-        t = 0;
+    } else {
+      int32_t* dst = packed + c0;
+      for (int j = lane; j < pre.n; j += 64) dst[j] = pre.tok[j];
+      const int64_t L = c1 - c0 - pre.n;
+      const int32_t* src = tokens + s0;
+      int32_t* out = dst + pre.n;
+      int64_t j = lane;
+      for (; j + 192 < L; j += 256) {
+        int32_t v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = src[j + 64 * u];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          if (v[u] < 0 || v[u] >= vocab) {
+            bad = true;
+            v[u] = 0;
+          }
+          out[j + 64 * u] = v[u];
+        }
       }
-      dst[pre.n + j] = t;
+      for (; j < L; j += 64) {
+        int32_t t = src[j];
+        if (t < 0 || t >= vocab) {
+          bad = true;
+          t = 0;
+        }
+        out[j] = t;
+      }
     }
+    i = in;
+    c0 = d0;
+    c1 = d1;
+    s0 = t0;
   }
   if (bad) set_status(ctr, AIQ_DEV_TOKEN_RANGE);
 }
@@ -63,7 +94,7 @@ hipError_t launch_gather_tokens(const int32_t* sel, const int64_t* n_ptr, int64_
                                 const int64_t* offsets, const int32_t* tokens, const int64_t* cu,
                                 const Prefix& prefix, int32_t vocab, int64_t t_ub, int32_t* packed,
                                 int64_t* ctr, hipStream_t s) {
-  hipLaunchKernelGGL(k_gather, dim3(grid_for(n_ub, 4, 2048)), dim3(256), 0, s, sel, n_ptr, offsets,
+  hipLaunchKernelGGL(k_gather, dim3(grid_for(n_ub, 4, 8192)), dim3(256), 0, s, sel, n_ptr, offsets,
                      tokens, cu, prefix, vocab, t_ub, packed, ctr);
   return hipGetLastError();
 }
