@@ -182,7 +182,9 @@ typedef struct aiq_query {
   int32_t probe_key_col, build_key_col, build_payload_col;
   int32_t n_build_pred;
   aiq_pred build_preds[AIQ_MAX_PREDS];
-  int32_t n_prefix;                    /* prompt tokens placed before each row's list */
+  int32_t n_prefix;                    /* prompt tokens placed before each row's list
+                                          (shared between rows on 16-bit models, see
+                                          AIQ_PLAN_UNSHARED_PREFIX) */
   int32_t prefix[AIQ_MAX_PREFIX];
   int32_t n_labels;                    /* 2..AIQ_MAX_LABELS */
   int32_t label_ids[AIQ_MAX_LABELS];
@@ -214,6 +216,22 @@ typedef struct aiq_plan_opts {
  * (its offsets are required).
  */
 #define AIQ_PLAN_RELATIONAL_ONLY 1
+
+/*
+ * Prompt prefix (the instruction of a prompted AI_IF, Table 1 and the join
+ * query of Section 4).  Row i's sequence is always prefix || row i's tokens,
+ * positions 0.. from the prefix start.  On 16-bit models with n_prefix > 0
+ * and at least one layer, aiq_run prefills the prefix once, keeps its keys
+ * and values for every layer, and runs each row's own tokens only, attending
+ * to the kept prefix: the result is the same function of the inputs as the
+ * per-row computation, with each row's own query positions meeting the same
+ * key blocks in the same order.  A row with an empty token list is then
+ * classified from the prefix's last token (per-row computation: the same).
+ * AIQ_PLAN_UNSHARED_PREFIX: recompute the prefix inside every row's sequence
+ * instead (fp32 models always do).  scalars[AIQ_S_TOKENS] counts the prefix
+ * once per selected row in both modes.
+ */
+#define AIQ_PLAN_UNSHARED_PREFIX 2
 
 /*
  * Outputs, all device buffers owned by the caller.  Optional buffers may be

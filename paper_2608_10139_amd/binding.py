@@ -22,6 +22,7 @@ AIQ_DECIDE_BINARY_GT, AIQ_DECIDE_ARGMAX = 1, 2
 AIQ_AGG_COUNT, AIQ_AGG_AVG_LABEL_COUNT_BY, AIQ_AGG_COUNT_BY_PAYLOAD, AIQ_AGG_SUM_F32 = 1, 2, 3, 4
 AIQ_LOGITS_LABELS, AIQ_LOGITS_FULL_VOCAB = 1, 2
 AIQ_PLAN_RELATIONAL_ONLY = 1
+AIQ_PLAN_UNSHARED_PREFIX = 2
 
 AIQ_DEV_TOKEN_RANGE, AIQ_DEV_DUP_KEY, AIQ_DEV_HASH_FULL, AIQ_DEV_IDS_CAP = 0x01, 0x02, 0x04, 0x08
 AIQ_DEV_GROUP_RANGE, AIQ_DEV_LIST_LEN, AIQ_DEV_GROUP_CAP = 0x10, 0x20, 0x40

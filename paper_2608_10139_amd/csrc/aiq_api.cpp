@@ -22,6 +22,9 @@ struct aiq_plan {
   std::vector<aiq_layer> layers;
   bool has_probe = false, has_build = false, has_query = false;
   bool rel_only = false;   // AIQ_PLAN_RELATIONAL_ONLY
+  // the prompt prefix is prefilled once per run and its keys / values are
+  // shared by every row (16-bit models, unless AIQ_PLAN_UNSHARED_PREFIX)
+  bool share_prefix = false;
   aiq_table probe{}, build{};
   std::vector<aiq_col> probe_cols, build_cols;
   aiq_query q{};
@@ -139,7 +142,8 @@ aiq_status validate_model(const aiq_model* m) {
 
 struct Layout {
   size_t ctr, mask, blk_cnt, blk_off, sel, payload, lens, label, logits, cu, blk_tok, tok_off, packed, hkeys, hvals,
-      bins, desc, rcos, rsin, rrev, x, delta, h, qkv, att, ffn, pos, hf, ssp, rs, total;
+      bins, desc, rcos, rsin, rrev, x, delta, h, qkv, att, ffn, pos, hf, ssp, rs, pkv, ptok, pcu, pdesc, pxlast,
+      total;
 };
 
 size_t act_bytes(const aiq_plan* p) { return p->bf16 ? 2 : 4; }
@@ -205,6 +209,14 @@ Layout run_layout(const aiq_plan* p) {
   L.rrev = c.take(static_cast<size_t>(p->hd / 2) * 4);
   take_resid(p, c, L, static_cast<size_t>(p->t_cap));
   L.hf = 0;
+  if (p->share_prefix) {   // per-layer q|k|v rows of the prefix, its batch, its last token's final state
+    const size_t np = static_cast<size_t>(p->prefix.n);
+    L.pkv = c.take(static_cast<size_t>(p->n_layers) * np * p->n_qkv * ab);
+    L.ptok = c.take(np * 4);
+    L.pcu = c.take(2 * 8);
+    L.pdesc = c.take(D_STRIDE * 8);
+    L.pxlast = c.take(static_cast<size_t>(d) * 4);
+  }
   L.total = c.off;
   return L;
 }
@@ -268,10 +280,23 @@ struct Tracer {
     (tr).end();                \
   } while (0)
 
+// Shared-prefix options of a chunk pass.  The prefix's own pass stores each
+// layer's q|k|v rows in qkv_layers (npre rows per layer) and runs no head;
+// the row passes read them back (pkv_layers), number positions from npre and
+// give rows without own tokens the prefix's final state (x_pre).
+struct PrefixUse {
+  void* qkv_layers = nullptr;
+  const void* pkv_layers = nullptr;
+  int32_t npre = 0;
+  const float* x_pre = nullptr;
+  bool head = true;
+};
+
 // Enqueues embedding, the layer stack and the label head for one chunk.
 aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int64_t* desc, const int64_t* cu,
                          int64_t* ctr, const int32_t* packed, int64_t t_cap, int64_t seq_ub, int32_t* label_out,
-                         float* logits_out, void* hf_out, Tracer& tr, hipStream_t s) {
+                         float* logits_out, void* hf_out, Tracer& tr, hipStream_t s,
+                         const PrefixUse& pu = PrefixUse{}) {
   const aiq_model& m = p->model;
   const int d = m.d_model;
   const int64_t* m_ptr = desc + D_NTOK;
@@ -330,14 +355,21 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
     // the consuming projection scales its rows by 1/rms, since
     // (x / rms * g) . W^T = ((x * g) . W^T) / rms.
     const float* g0 = p->n_layers > 0 ? p->layers[0].attn_norm : m.final_norm;
+    const int32_t pos_base = pu.pkv_layers ? pu.npre : 0;
     TRACED(tr, AIQ_K_EMBED, launch_embed_norm(desc, cu, packed, m.emb, m.wdtype, d, m.vocab, x, pos, ctr, g0, eps,
-                                              h, p->act, rs, t_cap, s));
+                                              h, p->act, rs, t_cap, s, pos_base));
+    const size_t pre_layer = static_cast<size_t>(pu.npre) * p->n_qkv * act_bytes(p);   // bytes per layer
     for (int l = 0; l < p->n_layers; ++l) {
       const aiq_layer& W = p->layers[l];
       const bool last = l + 1 == p->n_layers;
-      TRACED(tr, AIQ_K_GEMM_QKV, gemm(EPI_QKV_ROPE, h, d, p->n_qkv, d, W.wq, W.wk, W.wv, qkv, p->n_qkv));
+      void* qkv_l = pu.qkv_layers ? static_cast<char*>(pu.qkv_layers) + l * pre_layer : qkv;
+      TRACED(tr, AIQ_K_GEMM_QKV, gemm(EPI_QKV_ROPE, h, d, p->n_qkv, d, W.wq, W.wk, W.wv, qkv_l, p->n_qkv));
       AttnArgs aa{};
-      aa.qkv = qkv;
+      aa.qkv = qkv_l;
+      if (pu.pkv_layers) {
+        aa.pkv = static_cast<const char*>(pu.pkv_layers) + l * pre_layer;
+        aa.npre = pu.npre;
+      }
       aa.ld = p->n_qkv;
       aa.out = att;
       aa.ldo = p->d_q;
@@ -389,6 +421,7 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
     TRACED(tr, AIQ_K_GEMM_DOWN, gemm(EPI_STORE_F32, ffn, m.d_ff, d, m.d_ff, W.w_down, nullptr, nullptr, delta, d));
   }
   }
+  if (!pu.head) return AIQ_OK;
   HeadArgs ha{};
   ha.desc = desc;
   ha.cu = cu;
@@ -407,6 +440,7 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
   ha.hf_out = hf_out;
   ha.hf_act = p->act;
   ha.seq_ub = seq_ub;
+  ha.x_pre = pu.x_pre;
   TRACED(tr, AIQ_K_HEAD, launch_head(ha, s));
   return AIQ_OK;
 }
@@ -472,7 +506,7 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
     if (!query) return fail(AIQ_EINVAL);
     p->has_probe = true;
     p->rel_only = opts && (opts->flags & AIQ_PLAN_RELATIONAL_ONLY);
-    if (opts && (opts->flags & ~AIQ_PLAN_RELATIONAL_ONLY)) return fail(AIQ_EINVAL);
+    if (opts && (opts->flags & ~(AIQ_PLAN_RELATIONAL_ONLY | AIQ_PLAN_UNSHARED_PREFIX))) return fail(AIQ_EINVAL);
     st = copy_table(probe, &p->probe, &p->probe_cols, p->rel_only ? 1 : 2);
     if (st != AIQ_OK) return fail(st);
     const aiq_query& q = p->q;
@@ -516,8 +550,13 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
       default: return fail(AIQ_EINVAL);
     }
     p->n_rows = p->probe.n_rows;
-    p->t_ub = p->probe.n_list_tokens + p->n_rows * q.n_prefix;
-    p->max_seq = p->probe.max_list_len + q.n_prefix;
+    p->share_prefix = p->bf16 && q.n_prefix > 0 && p->n_layers > 0 && !p->rel_only &&
+                      !(opts && (opts->flags & AIQ_PLAN_UNSHARED_PREFIX));
+    // packed tokens: the row lists, plus the prefix per row unless it is shared
+    p->t_ub = p->probe.n_list_tokens + (p->share_prefix ? 0 : p->n_rows * q.n_prefix);
+    p->max_seq = p->probe.max_list_len + q.n_prefix;   // positions (rotary table rows)
+    // longest packed sequence: a chunk must hold one whole
+    const int64_t max_packed = p->share_prefix ? std::max<int64_t>(p->probe.max_list_len, q.n_prefix) : p->max_seq;
     // default chunk: about 48 GB of per-token activations (a fraction of one
     // MI355X's 288 GB), at most 4M tokens
     const int64_t per_tok = static_cast<int64_t>(resid_bytes(p)) +
@@ -525,11 +564,11 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
                                 (p->bf16 ? 2 : 4) + 4;
     const int64_t def_chunk = std::min<int64_t>((int64_t(48) << 30) / per_tok, int64_t(4) << 20);
     int64_t ct = (opts && opts->chunk_tokens > 0) ? opts->chunk_tokens : def_chunk;
-    ct = std::max<int64_t>(ct, p->max_seq);
-    ct = std::min<int64_t>(ct, std::max<int64_t>(p->t_ub, p->max_seq));
+    ct = std::max<int64_t>(ct, max_packed);
+    ct = std::min<int64_t>(ct, std::max<int64_t>(p->t_ub, max_packed));
     p->chunk_tokens = ct;
     p->n_chunks = std::max<int64_t>((p->t_ub + ct - 1) / ct, 1);
-    p->t_cap = ct + p->max_seq;
+    p->t_cap = ct + max_packed;
     p->seq_ub = std::min<int64_t>(p->n_rows, p->t_cap);
     p->prefix.n = q.n_prefix;
     for (int k = 0; k < q.n_prefix; ++k) p->prefix.tok[k] = q.prefix[k];
@@ -608,7 +647,8 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
   HIP_TRY(launch_scan_blocks(blk_cnt, nullptr, n, blk_off, ctr + C_SEL, s));
   // compaction: selected ids (straight into the caller's ids when nothing
   // else follows), join payloads, token counts and per-block token sums
-  ScatterLens sl{p->probe.list_offsets, p->probe.max_list_len, q.n_prefix, lens, blk_tok};
+  const int32_t npre_rows = p->share_prefix ? 0 : q.n_prefix;   // prefix tokens packed into each row
+  ScatterLens sl{p->probe.list_offsets, p->probe.max_list_len, npre_rows, lens, blk_tok};
   if (p->rel_only)
     HIP_TRY(launch_scatter_rows(mask, blk_off, nullptr, n, nullptr, out->ids, out->ids_cap, pkey, pkey_dt, h,
                                 p->has_build, payload, ctr, s,
@@ -631,16 +671,40 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
     return AIQ_OK;
   }
   // ---- pack: tokens, chunk descriptors
-  HIP_TRY(launch_gather_tokens(sel, ctr + C_SEL, n, p->probe.list_offsets, p->probe.list_tokens, cu, p->prefix,
+  Prefix row_prefix{};
+  if (!p->share_prefix) row_prefix = p->prefix;
+  HIP_TRY(launch_gather_tokens(sel, ctr + C_SEL, n, p->probe.list_offsets, p->probe.list_tokens, cu, row_prefix,
                                p->model.vocab, p->t_ub, packed, ctr, s));
   HIP_TRY(launch_chunk_desc(cu, ctr + C_SEL, p->chunk_tokens, p->n_chunks, p->t_ub, desc, s));
   HIP_TRY(launch_rope_table(p->max_seq, p->hd / 2, p->model.rope_theta, p->hd, at<float>(ws, L.rcos),
                             at<float>(ws, L.rsin), at<float>(ws, L.rrev), s));
   tr.end();
+  // ---- shared prompt prefix: its own prefill pass keeps every layer's q|k|v rows
+  PrefixUse rows_pu{};
+  if (p->share_prefix) {
+    const int32_t np = p->prefix.n;
+    int32_t* ptok = at<int32_t>(ws, L.ptok);
+    int64_t* pcu = at<int64_t>(ws, L.pcu);
+    int64_t* pdesc = at<int64_t>(ws, L.pdesc);
+    HIP_TRY(launch_prefix_batch(p->prefix, ptok, pcu, pdesc, s));
+    PrefixUse pre_pu{};
+    pre_pu.qkv_layers = at<void>(ws, L.pkv);
+    pre_pu.npre = np;
+    pre_pu.head = false;
+    const aiq_status e = enqueue_chunk(p, ws, L, pdesc, pcu, ctr, ptok, p->t_cap, 1, nullptr, nullptr, nullptr, tr,
+                                       s, pre_pu);
+    if (e != AIQ_OK) return e;
+    float* pxl = at<float>(ws, L.pxlast);
+    HIP_TRY(launch_copy_row_f32(at<float>(ws, L.x) + static_cast<int64_t>(np - 1) * p->model.d_model, pxl,
+                                p->model.d_model, s));
+    rows_pu.pkv_layers = at<void>(ws, L.pkv);
+    rows_pu.npre = np;
+    rows_pu.x_pre = pxl;
+  }
   // ---- prefill + label head, chunk by chunk
   for (int64_t c = 0; c < p->n_chunks; ++c) {
     const aiq_status e = enqueue_chunk(p, ws, L, desc + c * D_STRIDE, cu, ctr, packed, p->t_cap, p->seq_ub, label,
-                                       logits, nullptr, tr, s);
+                                       logits, nullptr, tr, s, rows_pu);
     if (e != AIQ_OK) return e;
   }
   // ---- decision -> kept ids, aggregates
@@ -673,7 +737,7 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
     if (out->sel_logits)
       HIP_TRY(launch_copy_f32(logits, ctr + C_SEL, n, q.n_labels, out->sel_logits, out->sel_cap, s));
   }
-  HIP_TRY(launch_finalize(ctr, out->scalars, s));
+  HIP_TRY(launch_finalize(ctr, out->scalars, s, p->share_prefix ? q.n_prefix : 0));
   tr.end();
   return AIQ_OK;
 }

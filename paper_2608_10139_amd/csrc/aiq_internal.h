@@ -109,7 +109,9 @@ hipError_t launch_copy_ids(const int32_t* src, const int64_t* n_ptr, int64_t n_u
                            int64_t cap, int64_t* ctr, int set_kept, hipStream_t s);
 hipError_t launch_copy_f32(const float* src, const int64_t* n_ptr, int64_t n_ub, int32_t per_row,
                            float* dst, int64_t cap_rows, hipStream_t s);
-hipError_t launch_finalize(const int64_t* ctr, int64_t* scalars, hipStream_t s);
+// scalars[AIQ_S_TOKENS] adds tok_per_row tokens per selected row to
+// ctr[C_TOK] (the shared prompt prefix, which is packed once, not per row).
+hipError_t launch_finalize(const int64_t* ctr, int64_t* scalars, hipStream_t s, int32_t tok_per_row = 0);
 // SUM_F32: fp64 sum of col[sel[i]] over the selected rows i < n_sel with
 // label[i] == 1 (binary decision) or all of them (argmax), in a fixed order:
 // SUM_BLOCKS fixed ranges of i, each reduced in a fixed tree, then the block
@@ -131,6 +133,10 @@ hipError_t launch_chunk_desc(const int64_t* cu, const int64_t* n_ptr, int64_t ch
                              int64_t n_chunks, int64_t t_ub, int64_t* desc, hipStream_t s);
 hipError_t launch_packed_desc(const int32_t* cu32, int32_t n_seq, int64_t n_tok, int64_t* cu64,
                               int64_t* desc, int64_t* ctr, hipStream_t s);
+// The shared prompt prefix as a one-sequence batch: tok[0..n) = prefix,
+// cu = {0, n}, desc = one chunk of n tokens.
+hipError_t launch_prefix_batch(const Prefix& prefix, int32_t* tok, int64_t* cu, int64_t* desc, hipStream_t s);
+hipError_t launch_copy_row_f32(const float* src, float* dst, int32_t n, hipStream_t s);
 
 // per-chunk transformer
 // cos/sin table [max_pos, hd/2] and the per-dim frequency in revolutions [hd/2]
@@ -141,10 +147,12 @@ hipError_t launch_embed(const int64_t* desc, const int64_t* cu, const int32_t* p
                         int64_t* ctr, int64_t t_cap, hipStream_t s);
 // MFMA path: the embedding also writes the first projection's operand
 // h = x * g (16-bit) and the row scale rs = 1 / sqrt(mean(x^2) + eps).
+// pos_base is added to every position (the row tokens that follow a shared
+// prefix start at the prefix length).
 hipError_t launch_embed_norm(const int64_t* desc, const int64_t* cu, const int32_t* packed, const void* emb,
                              int32_t wdtype, int32_t d, int32_t vocab, float* x, int32_t* pos, int64_t* ctr,
                              const float* g, float eps, void* h, int32_t h_act, float* rs, int64_t t_cap,
-                             hipStream_t s);
+                             hipStream_t s, int32_t pos_base = 0);
 // rs[t] = 1 / sqrt(sum_p ssp[t, p] / d + eps) for the chunk's tokens, the
 // partial sums added in order p = 0, 1, ...
 hipError_t launch_row_scale(const int64_t* desc, const float* ssp, int32_t n_part, int32_t d, float eps,
@@ -199,6 +207,11 @@ struct AttnArgs {
   int32_t n_heads, n_kv, hd;
   int64_t seq_ub;            // host upper bound on sequences per chunk
   int32_t out_act;           // MFMA path: output element type (1 bf16, 2 fp16)
+  // Shared prompt prefix (MFMA path): every sequence is read as
+  // pkv[0..npre) followed by its own rows, positions counted from the
+  // prefix start; only the own rows are queries.  pkv: [npre, ld] q|k|v rows.
+  const void* pkv;
+  int32_t npre;
 };
 hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s);
 hipError_t launch_attention_f32(const AttnArgs& a, hipStream_t s);
@@ -221,6 +234,8 @@ struct HeadArgs {
   void* hf_out;              // optional normalised rows [local seq, d] (full-vocab mode)
   int32_t hf_act;            // element type of hf_out (0 fp32, 1 bf16, 2 fp16)
   int64_t seq_ub;
+  const float* x_pre;        // shared prefix: final residual of its last token, used by
+                             // sequences with no own token (null: such sequences get 0 logits)
 };
 hipError_t launch_head(const HeadArgs& a, hipStream_t s);
 

@@ -16,6 +16,12 @@
 // for P^T, so probabilities never leave registers; V is staged transposed in
 // LDS.  The softmax denominator sums the fp16-rounded probabilities that the
 // P V product actually uses.
+//
+// Shared prompt prefix (MFMA path): a sequence is then the prefix's npre
+// rows (pkv, computed once) followed by its own rows, with blocks and
+// positions counted from the prefix start exactly as for the concatenated
+// sequence; only the own rows are queries.  Each own query therefore meets
+// the same key blocks, in the same order, as in the concatenated sequence.
 #include "aiq_internal.h"
 #include "dev_util.h"
 
@@ -47,6 +53,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   const int d_q = a.n_heads * HD, d_kv = a.n_kv * HD;
   const float scale = 1.4426950408889634f / sqrtf(static_cast<float>(HD));   // log2(e) / sqrt(hd)
   const uint16_t* qkv = static_cast<const uint16_t*>(a.qkv);
+  const uint16_t* pkv = static_cast<const uint16_t*>(a.pkv);
   uint16_t* out = static_cast<uint16_t*>(a.out);
 
   for (int64_t item = blockIdx.x; item < n_items; item += gridDim.x) {
@@ -54,16 +61,22 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
     const int h = static_cast<int>(item % a.n_heads);
     const int kvh = h / rep;
     const int64_t s0 = a.cu[sb + si] - tb;
-    const int L = static_cast<int>(a.cu[sb + si + 1] - a.cu[sb + si]);
+    const int np = a.npre;
+    const int Lo = static_cast<int>(a.cu[sb + si + 1] - a.cu[sb + si]);   // own rows
+    if (Lo == 0) continue;
+    const int L = Lo + np;   // positions 0 .. L-1, the first np in pkv
     const int qcol = h * HD, kcol = d_q + kvh * HD, vcol = d_q + d_kv + kvh * HD;
+    // row of position p: the prefix's rows, then the sequence's own rows
+    auto row_of = [&](int p) { return p < np ? pkv + static_cast<int64_t>(p) * a.ld : qkv + (s0 + p - np) * a.ld; };
 
-    for (int qb = 0; qb * KB < L; ++qb) {
-      const int qi = qb * KB + w * 16 + c16;   // this lane's query (column of S^T)
+    for (int qb = np / KB; qb * KB < L; ++qb) {
+      const int qi = qb * KB + w * 16 + c16;   // this lane's query position (column of S^T)
+      const bool q_own = qi >= np && qi < L;
       half8 qf[HD / 32];
 #pragma unroll
       for (int kc = 0; kc < HD / 32; ++kc) {
-        if (qi < L)
-          qf[kc] = *reinterpret_cast<const half8*>(qkv + (s0 + qi) * a.ld + qcol + kc * 32 + g * 8);
+        if (q_own)
+          qf[kc] = *reinterpret_cast<const half8*>(qkv + (s0 + qi - np) * a.ld + qcol + kc * 32 + g * 8);
         else
           qf[kc] = half8{};
       }
@@ -84,7 +97,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
           kr[u] = make_uint4(0, 0, 0, 0);
           vr[u] = make_uint4(0, 0, 0, 0);
           if (kk < L) {
-            const uint16_t* row = qkv + (s0 + kk) * a.ld;
+            const uint16_t* row = row_of(kk);
             kr[u] = *reinterpret_cast<const uint4*>(row + kcol + ch * 8);
             vr[u] = *reinterpret_cast<const uint4*>(row + vcol + ch * 8);
           }
@@ -177,9 +190,9 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
       float l_tot = l_run;
       l_tot += __shfl_xor(l_tot, 16);
       l_tot += __shfl_xor(l_tot, 32);
-      if (qi < L) {
+      if (q_own) {
         const float inv = 1.0f / l_tot;
-        uint16_t* orow = out + (s0 + qi) * a.ldo + h * HD;
+        uint16_t* orow = out + (s0 + qi - np) * a.ldo + h * HD;
 #pragma unroll
         for (int db = 0; db < HD / 16; ++db) {
           const f32x4 v = o[db];
@@ -194,6 +207,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
 }
 
 hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s) {
+  if (a.npre < 0 || (a.npre > 0 && !a.pkv)) return hipErrorInvalidValue;
   const int g = grid_cap(a.seq_ub * a.n_heads, 4096);
   if (a.hd == 64)
     hipLaunchKernelGGL(k_attn_bf16<64>, dim3(g), dim3(256), 0, s, a);
@@ -271,6 +285,7 @@ __global__ __launch_bounds__(64) void k_attn_f32(AttnArgs a) {
 }
 
 hipError_t launch_attention_f32(const AttnArgs& a, hipStream_t s) {
+  if (a.npre != 0) return hipErrorInvalidValue;   // no shared prefix on this path
   const int g = grid_cap(a.seq_ub * a.n_heads, 4096);
   switch (a.hd) {
     case 32: hipLaunchKernelGGL(k_attn_f32<32>, dim3(g), dim3(64), 0, s, a); break;

@@ -117,10 +117,13 @@ __global__ __launch_bounds__(256) void k_head(HeadArgs a) {
   const int d = a.d;
   for (int64_t i = wave; i < ns; i += n_waves) {
     const int64_t gi = sb + i;
-    const bool empty = a.cu[gi + 1] == a.cu[gi];   // no token: every logit is 0
-    const int64_t last = empty ? 0 : a.cu[gi + 1] - 1 - tb;
-    const float* xr = a.x + last * d;
-    const float* dr = a.delta ? a.delta + last * d : nullptr;   // last layer's pending output
+    // no own token: the shared prefix's last token, else every logit is 0
+    const bool no_own = a.cu[gi + 1] == a.cu[gi];
+    const bool empty = no_own && !a.x_pre;
+    const bool pre = no_own && a.x_pre;
+    const int64_t last = no_own ? 0 : a.cu[gi + 1] - 1 - tb;
+    const float* xr = pre ? a.x_pre : a.x + last * d;
+    const float* dr = (a.delta && !pre) ? a.delta + last * d : nullptr;   // last layer's pending output
     auto xv = [&](int c) { return dr ? xr[c] + dr[c] : xr[c]; };
     float ss = 0.f;
     for (int c = lane; c < d; c += 64) ss += xv(c) * xv(c);

@@ -174,6 +174,37 @@ hipError_t launch_packed_desc(const int32_t* cu32, int32_t n_seq, int64_t n_tok,
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ shared prompt prefix
+// The prefix alone as a packed batch of one sequence (its own prefill pass
+// produces the keys and values every row attends to).
+__global__ void k_prefix_batch(Prefix pre, int32_t* tok, int64_t* cu, int64_t* desc) {
+  const int i = threadIdx.x;
+  if (i < pre.n) tok[i] = pre.tok[i];
+  if (i == 0) {
+    cu[0] = 0;
+    cu[1] = pre.n;
+    desc[D_TOK_BEGIN] = 0;
+    desc[D_NTOK] = pre.n;
+    desc[D_SEQ_BEGIN] = 0;
+    desc[D_NSEQ] = 1;
+  }
+}
+
+hipError_t launch_prefix_batch(const Prefix& prefix, int32_t* tok, int64_t* cu, int64_t* desc, hipStream_t s) {
+  if (prefix.n <= 0 || prefix.n > AIQ_MAX_PREFIX) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_prefix_batch, dim3(1), dim3(AIQ_MAX_PREFIX), 0, s, prefix, tok, cu, desc);
+  return hipGetLastError();
+}
+
+__global__ void k_copy_row_f32(const float* src, float* dst, int32_t n) {
+  for (int i = threadIdx.x; i < n; i += blockDim.x) dst[i] = src[i];
+}
+
+hipError_t launch_copy_row_f32(const float* src, float* dst, int32_t n, hipStream_t s) {
+  hipLaunchKernelGGL(k_copy_row_f32, dim3(1), dim3(256), 0, s, src, dst, n);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ rotary table
 // cos / sin of pos * theta**(-2i/hd), evaluated in fp64 and rounded to fp32.
 __global__ void k_rope_table(int32_t max_pos, int32_t half, double theta, int32_t hd, float* cos_t, float* sin_t,
@@ -228,7 +259,7 @@ template <bool NORM>
 __global__ __launch_bounds__(256) void k_embed(const int64_t* desc, const int64_t* cu, const int32_t* packed,
                                                const void* emb, int32_t wdtype, int32_t d, int32_t vocab,
                                                float* x, int32_t* pos, int64_t* ctr, const float* g, float eps,
-                                               void* h, int32_t h_act, float* rs) {
+                                               void* h, int32_t h_act, float* rs, int32_t pos_base) {
   const int64_t tb = desc[D_TOK_BEGIN], nt = desc[D_NTOK], sb = desc[D_SEQ_BEGIN], ns = desc[D_NSEQ];
   const int lane = threadIdx.x & 63;
   const int64_t wave = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6;
@@ -241,7 +272,7 @@ __global__ __launch_bounds__(256) void k_embed(const int64_t* desc, const int64_
       tok = 0;
     }
     const int64_t sq = seq_of(cu, sb, ns, gt, lane);
-    if (lane == 0) pos[t] = static_cast<int32_t>(gt - cu[sq]);
+    if (lane == 0) pos[t] = pos_base + static_cast<int32_t>(gt - cu[sq]);
     float* xr = x + t * d;
     float ssq = 0.f;
     for (int c = lane * 4; c < d; c += 256) {
@@ -279,17 +310,17 @@ hipError_t launch_embed(const int64_t* desc, const int64_t* cu, const int32_t* p
                         const void* emb, int32_t wdtype, int32_t d, int32_t vocab, float* x, int32_t* pos,
                         int64_t* ctr, int64_t t_cap, hipStream_t s) {
   hipLaunchKernelGGL(k_embed<false>, dim3(grid_for(t_cap, 4, 8192)), dim3(256), 0, s, desc, cu, packed, emb,
-                     wdtype, d, vocab, x, pos, ctr, nullptr, 0.f, nullptr, 0, nullptr);
+                     wdtype, d, vocab, x, pos, ctr, nullptr, 0.f, nullptr, 0, nullptr, 0);
   return hipGetLastError();
 }
 
 hipError_t launch_embed_norm(const int64_t* desc, const int64_t* cu, const int32_t* packed, const void* emb,
                              int32_t wdtype, int32_t d, int32_t vocab, float* x, int32_t* pos, int64_t* ctr,
                              const float* g, float eps, void* h, int32_t h_act, float* rs, int64_t t_cap,
-                             hipStream_t s) {
+                             hipStream_t s, int32_t pos_base) {
   if (h_act == ACT_F32) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_embed<true>, dim3(grid_for(t_cap, 4, 8192)), dim3(256), 0, s, desc, cu, packed, emb,
-                     wdtype, d, vocab, x, pos, ctr, g, eps, h, h_act, rs);
+                     wdtype, d, vocab, x, pos, ctr, g, eps, h, h_act, rs, pos_base);
   return hipGetLastError();
 }
 

@@ -788,14 +788,14 @@ hipError_t launch_group_emit(const int64_t* bins, int32_t n_keys, int32_t* key_o
 
 // ------------------------------------------------------------------ finalize
 
-__global__ void k_finalize(const int64_t* ctr, int64_t* scalars) {
+__global__ void k_finalize(const int64_t* ctr, int64_t* scalars, int32_t tok_per_row) {
   const int i = threadIdx.x;
   if (i >= AIQ_N_SCALARS) return;
   int64_t v = 0;
   switch (i) {
     case AIQ_S_SELECTED: v = ctr[C_SEL]; break;
     case AIQ_S_KEPT: v = ctr[C_KEPT]; break;
-    case AIQ_S_TOKENS: v = ctr[C_TOK]; break;
+    case AIQ_S_TOKENS: v = ctr[C_TOK] + static_cast<int64_t>(tok_per_row) * ctr[C_SEL]; break;
     case AIQ_S_STATUS: v = ctr[C_STATUS]; break;
     case AIQ_S_GROUPS: v = ctr[C_GROUPS]; break;
     default: v = 0;
@@ -803,8 +803,8 @@ __global__ void k_finalize(const int64_t* ctr, int64_t* scalars) {
   scalars[i] = v;
 }
 
-hipError_t launch_finalize(const int64_t* ctr, int64_t* scalars, hipStream_t s) {
-  hipLaunchKernelGGL(k_finalize, dim3(1), dim3(64), 0, s, ctr, scalars);
+hipError_t launch_finalize(const int64_t* ctr, int64_t* scalars, hipStream_t s, int32_t tok_per_row) {
+  hipLaunchKernelGGL(k_finalize, dim3(1), dim3(64), 0, s, ctr, scalars, tok_per_row);
   return hipGetLastError();
 }
 

@@ -172,7 +172,7 @@ class DeviceQuery:
 
     def __init__(self, tables: dict, model, query, device="cuda", chunk_tokens: int = 0,
                  n_layers: int | None = None, dmodel: DeviceModel | None = None, relational_only: bool = False,
-                 want_sel: bool = True):
+                 want_sel: bool = True, share_prefix: bool = True):
         self.device = torch.device(device)
         self.query = query
         self.dm = dmodel if dmodel is not None else DeviceModel(model, device)
@@ -182,7 +182,8 @@ class DeviceQuery:
         opts = B.aiq_plan_opts()
         opts.chunk_tokens = int(chunk_tokens)
         opts.n_layers_override = _layers_opt(n_layers)
-        opts.flags = B.AIQ_PLAN_RELATIONAL_ONLY if relational_only else 0
+        opts.flags = (B.AIQ_PLAN_RELATIONAL_ONLY if relational_only else 0) | \
+            (0 if share_prefix else B.AIQ_PLAN_UNSHARED_PREFIX)
         self.plan = B.aiq_plan_create(self.dm.struct, self.probe.struct,
                                       self.build.struct if self.build else None, self.q, opts)
         self.ws_bytes = B.aiq_workspace_size(self.plan)

@@ -179,7 +179,34 @@ def test_relational_only_plan_validation():
     assert B.aiq_plan_create_status(model(), table(), None, q) == B.AIQ_OK
     assert B.aiq_plan_create_status(model(), table(), None, q, _opts(B.AIQ_PLAN_RELATIONAL_ONLY)) == B.AIQ_EINVAL
     # unknown flag bits
-    assert B.aiq_plan_create_status(model(), table(), None, query(), _opts(2)) == B.AIQ_EINVAL
+    assert B.aiq_plan_create_status(model(), table(), None, query(), _opts(4)) == B.AIQ_EINVAL
+    assert B.aiq_plan_create_status(model(), table(), None, query(), _opts(B.AIQ_PLAN_UNSHARED_PREFIX)) == B.AIQ_OK
+
+
+def _prefix_query(n):
+    q = query()
+    q.n_prefix = n
+    for k in range(n):
+        q.prefix[k] = 3 + k
+    return q
+
+
+def test_shared_prefix_is_packed_once():
+    # 1000 rows of 100 tokens with a 32-token prompt: the shared plan packs
+    # the 100,000 row tokens only (plus per-layer prefix keys / values), the
+    # unshared plan 132,000 tokens, and every per-token buffer grows with that
+    shared = B.aiq_plan_create(model(), table(), None, _prefix_query(32))
+    unshared = B.aiq_plan_create(model(), table(), None, _prefix_query(32), _opts(B.AIQ_PLAN_UNSHARED_PREFIX))
+    plain = B.aiq_plan_create(model(), table(), None, query())
+    try:
+        ws, wu, wp = (B.aiq_workspace_size(p) for p in (shared, unshared, plain))
+        assert wp <= ws < wu
+        # the shared plan adds only the prefix's per-layer q|k|v rows and its small batch
+        d, n_qkv, layers = 512, 512 * 3, 2
+        assert ws - wp <= layers * 32 * n_qkv * 2 + 32 * 4 + d * 4 + 4 * 4096
+    finally:
+        for p in (shared, unshared, plain):
+            B.aiq_plan_destroy(p)
 
 
 def test_relational_only_workspace_holds_no_model_activations():
