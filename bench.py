@@ -106,19 +106,29 @@ def per_kind_ms(B, trace, events) -> dict:
 
 
 # ------------------------------------------------------------------ algorithmic work
-def prefill_flops(spec, lens: np.ndarray, n_labels: int) -> dict:
+def prefill_flops(spec, own: np.ndarray, n_labels: int, npre: int = 0, shared: bool = False) -> dict:
     """Algorithmic FLOPs of the prefill (no padding): the four projections,
-    causal attention (unmasked half: QK^T and PV), and the label head."""
-    T = float(lens.sum())
+    causal attention (unmasked half: QK^T and PV), and the label head.
+    own: each selected row's token count; npre: prompt prefix length, packed
+    into every row, or with ``shared`` prefilled once and attended to by
+    every row's own positions npre.. ."""
+    own = np.asarray(own, dtype=np.float64)
     d, dq, dkv, f, L = spec.d_model, spec.d_q, spec.d_kv, spec.d_ff, spec.n_layers
     n_ffn = 3 if spec.act == "swiglu" else 2
+    if shared and npre > 0:
+        T = float(own.sum()) + npre
+        attn = float(np.sum(2.0 * dq * (2.0 * npre * own + own * (own + 1.0)))) + 2.0 * dq * npre * (npre + 1.0)
+    else:
+        lens = own + npre
+        T = float(lens.sum())
+        attn = float(np.sum(2.0 * dq * lens * (lens + 1.0)))
     per = {
         "qkv": 2 * T * d * (dq + 2 * dkv) * L,
         "o": 2 * T * dq * d * L,
         "up": 2 * T * d * f * (n_ffn - 1) * L,
         "down": 2 * T * f * d * L,
-        "attn": float(np.sum(2.0 * dq * lens * (lens + 1.0))) * L,
-        "head": 2.0 * len(lens) * n_labels * d,
+        "attn": attn * L,
+        "head": 2.0 * len(own) * n_labels * d,
     }
     per["total"] = sum(per.values())
     return per
@@ -325,6 +335,8 @@ def main(argv=None) -> int:
     ap.add_argument("--cpu-rows", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-split", action="store_true")
+    ap.add_argument("--unshared-prefix", action="store_true",
+                    help="recompute the prompt prefix inside every row (default: prefilled once and shared)")
     ap.add_argument("--relational-scale", action="store_true",
                     help="only the relational part at 2^26 and 2^28 rows (relational-only plans); one JSON line")
     ap.add_argument("--no-relational-scale", action="store_true",
@@ -375,7 +387,8 @@ def main(argv=None) -> int:
     tables = make_tables(w)
     model = make_model(spec)
     dm = DeviceModel(model, compute=a.compute)
-    dq = DeviceQuery(tables, model, q, dmodel=dm)
+    shared = q.n_prefix > 0 and dm.compute != "f32" and not a.unshared_prefix
+    dq = DeviceQuery(tables, model, q, dmodel=dm, share_prefix=not a.unshared_prefix)
     log(f"[bench] workspace {dq.ws_bytes / 2**30:.2f} GiB; warmup {a.warmup}")
 
     for _ in range(a.warmup):
@@ -386,12 +399,16 @@ def main(argv=None) -> int:
         raise RuntimeError(f"device status {res['status']:#x}")
     n_rows = len(tables["probe"]["id"])
     sel = res["sel_ids"]
-    lens = tables["probe"]["len"][sel].astype(np.float64) + q.n_prefix
+    own = tables["probe"]["len"][sel].astype(np.float64)
+    lens = own + q.n_prefix
     T = int(lens.sum())
     assert T == res["n_tokens"]
 
     # ---- timed region: whole steps; HIP events around the dominant kernel's launches only
-    launches_per_step = spec.n_layers * 8
+    # every prefill pass (chunk, or the shared prefix) launches the gate/up GEMM once per layer
+    chunks, pre_pass = B.aiq_plan_passes(dq.plan)
+    passes = chunks + pre_pass
+    launches_per_step = spec.n_layers * passes
     ev = HipEvents(2 * a.steps * launches_per_step)
     trace = make_trace(B, ev, 1 << B.AIQ_K_GEMM_UP)
     log(f"[bench] timing {a.steps} steps")
@@ -402,11 +419,13 @@ def main(argv=None) -> int:
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     ms_step = dt / a.steps * 1e3
+    if trace.count != a.steps * launches_per_step:
+        raise RuntimeError(f"traced {trace.count} gate/up launches, expected {a.steps * launches_per_step}")
     up = per_kind_ms(B, trace, ev).get(B.AIQ_K_GEMM_UP, [])
     ev.close()
-    fl = prefill_flops(spec, lens, len(q.labels))
-    # every launch of the gate/up GEMM covers one chunk; empty chunks (none at
-    # the default chunk size here) would contribute zero work
+    fl = prefill_flops(spec, own, len(q.labels), q.n_prefix, shared)
+    # every launch of the gate/up GEMM covers one chunk (or the shared prefix);
+    # chunks the selection leaves empty are launched and do no work
     n_up = len(up)
     up_flops_per_launch = fl["up"] * a.steps / max(n_up, 1)
     up_avg_ms = float(np.mean(up)) if up else float("nan")
@@ -414,10 +433,12 @@ def main(argv=None) -> int:
     peak = PEAK_F32_TFLOPS if dm.compute == "f32" else PEAK_BF16_TFLOPS   # fp16 and bf16 MFMA peaks are equal
 
     # ---- one untimed traced step for the stage breakdown
-    ev2 = HipEvents(2 * (launches_per_step + 64))
+    ev2 = HipEvents(2 * (passes * (8 * spec.n_layers + 2) + 64))
     tr2 = make_trace(B, ev2, 0xFFFFFFFF)
     dq.run(trace=tr2)
     torch.cuda.synchronize()
+    if tr2.count >= tr2.capacity:
+        raise RuntimeError("stage trace buffer full")
     kinds = per_kind_ms(B, tr2, ev2)
     ev2.close()
     names = {B.AIQ_K_REL: "relational", B.AIQ_K_PACK: "pack", B.AIQ_K_EMBED: "embed", B.AIQ_K_NORM: "rmsnorm",
@@ -453,6 +474,8 @@ def main(argv=None) -> int:
                    f"{spec.n_heads}q/{spec.n_kv_heads}kv ffn{spec.d_ff} {spec.act}, weights drawn in {spec.dtype}, "
                    f"projections in {dm.compute} with fp32 accumulation",
                    "parallelism": "single GPU"},
+        "prompt_prefix": {"tokens": q.n_prefix, "shared": shared} if q.n_prefix else None,
+        "prefill_flops": fl["total"],
         "tokens_per_s": round(T / (ms_step * 1e-3), 1),
         "prefill_tokens_per_s": round(T / (prefill_ms * 1e-3), 1) if prefill_ms > 0 else None,
         "prefill_mfma_frac": round(fl["total"] / (prefill_ms * 1e-3) / 1e12 / peak, 4) if prefill_ms > 0 else None,

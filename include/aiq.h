@@ -306,6 +306,17 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
 aiq_status aiq_workspace_size(const aiq_plan* plan, size_t* bytes);
 
 /*
+ * Prefill passes aiq_run enqueues: the chunks of the packed batch, an upper
+ * bound fixed at plan creation from the table's token total (chunks that
+ * the selection leaves empty cost one launch per kernel and no work), plus
+ * one pass for a shared prompt prefix.  Each pass launches the embedding,
+ * per layer the four projections, attention and the norm row scales, and,
+ * except the prefix pass, the label head.  For sizing trace buffers
+ * (aiq_trace).  Errors: AIQ_EINVAL (NULL argument, prefill-only plan).
+ */
+aiq_status aiq_plan_passes(const aiq_plan* plan, int64_t* chunks, int32_t* prefix_pass);
+
+/*
  * Enqueues the whole query on `stream`.  The workspace contents on entry do
  * not matter.  Outputs are valid after the caller synchronises the stream.
  * Errors: AIQ_EINVAL (NULL plan/out/scalars/ids, prefill-only plan, a

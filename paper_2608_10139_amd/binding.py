@@ -93,7 +93,7 @@ class aiq_trace(C.Structure):
                 ("capacity", C.c_int32), ("count", C.c_int32), ("kind_mask", C.c_uint32)]
 
 
-EXPORTS = ("aiq_plan_create", "aiq_workspace_size", "aiq_run", "aiq_prefill_workspace_size",
+EXPORTS = ("aiq_plan_create", "aiq_workspace_size", "aiq_plan_passes", "aiq_run", "aiq_prefill_workspace_size",
            "aiq_prefill_packed", "aiq_plan_destroy", "aiq_status_str", "aiq_abi_version")
 
 
@@ -120,6 +120,8 @@ def load(path: str = LIB_PATH) -> C.CDLL:
     lib.aiq_plan_create.restype = C.c_int
     lib.aiq_workspace_size.argtypes = [P, C.POINTER(C.c_size_t)]
     lib.aiq_workspace_size.restype = C.c_int
+    lib.aiq_plan_passes.argtypes = [P, C.POINTER(C.c_int64), C.POINTER(C.c_int32)]
+    lib.aiq_plan_passes.restype = C.c_int
     lib.aiq_run.argtypes = [P, P, C.c_size_t, C.POINTER(aiq_out), C.POINTER(aiq_trace), P]
     lib.aiq_run.restype = C.c_int
     lib.aiq_prefill_workspace_size.argtypes = [P, C.c_int64, C.POINTER(C.c_size_t)]
@@ -173,6 +175,14 @@ def aiq_workspace_size(plan) -> int:
     n = C.c_size_t()
     check("aiq_workspace_size", load().aiq_workspace_size(plan, C.byref(n)))
     return n.value
+
+
+def aiq_plan_passes(plan) -> tuple:
+    """(chunk passes, 1 if a shared-prefix pass runs else 0) of aiq_run."""
+    n = C.c_int64()
+    pp = C.c_int32()
+    check("aiq_plan_passes", load().aiq_plan_passes(plan, C.byref(n), C.byref(pp)))
+    return n.value, pp.value
 
 
 def aiq_prefill_workspace_size(plan, max_tokens: int) -> int:

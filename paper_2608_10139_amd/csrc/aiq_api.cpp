@@ -586,6 +586,13 @@ aiq_status aiq_workspace_size(const aiq_plan* plan, size_t* bytes) {
   return AIQ_OK;
 }
 
+aiq_status aiq_plan_passes(const aiq_plan* plan, int64_t* chunks, int32_t* prefix_pass) {
+  if (!plan || !chunks || !prefix_pass || !plan->has_probe) return AIQ_EINVAL;
+  *chunks = plan->rel_only ? 0 : plan->n_chunks;
+  *prefix_pass = plan->share_prefix ? 1 : 0;
+  return AIQ_OK;
+}
+
 aiq_status aiq_prefill_workspace_size(const aiq_plan* plan, int64_t max_tokens, size_t* bytes) {
   if (!plan || !bytes || max_tokens <= 0) return AIQ_EINVAL;
   *bytes = prefill_layout(plan, max_tokens).total;

@@ -191,6 +191,24 @@ def _prefix_query(n):
     return q
 
 
+def test_plan_passes():
+    shared = B.aiq_plan_create(model(), table(), None, _prefix_query(32))
+    unshared = B.aiq_plan_create(model(), table(), None, _prefix_query(32), _opts(B.AIQ_PLAN_UNSHARED_PREFIX))
+    rel = B.aiq_plan_create(model(), table(), None, query(), _opts(B.AIQ_PLAN_RELATIONAL_ONLY))
+    small = B.aiq_plan_opts()
+    small.chunk_tokens = 10_000
+    chunked = B.aiq_plan_create(model(), table(), None, query(), small)
+    try:
+        assert B.aiq_plan_passes(shared) == (1, 1)
+        assert B.aiq_plan_passes(unshared) == (1, 0)
+        assert B.aiq_plan_passes(rel) == (0, 0)
+        # 100,000 table tokens in chunks of 10,000
+        assert B.aiq_plan_passes(chunked) == (10, 0)
+    finally:
+        for p in (shared, unshared, rel, chunked):
+            B.aiq_plan_destroy(p)
+
+
 def test_shared_prefix_is_packed_once():
     # 1000 rows of 100 tokens with a 32-token prompt: the shared plan packs
     # the 100,000 row tokens only (plus per-layer prefix keys / values), the
