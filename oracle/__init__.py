@@ -23,9 +23,11 @@ from .relational import (eval_pred, select, hash_join, sequences, pack, group_av
 from .transformer import (rmsnorm, rope, causal_attention, gelu_erf, silu, forward_hidden,
                           label_logits, full_logits, Weights64)
 from .query import run_query, decide, aggregate, relational
+from .generate import position_logits, greedy_generate, generated_length, like_tokens
 
 __all__ = [
     "eval_pred", "select", "hash_join", "sequences", "pack", "group_avg_count", "count_by",
     "rmsnorm", "rope", "causal_attention", "gelu_erf", "silu", "forward_hidden",
     "label_logits", "full_logits", "Weights64", "run_query", "decide", "aggregate", "relational",
+    "position_logits", "greedy_generate", "generated_length", "like_tokens",
 ]
