@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define AIQ_ABI_VERSION 2
+#define AIQ_ABI_VERSION 3
 
 typedef enum aiq_status {
   AIQ_OK = 0,
@@ -103,6 +103,8 @@ typedef enum aiq_logits_mode { AIQ_LOGITS_LABELS = 1, AIQ_LOGITS_FULL_VOCAB = 2 
 #define AIQ_MAX_IN_SET 32
 #define AIQ_MAX_PREFIX 64
 #define AIQ_MAX_LABELS 8
+#define AIQ_MAX_GEN 512
+#define AIQ_MAX_LIKE 16
 
 /* One fixed-width column: `data` is a device array of n_rows elements,
  * 16-byte aligned (predicates read it in 16-byte vectors; a misaligned
@@ -194,6 +196,21 @@ typedef struct aiq_query {
   int32_t group_col;                   /* AVG_LABEL_COUNT_BY: probe key column (integer);
                                           SUM_F32: the summed probe column (AIQ_F32) */
   int32_t n_group_keys;                /* group keys are codes in [0, n_group_keys) */
+  /* AI_TRANSFORM (Table 1; Section 4, Q3 and Q5).  gen_tokens > 0 replaces
+     the label decision: every selected row's sequence is continued by up
+     to gen_tokens tokens, each the argmax of the last position's logits over
+     the whole vocabulary (ties to the lowest id); a row's generation stops
+     after eos_id (kept as its last token) and its later slots hold pad_id.
+     A row is kept iff its generated tokens (up to the end) contain
+     like[0..n_like) contiguously (LIKE '%pattern%' on token ids); with
+     n_like = 0 every selected row is kept.  n_labels / label_ids / decision
+     are ignored; agg AVG_LABEL_COUNT_BY is refused.  16-bit models only
+     (AIQ_EUNSUPPORTED otherwise, or when vocab % 256 != 0). */
+  int32_t gen_tokens;                  /* 0 = AI_IF classification; 1..AIQ_MAX_GEN */
+  int32_t eos_id;                      /* -1 = no end token */
+  int32_t pad_id;
+  int32_t n_like;                      /* 0..AIQ_MAX_LIKE */
+  int32_t like[AIQ_MAX_LIKE];
 } aiq_query;
 
 typedef struct aiq_plan_opts {
@@ -243,8 +260,10 @@ typedef struct aiq_out {
   int64_t ids_cap;
   int32_t* sel_ids;          /* optional: selected row ids (ascending), cap sel_cap */
   int32_t* sel_labels;       /* optional: label value per selected row (binary 1/0,
-                                argmax: the winning label token id) */
-  float* sel_logits;         /* optional: [sel_cap, n_labels] label logits */
+                                argmax: the winning label token id; AI_TRANSFORM:
+                                1 if the row's generation matches the LIKE pattern) */
+  float* sel_logits;         /* optional: [sel_cap, n_labels] label logits (not
+                                written by AI_TRANSFORM queries) */
   int64_t sel_cap;
   int32_t* grp_key;          /* groups in ascending key order, capacity grp_cap */
   int64_t* grp_count;
@@ -255,6 +274,9 @@ typedef struct aiq_out {
      selected rows alone, so repeated runs give the same bits.  Its distance
      to the exactly rounded sum is at most 2^-52 * (n_kept + 64) * sum|v|. */
   double* sum_out;
+  /* optional, AI_TRANSFORM: [sel_cap, gen_tokens] generated tokens of each
+     selected row (same order as sel_ids), pad_id after a row's end */
+  int32_t* sel_gen;
 } aiq_out;
 
 /*
@@ -285,7 +307,8 @@ enum {
   AIQ_K_GEMM_UP = 7,    /* gate/up (SwiGLU) or W1 (GELU) */
   AIQ_K_GEMM_DOWN = 8,
   AIQ_K_HEAD = 9,
-  AIQ_K_AGG = 10
+  AIQ_K_AGG = 10,
+  AIQ_K_DECODE = 11     /* AI_TRANSFORM: every kernel of a generation step, the LIKE match */
 };
 
 typedef struct aiq_plan aiq_plan;

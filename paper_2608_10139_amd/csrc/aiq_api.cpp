@@ -25,6 +25,8 @@ struct aiq_plan {
   // the prompt prefix is prefilled once per run and its keys / values are
   // shared by every row (16-bit models, unless AIQ_PLAN_UNSHARED_PREFIX)
   bool share_prefix = false;
+  int32_t gen = 0;        // AI_TRANSFORM: tokens generated per selected row (0: AI_IF)
+  int32_t gen_blocks = 0; // row blocks of the full-vocabulary head
   aiq_table probe{}, build{};
   std::vector<aiq_col> probe_cols, build_cols;
   aiq_query q{};
@@ -143,7 +145,7 @@ aiq_status validate_model(const aiq_model* m) {
 struct Layout {
   size_t ctr, mask, blk_cnt, blk_off, sel, payload, lens, label, logits, cu, blk_tok, tok_off, packed, hkeys, hvals,
       bins, desc, rcos, rsin, rrev, x, delta, h, qkv, att, ffn, pos, hf, ssp, rs, pkv, ptok, pcu, pdesc, pxlast,
-      total;
+      kvc, gkv, glog, gtok, gdone, gen, gdesc, gcnt, total;
 };
 
 size_t act_bytes(const aiq_plan* p) { return p->bf16 ? 2 : 4; }
@@ -217,6 +219,18 @@ Layout run_layout(const aiq_plan* p) {
     L.pdesc = c.take(D_STRIDE * 8);
     L.pxlast = c.take(static_cast<size_t>(d) * 4);
   }
+  if (p->gen > 0) {   // AI_TRANSFORM: kept prompt keys / values, generated-token cache, head, tokens
+    const size_t G = static_cast<size_t>(p->gen), su = static_cast<size_t>(p->seq_ub);
+    L.kvc = c.take(static_cast<size_t>(p->n_layers) * p->t_cap * p->n_qkv * ab);
+    L.gkv = c.take(static_cast<size_t>(p->n_layers) * su * G * 2 * p->d_kv * ab);
+    L.hf = c.take(su * d * ab);
+    L.glog = c.take(std::min<size_t>(su, GEN_HEAD_ROWS) * p->model.vocab * 4);
+    L.gtok = c.take(su * 4);
+    L.gdone = c.take(su * 4);
+    L.gen = c.take(static_cast<size_t>(n + 1) * G * 4);
+    L.gdesc = c.take(D_STRIDE * 8);
+    L.gcnt = c.take(static_cast<size_t>(p->gen_blocks) * 8);
+  }
   L.total = c.off;
   return L;
 }
@@ -280,12 +294,15 @@ struct Tracer {
     (tr).end();                \
   } while (0)
 
-// Shared-prefix options of a chunk pass.  The prefix's own pass stores each
+// Options of a chunk pass.  Shared prefix: the prefix's own pass stores each
 // layer's q|k|v rows in qkv_layers (npre rows per layer) and runs no head;
 // the row passes read them back (pkv_layers), number positions from npre and
 // give rows without own tokens the prefix's final state (x_pre).
+// AI_TRANSFORM: the row passes keep every layer's q|k|v rows in qkv_layers
+// (qkv_rows rows per layer) for the generation steps.
 struct PrefixUse {
   void* qkv_layers = nullptr;
+  int64_t qkv_rows = 0;
   const void* pkv_layers = nullptr;
   int32_t npre = 0;
   const float* x_pre = nullptr;
@@ -359,10 +376,11 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
     TRACED(tr, AIQ_K_EMBED, launch_embed_norm(desc, cu, packed, m.emb, m.wdtype, d, m.vocab, x, pos, ctr, g0, eps,
                                               h, p->act, rs, t_cap, s, pos_base));
     const size_t pre_layer = static_cast<size_t>(pu.npre) * p->n_qkv * act_bytes(p);   // bytes per layer
+    const size_t keep_layer = static_cast<size_t>(pu.qkv_rows) * p->n_qkv * act_bytes(p);
     for (int l = 0; l < p->n_layers; ++l) {
       const aiq_layer& W = p->layers[l];
       const bool last = l + 1 == p->n_layers;
-      void* qkv_l = pu.qkv_layers ? static_cast<char*>(pu.qkv_layers) + l * pre_layer : qkv;
+      void* qkv_l = pu.qkv_layers ? static_cast<char*>(pu.qkv_layers) + l * keep_layer : qkv;
       TRACED(tr, AIQ_K_GEMM_QKV, gemm(EPI_QKV_ROPE, h, d, p->n_qkv, d, W.wq, W.wk, W.wv, qkv_l, p->n_qkv));
       AttnArgs aa{};
       aa.qkv = qkv_l;
@@ -432,7 +450,7 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
   ha.d = d;
   ha.lm_head = m.lm_head;
   ha.wdtype = m.wdtype;
-  ha.n_labels = p->has_query ? p->q.n_labels : 0;
+  ha.n_labels = (p->has_query && p->gen == 0) ? p->q.n_labels : 0;
   for (int k = 0; k < ha.n_labels; ++k) ha.labels[k] = p->q.label_ids[k];
   ha.decision = p->has_query ? p->q.decision : AIQ_DECIDE_BINARY_GT;
   ha.label_out = ha.n_labels >= 2 ? label_out : nullptr;
@@ -442,6 +460,129 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
   ha.seq_ub = seq_ub;
   ha.x_pre = pu.x_pre;
   TRACED(tr, AIQ_K_HEAD, launch_head(ha, s));
+  return AIQ_OK;
+}
+
+// AI_TRANSFORM for the sequences of one chunk, after its prefill pass (which
+// kept every layer's q|k|v rows and wrote each sequence's normalised last
+// row to hf): the first token from hf, then gen - 1 steps of one row per
+// sequence through the layer stack and the full-vocabulary head.
+aiq_status enqueue_generation(const aiq_plan* p, void* ws, const Layout& L, const int64_t* cdesc, const int64_t* cu,
+                              const PrefixUse& pu, Tracer& tr, hipStream_t s) {
+  const aiq_model& m = p->model;
+  const aiq_query& q = p->q;
+  const int d = m.d_model, G = p->gen;
+  const size_t ab = act_bytes(p);
+  const int64_t su = p->seq_ub;
+  int64_t* gd = at<int64_t>(ws, L.gdesc);
+  int64_t* cnt = at<int64_t>(ws, L.gcnt);
+  int32_t* tok = at<int32_t>(ws, L.gtok);
+  int32_t* done = at<int32_t>(ws, L.gdone);
+  int32_t* gen = at<int32_t>(ws, L.gen);
+  float* logits = at<float>(ws, L.glog);
+  void* hf = at<void>(ws, L.hf);
+  float* x = at<float>(ws, L.x);
+  float* ssp = at<float>(ws, L.ssp);
+  float* rs = at<float>(ws, L.rs);
+  void* h = at<void>(ws, L.h);
+  void* qkv = at<void>(ws, L.qkv);
+  void* att = at<void>(ws, L.att);
+  void* ffn = at<void>(ws, L.ffn);
+  int32_t* pos = at<int32_t>(ws, L.pos);
+  const float eps = static_cast<float>(m.norm_eps);
+  const int32_t npre = pu.pkv_layers ? pu.npre : 0;
+  TRACED(tr, AIQ_K_DECODE, launch_gen_desc(cdesc, gd, cnt, p->gen_blocks, s));
+  TRACED(tr, AIQ_K_DECODE, launch_fill_i32(done, su, 0, s));
+  auto gemm = [&](int epi, const void* A, int64_t lda, const int64_t* m_ptr, int64_t m_ub, int N, int K,
+                  const void* B0, const void* B1, const void* B2, void* C, int64_t ldc, const float* gnext,
+                  bool resid) {
+    GemmArgs g{};
+    g.A = A;
+    g.lda = lda;
+    g.m_ptr = m_ptr;
+    g.m_ub = m_ub;
+    g.N = N;
+    g.K = K;
+    g.B0 = B0;
+    g.B1 = B1;
+    g.B2 = B2;
+    g.n_q = p->d_q;
+    g.n_kv = p->d_kv;
+    g.hd = p->hd;
+    g.C = C;
+    g.ldc = ldc;
+    g.pos = pos;
+    g.rope_rev = at<float>(ws, L.rrev);
+    g.f16 = p->act == 2;
+    g.rs = rs;
+    if (resid) {
+      g.x = x;
+      g.gnext = gnext;
+      g.hout = h;
+      g.ssp = ssp;
+      g.n_part = d / 64;
+    }
+    return launch_gemm_bf16(epi, g, s);
+  };
+  // full-vocabulary head over hf in row blocks, argmax into generated slot `step`
+  auto next_tokens = [&](int step) -> aiq_status {
+    for (int b = 0; b < p->gen_blocks; ++b) {
+      const int64_t row0 = static_cast<int64_t>(b) * GEN_HEAD_ROWS;
+      TRACED(tr, AIQ_K_DECODE, gemm(EPI_STORE_F32, static_cast<const char*>(hf) + row0 * d * ab, d, cnt + b,
+                                    std::min<int64_t>(su - row0, GEN_HEAD_ROWS), m.vocab, d, m.lm_head, nullptr,
+                                    nullptr, logits, m.vocab, nullptr, false));
+      TRACED(tr, AIQ_K_DECODE, launch_gen_argmax(logits, m.vocab, cnt + b, row0, gd, step, G, q.eos_id, q.pad_id,
+                                                 tok, done, gen, s));
+    }
+    return AIQ_OK;
+  };
+  aiq_status e = next_tokens(0);
+  if (e != AIQ_OK) return e;
+  const int64_t* n_rows = gd + D_NTOK;
+  const size_t kv_layer = static_cast<size_t>(pu.qkv_rows) * p->n_qkv * ab;
+  const size_t pre_layer = static_cast<size_t>(npre) * p->n_qkv * ab;
+  const size_t gkv_layer = static_cast<size_t>(su) * G * 2 * p->d_kv * ab;
+  const float* g0 = p->n_layers > 0 ? p->layers[0].attn_norm : m.final_norm;
+  for (int k = 0; k + 1 < G; ++k) {
+    TRACED(tr, AIQ_K_DECODE, launch_gen_embed(gd, cu, tok, k, npre, m.emb, m.wdtype, d, m.vocab, x, pos, g0, eps, h,
+                                              p->act, rs, su, s));
+    for (int l = 0; l < p->n_layers; ++l) {
+      const aiq_layer& W = p->layers[l];
+      const bool last = l + 1 == p->n_layers;
+      TRACED(tr, AIQ_K_DECODE, gemm(EPI_QKV_ROPE, h, d, n_rows, su, p->n_qkv, d, W.wq, W.wk, W.wv, qkv, p->n_qkv,
+                                    nullptr, false));
+      GenAttnArgs ga{};
+      ga.qkv = qkv;
+      ga.kvc = static_cast<const char*>(pu.qkv_layers) + l * kv_layer;
+      ga.pkv = npre ? static_cast<const char*>(pu.pkv_layers) + l * pre_layer : nullptr;
+      ga.npre = npre;
+      ga.gkv = at<char>(ws, L.gkv) + l * gkv_layer;
+      ga.step = k;
+      ga.gen = G;
+      ga.ld = p->n_qkv;
+      ga.gen_desc = gd;
+      ga.chunk_desc = cdesc;
+      ga.cu = cu;
+      ga.out = att;
+      ga.n_heads = m.n_heads;
+      ga.n_kv = m.n_kv_heads;
+      ga.hd = p->hd;
+      ga.out_act = p->act;
+      ga.seq_ub = su;
+      TRACED(tr, AIQ_K_DECODE, launch_attention_gen(ga, s));
+      TRACED(tr, AIQ_K_DECODE, gemm(EPI_RESID, att, p->d_q, n_rows, su, d, p->d_q, W.wo, nullptr, nullptr, nullptr,
+                                    d, W.ffn_norm, true));
+      TRACED(tr, AIQ_K_DECODE, launch_row_scale(gd, ssp, d / 64, d, eps, rs, su, s));
+      TRACED(tr, AIQ_K_DECODE, gemm(EPI_SWIGLU, h, d, n_rows, su, 2 * m.d_ff, d, W.w_gate, W.w_up, nullptr, ffn,
+                                    m.d_ff, nullptr, false));
+      TRACED(tr, AIQ_K_DECODE, gemm(EPI_RESID, ffn, m.d_ff, n_rows, su, d, m.d_ff, W.w_down, nullptr, nullptr,
+                                    nullptr, d, last ? nullptr : p->layers[l + 1].attn_norm, true));
+      if (!last) TRACED(tr, AIQ_K_DECODE, launch_row_scale(gd, ssp, d / 64, d, eps, rs, su, s));
+    }
+    TRACED(tr, AIQ_K_DECODE, launch_norm_rows(gd, x, m.final_norm, d, eps, hf, p->act, su, s));
+    e = next_tokens(k + 1);
+    if (e != AIQ_OK) return e;
+  }
   return AIQ_OK;
 }
 
@@ -494,10 +635,20 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
     p->has_query = true;
     p->q = *query;
     const aiq_query& q = p->q;
-    if (q.n_labels < 2 || q.n_labels > AIQ_MAX_LABELS) return fail(AIQ_EINVAL);
-    for (int k = 0; k < q.n_labels; ++k)
-      if (q.label_ids[k] < 0 || q.label_ids[k] >= model->vocab) return fail(AIQ_EINVAL);
-    if (q.decision != AIQ_DECIDE_BINARY_GT && q.decision != AIQ_DECIDE_ARGMAX) return fail(AIQ_EINVAL);
+    if (q.gen_tokens < 0 || q.gen_tokens > AIQ_MAX_GEN) return fail(AIQ_EINVAL);
+    p->gen = q.gen_tokens;
+    if (p->gen > 0) {   // AI_TRANSFORM: generation replaces the label decision
+      if (!p->bf16 || model->vocab % 256 || model->n_heads / model->n_kv_heads > 8) return fail(AIQ_EUNSUPPORTED);
+      if (q.eos_id < -1 || q.eos_id >= model->vocab) return fail(AIQ_EINVAL);
+      if (q.n_like < 0 || q.n_like > AIQ_MAX_LIKE) return fail(AIQ_EINVAL);
+      for (int k = 0; k < q.n_like; ++k)
+        if (q.like[k] < 0 || q.like[k] >= model->vocab) return fail(AIQ_EINVAL);
+    } else {
+      if (q.n_labels < 2 || q.n_labels > AIQ_MAX_LABELS) return fail(AIQ_EINVAL);
+      for (int k = 0; k < q.n_labels; ++k)
+        if (q.label_ids[k] < 0 || q.label_ids[k] >= model->vocab) return fail(AIQ_EINVAL);
+      if (q.decision != AIQ_DECIDE_BINARY_GT && q.decision != AIQ_DECIDE_ARGMAX) return fail(AIQ_EINVAL);
+    }
     if (q.n_prefix < 0 || q.n_prefix > AIQ_MAX_PREFIX) return fail(AIQ_EINVAL);
     for (int k = 0; k < q.n_prefix; ++k)
       if (q.prefix[k] < 0 || q.prefix[k] >= model->vocab) return fail(AIQ_EINVAL);
@@ -536,6 +687,7 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
     switch (q.agg) {
       case AIQ_AGG_COUNT: break;
       case AIQ_AGG_AVG_LABEL_COUNT_BY:
+        if (p->gen > 0) return fail(AIQ_EINVAL);   // no label to average
         if (q.group_col < 0 || q.group_col >= static_cast<int>(p->probe_cols.size())) return fail(AIQ_EINVAL);
         if (!int_dtype(p->probe_cols[q.group_col].dtype)) return fail(AIQ_EUNSUPPORTED);
         if (q.n_group_keys <= 0) return fail(AIQ_EINVAL);
@@ -559,17 +711,27 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
     const int64_t max_packed = p->share_prefix ? std::max<int64_t>(p->probe.max_list_len, q.n_prefix) : p->max_seq;
     // default chunk: about 48 GB of per-token activations (a fraction of one
     // MI355X's 288 GB), at most 4M tokens
+    // (+ every layer's kept q|k|v rows when the rows go on to generate)
     const int64_t per_tok = static_cast<int64_t>(resid_bytes(p)) +
                             static_cast<int64_t>(model->d_model + p->n_qkv + p->d_q + model->d_ff) *
-                                (p->bf16 ? 2 : 4) + 4;
+                                (p->bf16 ? 2 : 4) + 4 +
+                            (p->gen > 0 ? static_cast<int64_t>(p->n_layers) * p->n_qkv * 2 : 0);
     const int64_t def_chunk = std::min<int64_t>((int64_t(48) << 30) / per_tok, int64_t(4) << 20);
     int64_t ct = (opts && opts->chunk_tokens > 0) ? opts->chunk_tokens : def_chunk;
     ct = std::max<int64_t>(ct, max_packed);
     ct = std::min<int64_t>(ct, std::max<int64_t>(p->t_ub, max_packed));
     p->chunk_tokens = ct;
-    p->n_chunks = std::max<int64_t>((p->t_ub + ct - 1) / ct, 1);
     p->t_cap = ct + max_packed;
-    p->seq_ub = std::min<int64_t>(p->n_rows, p->t_cap);
+    if (p->gen > 0) {
+      // generation keeps per-sequence state: chunks are cut so that each holds
+      // at most ct sequences as well (a sequence counts one unit besides its tokens)
+      p->n_chunks = std::max<int64_t>((p->t_ub + p->n_rows + ct - 1) / ct, 1);
+      p->seq_ub = std::min<int64_t>(p->n_rows, ct);
+    } else {
+      p->n_chunks = std::max<int64_t>((p->t_ub + ct - 1) / ct, 1);
+      p->seq_ub = std::min<int64_t>(p->n_rows, p->t_cap);
+    }
+    p->gen_blocks = p->gen > 0 ? static_cast<int32_t>((p->seq_ub + GEN_HEAD_ROWS - 1) / GEN_HEAD_ROWS) : 0;
     p->prefix.n = q.n_prefix;
     for (int k = 0; k < q.n_prefix; ++k) p->prefix.tok[k] = q.prefix[k];
   }
@@ -682,7 +844,7 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
   if (!p->share_prefix) row_prefix = p->prefix;
   HIP_TRY(launch_gather_tokens(sel, ctr + C_SEL, n, p->probe.list_offsets, p->probe.list_tokens, cu, row_prefix,
                                p->model.vocab, p->t_ub, packed, ctr, s));
-  HIP_TRY(launch_chunk_desc(cu, ctr + C_SEL, p->chunk_tokens, p->n_chunks, p->t_ub, desc, s));
+  HIP_TRY(launch_chunk_desc(cu, ctr + C_SEL, p->chunk_tokens, p->n_chunks, p->t_ub, desc, s, p->gen > 0 ? 1 : 0));
   HIP_TRY(launch_rope_table(p->max_seq, p->hd / 2, p->model.rope_theta, p->hd, at<float>(ws, L.rcos),
                             at<float>(ws, L.rsin), at<float>(ws, L.rrev), s));
   tr.end();
@@ -696,6 +858,7 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
     HIP_TRY(launch_prefix_batch(p->prefix, ptok, pcu, pdesc, s));
     PrefixUse pre_pu{};
     pre_pu.qkv_layers = at<void>(ws, L.pkv);
+    pre_pu.qkv_rows = np;
     pre_pu.npre = np;
     pre_pu.head = false;
     const aiq_status e = enqueue_chunk(p, ws, L, pdesc, pcu, ctr, ptok, p->t_cap, 1, nullptr, nullptr, nullptr, tr,
@@ -708,15 +871,31 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
     rows_pu.npre = np;
     rows_pu.x_pre = pxl;
   }
-  // ---- prefill + label head, chunk by chunk
+  if (p->gen > 0) {   // the generation steps read every layer's prompt keys and values
+    rows_pu.qkv_layers = at<void>(ws, L.kvc);
+    rows_pu.qkv_rows = p->t_cap;
+  }
+  // ---- prefill + label head (or generation), chunk by chunk
   for (int64_t c = 0; c < p->n_chunks; ++c) {
-    const aiq_status e = enqueue_chunk(p, ws, L, desc + c * D_STRIDE, cu, ctr, packed, p->t_cap, p->seq_ub, label,
-                                       logits, nullptr, tr, s, rows_pu);
+    aiq_status e = enqueue_chunk(p, ws, L, desc + c * D_STRIDE, cu, ctr, packed, p->t_cap, p->seq_ub, label, logits,
+                                 p->gen > 0 ? at<void>(ws, L.hf) : nullptr, tr, s, rows_pu);
     if (e != AIQ_OK) return e;
+    if (p->gen > 0) {
+      e = enqueue_generation(p, ws, L, desc + c * D_STRIDE, cu, rows_pu, tr, s);
+      if (e != AIQ_OK) return e;
+    }
+  }
+  int32_t* gen = p->gen > 0 ? at<int32_t>(ws, L.gen) : nullptr;
+  if (p->gen > 0) {   // LIKE over each selected row's generation -> keep flags
+    LikePattern pat{};
+    pat.n = q.n_like;
+    for (int k = 0; k < q.n_like; ++k) pat.tok[k] = q.like[k];
+    TRACED(tr, AIQ_K_DECODE, launch_gen_like(gen, ctr + C_SEL, n, p->gen, q.eos_id, pat, label, s));
   }
   // ---- decision -> kept ids, aggregates
   tr.begin(AIQ_K_AGG);
-  if (q.decision == AIQ_DECIDE_BINARY_GT) {
+  const bool binary = q.decision == AIQ_DECIDE_BINARY_GT || p->gen > 0;   // label = keep flag
+  if (binary) {
     HIP_TRY(launch_label_mask(label, ctr + C_SEL, n, mask, blk_cnt, s));
     HIP_TRY(launch_scan_blocks(blk_cnt, ctr + C_SEL, n, blk_off, ctr + C_KEPT, s));
     HIP_TRY(launch_scatter_rows(mask, blk_off, ctr + C_SEL, n, sel, out->ids, out->ids_cap, nullptr, AIQ_I32, h, 0,
@@ -737,12 +916,14 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
   }
   if (q.agg == AIQ_AGG_SUM_F32)
     HIP_TRY(launch_sum_f32(sel, label, ctr + C_SEL, static_cast<const float*>(p->probe_cols[q.group_col].data),
-                           q.decision == AIQ_DECIDE_BINARY_GT, at<double>(ws, L.bins), out->sum_out, s));
+                           binary, at<double>(ws, L.bins), out->sum_out, s));
   if (out->sel_cap > 0) {
     if (out->sel_ids) HIP_TRY(launch_copy_ids(sel, ctr + C_SEL, n, out->sel_ids, out->sel_cap, ctr, 0, s));
     if (out->sel_labels) HIP_TRY(launch_copy_ids(label, ctr + C_SEL, n, out->sel_labels, out->sel_cap, ctr, 0, s));
-    if (out->sel_logits)
+    if (out->sel_logits && p->gen == 0)
       HIP_TRY(launch_copy_f32(logits, ctr + C_SEL, n, q.n_labels, out->sel_logits, out->sel_cap, s));
+    if (out->sel_gen && p->gen > 0)
+      HIP_TRY(launch_copy_rows_i32(gen, ctr + C_SEL, n, p->gen, out->sel_gen, out->sel_cap, s));
   }
   HIP_TRY(launch_finalize(ctr, out->scalars, s, p->share_prefix ? q.n_prefix : 0));
   tr.end();

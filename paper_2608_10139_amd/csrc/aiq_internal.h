@@ -129,8 +129,10 @@ hipError_t launch_gather_tokens(const int32_t* sel, const int64_t* n_ptr, int64_
                                 const int64_t* offsets, const int32_t* tokens, const int64_t* cu,
                                 const Prefix& prefix, int32_t vocab, int64_t t_ub, int32_t* packed,
                                 int64_t* ctr, hipStream_t s);
+// Chunk c: the sequences i with cu[i] + per_seq * i in [c, c + 1) * chunk_tokens
+// (per_seq = 1 also caps the sequences per chunk at chunk_tokens).
 hipError_t launch_chunk_desc(const int64_t* cu, const int64_t* n_ptr, int64_t chunk_tokens,
-                             int64_t n_chunks, int64_t t_ub, int64_t* desc, hipStream_t s);
+                             int64_t n_chunks, int64_t t_ub, int64_t* desc, hipStream_t s, int32_t per_seq = 0);
 hipError_t launch_packed_desc(const int32_t* cu32, int32_t n_seq, int64_t n_tok, int64_t* cu64,
                               int64_t* desc, int64_t* ctr, hipStream_t s);
 // The shared prompt prefix as a one-sequence batch: tok[0..n) = prefix,
@@ -238,5 +240,58 @@ struct HeadArgs {
                              // sequences with no own token (null: such sequences get 0 logits)
 };
 hipError_t launch_head(const HeadArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- AI_TRANSFORM generation
+// A generation step works on one row per sequence of the chunk: its
+// descriptor (D_TOK_BEGIN 0, D_NTOK = D_NSEQ = the chunk's sequences,
+// D_SEQ_BEGIN = the chunk's first sequence) comes from the chunk's.  The
+// full-vocabulary head runs in blocks of GEN_HEAD_ROWS rows; cnt[b] = rows
+// of block b.
+constexpr int GEN_HEAD_ROWS = 4096;
+hipError_t launch_gen_desc(const int64_t* chunk_desc, int64_t* gen_desc, int64_t* cnt, int32_t n_blocks,
+                           hipStream_t s);
+// Embedding of each sequence's current token at position (its prompt
+// length incl. a shared prefix of npre tokens) + step, with the first norm's
+// operand h = x * g and row scale rs (as launch_embed_norm).
+hipError_t launch_gen_embed(const int64_t* gen_desc, const int64_t* cu, const int32_t* tok, int32_t step,
+                            int32_t npre, const void* emb, int32_t wdtype, int32_t d, int32_t vocab, float* x,
+                            int32_t* pos, const float* g, float eps, void* h, int32_t h_act, float* rs,
+                            int64_t seq_ub, hipStream_t s);
+struct GenAttnArgs {
+  const void* qkv;           // [n, ld] this step's q|k|v, one row per sequence
+  const void* kvc;           // the chunk's prompt rows for this layer, [chunk tokens, ld] q|k|v
+  const void* pkv;           // shared prefix rows for this layer [npre, ld], or null
+  int32_t npre;
+  void* gkv;                 // generated keys/values [seq_ub][gen][2 d_kv]; slot `step` is written
+  int32_t step, gen;
+  int64_t ld;
+  const int64_t* gen_desc;
+  const int64_t* chunk_desc; // for the chunk's first token
+  const int64_t* cu;
+  void* out;                 // [n, n_heads * hd]
+  int32_t n_heads, n_kv, hd, out_act;
+  int64_t seq_ub;
+};
+hipError_t launch_attention_gen(const GenAttnArgs& a, hipStream_t s);
+// hf[i] = x[i] / rms * g in 16 bits, i < gen_desc[D_NSEQ]
+hipError_t launch_norm_rows(const int64_t* gen_desc, const float* x, const float* g, int32_t d, float eps, void* hf,
+                            int32_t act, int64_t seq_ub, hipStream_t s);
+// Argmax over a block of full-vocabulary logits rows (ties to the lowest id):
+// row r is sequence i = row0 + r; its token goes to gen[(seq_begin + i) * G +
+// step] (pad_id once the sequence has ended), tok[i] and done[i].
+hipError_t launch_gen_argmax(const float* logits, int32_t vocab, const int64_t* cnt, int64_t row0,
+                             const int64_t* gen_desc, int32_t step, int32_t G, int32_t eos, int32_t pad,
+                             int32_t* tok, int32_t* done, int32_t* gen, hipStream_t s);
+struct LikePattern {
+  int32_t n;
+  int32_t tok[AIQ_MAX_LIKE];
+};
+// label[i] = 1 iff the generated tokens of selected row i (up to its end
+// token) contain the pattern contiguously (every row for an empty pattern).
+hipError_t launch_gen_like(const int32_t* gen, const int64_t* n_ptr, int64_t n_ub, int32_t G, int32_t eos,
+                           const LikePattern& pat, int32_t* label, hipStream_t s);
+// dst[i * per_row ..] = src[i * per_row ..] for i < min(*n_ptr, cap_rows)
+hipError_t launch_copy_rows_i32(const int32_t* src, const int64_t* n_ptr, int64_t n_ub, int32_t per_row,
+                                int32_t* dst, int64_t cap_rows, hipStream_t s);
 
 }  // namespace aiq

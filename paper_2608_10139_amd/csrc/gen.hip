@@ -1,0 +1,423 @@
+// AI_TRANSFORM: greedy generation after the prefill (Table 1 maps it to a
+// causal-LM forward with generative decoding, output masked with a pad id;
+// Section 4, Q3 and Q5), and the LIKE match over the generated tokens.
+//
+// A generation step runs one row per sequence of the chunk through the same
+// projections as the prefill (M = number of sequences), a decode attention
+// kernel over the sequence's kept keys and values, and the full-vocabulary
+// head as a GEMM into fp32 logits followed by a row argmax.  Keys and values
+// of the prompt stay where the prefill put them (the chunk's per-layer q|k|v
+// rows, plus the shared prefix's rows); those of generated tokens go to a
+// per-layer cache [sequence][step][2 d_kv].  Everything runs on the launch
+// stream; counts come from device memory.
+#include "aiq_internal.h"
+#include "dev_util.h"
+
+namespace aiq {
+
+static int grid_for(int64_t n, int per_block, int cap) {
+  int64_t g = (n + per_block - 1) / per_block;
+  if (g < 1) g = 1;
+  if (g > cap) g = cap;
+  return static_cast<int>(g);
+}
+
+__device__ __forceinline__ float wave_sum_g(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ float wave_max_g(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+// ------------------------------------------------------------------ descriptors
+__global__ void k_gen_desc(const int64_t* cd, int64_t* gd, int64_t* cnt, int32_t nb) {
+  const int64_t n = cd[D_NSEQ];
+  if (threadIdx.x == 0) {
+    gd[D_TOK_BEGIN] = 0;
+    gd[D_NTOK] = n;
+    gd[D_SEQ_BEGIN] = cd[D_SEQ_BEGIN];
+    gd[D_NSEQ] = n;
+  }
+  for (int b = threadIdx.x; b < nb; b += blockDim.x) {
+    const int64_t r = n - static_cast<int64_t>(b) * GEN_HEAD_ROWS;
+    cnt[b] = r < 0 ? 0 : (r > GEN_HEAD_ROWS ? GEN_HEAD_ROWS : r);
+  }
+}
+
+hipError_t launch_gen_desc(const int64_t* chunk_desc, int64_t* gen_desc, int64_t* cnt, int32_t n_blocks,
+                           hipStream_t s) {
+  hipLaunchKernelGGL(k_gen_desc, dim3(1), dim3(256), 0, s, chunk_desc, gen_desc, cnt, n_blocks);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ embedding of the current tokens
+// Wave per sequence: x = E[tok], h = x * g (16-bit), rs = 1 / rms(x), and the
+// position after the prompt (shared prefix included) and the earlier steps.
+__global__ __launch_bounds__(256) void k_gen_embed(const int64_t* gd, const int64_t* cu, const int32_t* tok,
+                                                   int32_t step, int32_t npre, const uint16_t* emb, int32_t ea,
+                                                   int32_t d, int32_t vocab, float* x, int32_t* pos, const float* g,
+                                                   float eps, uint16_t* h, int32_t h_act, float* rs) {
+  const int64_t n = gd[D_NSEQ], sb = gd[D_SEQ_BEGIN];
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6;
+  const int64_t n_waves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t i = wave; i < n; i += n_waves) {
+    int32_t t = tok[i];
+    if (t < 0 || t >= vocab) t = 0;   // argmax ids are in range; keeps the gather in bounds regardless
+    if (lane == 0) pos[i] = npre + static_cast<int32_t>(cu[sb + i + 1] - cu[sb + i]) + step;
+    const uint16_t* er = emb + static_cast<int64_t>(t) * d;
+    float* xr = x + i * d;
+    float ssq = 0.f;
+    for (int c = lane * 4; c < d; c += 256) {
+      const uint2 v = *reinterpret_cast<const uint2*>(er + c);
+      float4 o;
+      o.x = act2f(static_cast<uint16_t>(v.x & 0xFFFFu), ea);
+      o.y = act2f(static_cast<uint16_t>(v.x >> 16), ea);
+      o.z = act2f(static_cast<uint16_t>(v.y & 0xFFFFu), ea);
+      o.w = act2f(static_cast<uint16_t>(v.y >> 16), ea);
+      *reinterpret_cast<float4*>(xr + c) = o;
+      const float4 gv = *reinterpret_cast<const float4*>(g + c);
+      uint2 hv;
+      hv.x = f2act(o.x * gv.x, h_act) | (static_cast<uint32_t>(f2act(o.y * gv.y, h_act)) << 16);
+      hv.y = f2act(o.z * gv.z, h_act) | (static_cast<uint32_t>(f2act(o.w * gv.w, h_act)) << 16);
+      *reinterpret_cast<uint2*>(h + i * d + c) = hv;
+      ssq += (o.x * o.x + o.y * o.y) + (o.z * o.z + o.w * o.w);
+    }
+    ssq = wave_sum_g(ssq);
+    if (lane == 0) rs[i] = 1.0f / sqrtf(ssq / static_cast<float>(d) + eps);
+  }
+}
+
+hipError_t launch_gen_embed(const int64_t* gen_desc, const int64_t* cu, const int32_t* tok, int32_t step,
+                            int32_t npre, const void* emb, int32_t wdtype, int32_t d, int32_t vocab, float* x,
+                            int32_t* pos, const float* g, float eps, void* h, int32_t h_act, float* rs,
+                            int64_t seq_ub, hipStream_t s) {
+  if ((wdtype != AIQ_BF16 && wdtype != AIQ_F16) || h_act == ACT_F32 || d % 4) return hipErrorInvalidValue;
+  const int ea = wdtype == AIQ_F16 ? ACT_F16 : ACT_BF16;
+  hipLaunchKernelGGL(k_gen_embed, dim3(grid_for(seq_ub, 4, 8192)), dim3(256), 0, s, gen_desc, cu, tok, step, npre,
+                     static_cast<const uint16_t*>(emb), ea, d, vocab, x, pos, g, eps, static_cast<uint16_t*>(h),
+                     h_act, rs);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ decode attention
+// Workgroup per (sequence, K/V head): the rep = n_heads / n_kv query heads of
+// the group against every kept key of the sequence (prompt, earlier
+// generated tokens, this token).  Wave w takes the 64-key blocks w, w + 4,
+// ...: lane j scores key j against the group's queries (held in LDS, scaled
+// by log2(e) / sqrt(hd)), an online softmax runs per head, and for P V the
+// lanes switch to value dimensions, reading one value row per key (a
+// coalesced row read) with the key's probability broadcast by readlane.  The
+// four waves' partial states are merged through LDS.  The workgroup also
+// stores this step's key and value into the generated cache.
+template <int HD>
+__global__ __launch_bounds__(256) void k_attn_gen(GenAttnArgs a) {
+  constexpr int DPL = HD / 64;   // value dimensions per lane
+  constexpr int RMAX = 8;        // query heads per K/V head (checked by the launcher)
+  __shared__ float qs[RMAX][HD];
+  __shared__ float mw[4][RMAX], lw[4][RMAX];
+  __shared__ float ow[4][RMAX][HD];
+  const int64_t n = a.gen_desc[D_NSEQ], sb = a.gen_desc[D_SEQ_BEGIN], tb = a.chunk_desc[D_TOK_BEGIN];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int rep = a.n_heads / a.n_kv;
+  const int d_q = a.n_heads * HD, d_kv = a.n_kv * HD;
+  const float scale = 1.4426950408889634f / sqrtf(static_cast<float>(HD));
+  const uint16_t* qkv = static_cast<const uint16_t*>(a.qkv);
+  const uint16_t* kvc = static_cast<const uint16_t*>(a.kvc);
+  const uint16_t* pkv = static_cast<const uint16_t*>(a.pkv);
+  uint16_t* gkv = static_cast<uint16_t*>(a.gkv);
+  uint16_t* out = static_cast<uint16_t*>(a.out);
+  const int64_t ld = a.ld;
+  const int64_t items = n * a.n_kv;
+
+  for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
+    const int64_t i = item / a.n_kv;
+    const int kvh = static_cast<int>(item % a.n_kv);
+    const int64_t s0 = a.cu[sb + i] - tb;
+    const int P = a.npre + static_cast<int>(a.cu[sb + i + 1] - a.cu[sb + i]);   // prompt positions
+    const int N = P + a.step + 1;   // keys: the prompt, the earlier generated tokens, this token
+    const uint16_t* qrow = qkv + i * ld;
+    const int kc = d_q + kvh * HD, vc = d_q + d_kv + kvh * HD;   // key / value columns of a q|k|v row
+    uint16_t* gslot = gkv + (i * a.gen + a.step) * (2 * d_kv);
+    for (int e = t; e < 2 * HD; e += 256)
+      gslot[e < HD ? kvh * HD + e : d_kv + kvh * HD + (e - HD)] = qrow[e < HD ? kc + e : vc + (e - HD)];
+    for (int e = t; e < rep * HD; e += 256) qs[e / HD][e % HD] = h2f(qrow[(kvh * rep + e / HD) * HD + e % HD]) * scale;
+    __syncthreads();
+
+    // key j's key and value rows
+    auto kv_of = [&](int j, const uint16_t*& kp, const uint16_t*& vp) {
+      if (j < a.npre) {
+        kp = pkv + static_cast<int64_t>(j) * ld + kc;
+        vp = pkv + static_cast<int64_t>(j) * ld + vc;
+      } else if (j < P) {
+        const uint16_t* row = kvc + (s0 + j - a.npre) * ld;
+        kp = row + kc;
+        vp = row + vc;
+      } else if (j < P + a.step) {
+        const uint16_t* row = gkv + (i * a.gen + (j - P)) * (2 * d_kv);
+        kp = row + kvh * HD;
+        vp = row + d_kv + kvh * HD;
+      } else {
+        kp = qrow + kc;
+        vp = qrow + vc;
+      }
+    };
+
+    float m[RMAX], l[RMAX], o[RMAX][DPL];
+#pragma unroll
+    for (int r = 0; r < RMAX; ++r) {
+      m[r] = -INFINITY;
+      l[r] = 0.f;
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) o[r][e] = 0.f;
+    }
+    for (int blk = w; blk * 64 < N; blk += 4) {
+      // the queries stay in LDS: without this the compiler hoists all rep * HD
+      // of them into registers for the whole loop and spills
+      asm volatile("" ::: "memory");
+      const int j = blk * 64 + lane;
+      const bool valid = j < N;
+      float sc[RMAX];
+#pragma unroll
+      for (int r = 0; r < RMAX; ++r) sc[r] = 0.f;
+      if (valid) {
+        const uint16_t *kp, *vp;
+        kv_of(j, kp, vp);
+#pragma unroll 2
+        for (int c = 0; c < HD; c += 8) {
+          const uint4 u = *reinterpret_cast<const uint4*>(kp + c);
+          const uint32_t uw[4] = {u.x, u.y, u.z, u.w};
+          float kf[8];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            kf[2 * e] = h2f(static_cast<uint16_t>(uw[e] & 0xFFFFu));
+            kf[2 * e + 1] = h2f(static_cast<uint16_t>(uw[e] >> 16));
+          }
+#pragma unroll
+          for (int r = 0; r < RMAX; ++r) {
+            if (r < rep) {
+#pragma unroll
+              for (int e = 0; e < 8; ++e) sc[r] = fmaf(qs[r][c + e], kf[e], sc[r]);
+            }
+          }
+        }
+      }
+      float p[RMAX];
+#pragma unroll
+      for (int r = 0; r < RMAX; ++r) {
+        p[r] = 0.f;
+        if (r < rep) {
+          const float s = valid ? sc[r] : -INFINITY;
+          const float m_new = fmaxf(m[r], wave_max_g(s));   // finite: key blk * 64 is valid
+          const float alpha = exp2f(m[r] - m_new);
+          p[r] = valid ? exp2f(s - m_new) : 0.f;
+          l[r] = l[r] * alpha + wave_sum_g(p[r]);
+#pragma unroll
+          for (int e = 0; e < DPL; ++e) o[r][e] *= alpha;
+          m[r] = m_new;
+        }
+      }
+      const int nk = (N - blk * 64) < 64 ? (N - blk * 64) : 64;
+      for (int jj = 0; jj < nk; ++jj) {
+        const uint16_t *kp, *vp;
+        kv_of(blk * 64 + jj, kp, vp);
+        float v[DPL];
+        if constexpr (DPL == 1) {
+          v[0] = h2f(vp[lane]);
+        } else {
+          const uint32_t u = *reinterpret_cast<const uint32_t*>(vp + 2 * lane);
+          v[0] = h2f(static_cast<uint16_t>(u & 0xFFFFu));
+          v[DPL - 1] = h2f(static_cast<uint16_t>(u >> 16));
+        }
+#pragma unroll
+        for (int r = 0; r < RMAX; ++r) {
+          if (r < rep) {
+            const float pj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(p[r]), jj));
+#pragma unroll
+            for (int e = 0; e < DPL; ++e) o[r][e] = fmaf(pj, v[e], o[r][e]);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < RMAX; ++r) {
+      if (r < rep) {
+        if (lane == 0) {
+          mw[w][r] = m[r];
+          lw[w][r] = l[r];
+        }
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) ow[w][r][lane * DPL + e] = o[r][e];
+      }
+    }
+    __syncthreads();
+    for (int e = t; e < rep * HD; e += 256) {
+      const int r = e / HD, dd = e % HD;
+      float M = mw[0][r];
+#pragma unroll
+      for (int u = 1; u < 4; ++u) M = fmaxf(M, mw[u][r]);
+      float O = 0.f, Ls = 0.f;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float f = exp2f(mw[u][r] - M);   // 0 for a wave that saw no key
+        O += ow[u][r][dd] * f;
+        Ls += lw[u][r] * f;
+      }
+      out[i * d_q + (kvh * rep + r) * HD + dd] = f2act(O / Ls, a.out_act);
+    }
+    __syncthreads();   // LDS reused by the next item
+  }
+}
+
+hipError_t launch_attention_gen(const GenAttnArgs& a, hipStream_t s) {
+  if (a.n_kv <= 0 || a.n_heads % a.n_kv || a.n_heads / a.n_kv > 8 || a.npre < 0 || (a.npre > 0 && !a.pkv) ||
+      a.step < 0 || a.step >= a.gen || a.out_act == ACT_F32)
+    return hipErrorInvalidValue;
+  const int g = grid_for(a.seq_ub * a.n_kv, 1, 4096);
+  if (a.hd == 64)
+    hipLaunchKernelGGL(k_attn_gen<64>, dim3(g), dim3(256), 0, s, a);
+  else if (a.hd == 128)
+    hipLaunchKernelGGL(k_attn_gen<128>, dim3(g), dim3(256), 0, s, a);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ final norm of the step rows
+__global__ __launch_bounds__(256) void k_norm_rows(const int64_t* gd, const float* x, const float* g, int32_t d,
+                                                   float eps, uint16_t* hf, int32_t act) {
+  const int64_t n = gd[D_NSEQ];
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6;
+  const int64_t n_waves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t i = wave; i < n; i += n_waves) {
+    const float* xr = x + i * d;
+    float ss = 0.f;
+    for (int c = lane; c < d; c += 64) ss += xr[c] * xr[c];
+    ss = wave_sum_g(ss);
+    const float r = 1.0f / sqrtf(ss / static_cast<float>(d) + eps);
+    for (int c = lane; c < d; c += 64) hf[i * d + c] = f2act(xr[c] * r * g[c], act);
+  }
+}
+
+hipError_t launch_norm_rows(const int64_t* gen_desc, const float* x, const float* g, int32_t d, float eps, void* hf,
+                            int32_t act, int64_t seq_ub, hipStream_t s) {
+  if (act == ACT_F32) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_norm_rows, dim3(grid_for(seq_ub, 4, 4096)), dim3(256), 0, s, gen_desc, x, g, d, eps,
+                     static_cast<uint16_t*>(hf), act);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ argmax of the next token
+__global__ __launch_bounds__(256) void k_gen_argmax(const float* logits, int32_t vocab, const int64_t* cnt,
+                                                    int64_t row0, const int64_t* gd, int32_t step, int32_t G,
+                                                    int32_t eos, int32_t pad, int32_t* tok, int32_t* done,
+                                                    int32_t* gen) {
+  const int64_t rows = *cnt, sb = gd[D_SEQ_BEGIN];
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6;
+  const int64_t n_waves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t r = wave; r < rows; r += n_waves) {
+    const float* lr = logits + r * vocab;
+    float best = -INFINITY;
+    int32_t bi = INT32_MAX;
+    for (int c = lane; c < vocab; c += 64) {   // ascending ids: strict > keeps each lane's first maximum
+      const float v = lr[c];
+      if (v > best) {
+        best = v;
+        bi = c;
+      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(best, o);
+      const int32_t oi = __shfl_xor(bi, o);
+      if (ov > best || (ov == best && oi < bi)) {
+        best = ov;
+        bi = oi;
+      }
+    }
+    if (bi == INT32_MAX) bi = 0;   // no finite maximum (every logit NaN or -inf)
+    if (lane == 0) {
+      const int64_t i = row0 + r;
+      const bool ended = done[i] != 0;
+      gen[(sb + i) * G + step] = ended ? pad : bi;
+      tok[i] = bi;
+      if (!ended && bi == eos) done[i] = 1;
+    }
+  }
+}
+
+hipError_t launch_gen_argmax(const float* logits, int32_t vocab, const int64_t* cnt, int64_t row0,
+                             const int64_t* gen_desc, int32_t step, int32_t G, int32_t eos, int32_t pad,
+                             int32_t* tok, int32_t* done, int32_t* gen, hipStream_t s) {
+  hipLaunchKernelGGL(k_gen_argmax, dim3(grid_for(GEN_HEAD_ROWS, 4, 1024)), dim3(256), 0, s, logits, vocab, cnt,
+                     row0, gen_desc, step, G, eos, pad, tok, done, gen);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ LIKE over the generated tokens
+// Wave per selected row: the generated length (through the first end token),
+// then every start position tested by one lane.
+__global__ __launch_bounds__(256) void k_gen_like(const int32_t* gen, const int64_t* n_ptr, int32_t G, int32_t eos,
+                                                  LikePattern pat, int32_t* label) {
+  const int64_t n = *n_ptr;
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6;
+  const int64_t n_waves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t i = wave; i < n; i += n_waves) {
+    const int32_t* gr = gen + i * G;
+    int glen = G;
+    if (eos >= 0) {
+      for (int c = 0; c < G; c += 64) {
+        const uint64_t b = __ballot(c + lane < G && gr[c + lane] == eos);
+        if (b) {
+          glen = c + __builtin_ctzll(b) + 1;
+          break;
+        }
+      }
+    }
+    bool hit = false;
+    if (pat.n == 0) {
+      hit = true;
+    } else {
+      for (int s = lane; s + pat.n <= glen; s += 64) {
+        bool ok = true;
+        for (int q = 0; q < pat.n && ok; ++q) ok = gr[s + q] == pat.tok[q];
+        hit = hit || ok;
+      }
+      hit = __ballot(hit) != 0;
+    }
+    if (lane == 0) label[i] = hit ? 1 : 0;
+  }
+}
+
+hipError_t launch_gen_like(const int32_t* gen, const int64_t* n_ptr, int64_t n_ub, int32_t G, int32_t eos,
+                           const LikePattern& pat, int32_t* label, hipStream_t s) {
+  if (pat.n < 0 || pat.n > AIQ_MAX_LIKE || G <= 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_gen_like, dim3(grid_for(n_ub, 4, 4096)), dim3(256), 0, s, gen, n_ptr, G, eos, pat, label);
+  return hipGetLastError();
+}
+
+__global__ void k_copy_rows_i32(const int32_t* src, const int64_t* n_ptr, int32_t per_row, int32_t* dst,
+                                int64_t cap_rows) {
+  int64_t rows = *n_ptr;
+  if (rows > cap_rows) rows = cap_rows;
+  const int64_t total = rows * per_row;
+  for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < total; j += (int64_t)gridDim.x * blockDim.x)
+    dst[j] = src[j];
+}
+
+hipError_t launch_copy_rows_i32(const int32_t* src, const int64_t* n_ptr, int64_t n_ub, int32_t per_row,
+                                int32_t* dst, int64_t cap_rows, hipStream_t s) {
+  const int64_t ub = (n_ub < cap_rows ? n_ub : cap_rows) * per_row;
+  hipLaunchKernelGGL(k_copy_rows_i32, dim3(grid_for(ub, 256, 4096)), dim3(256), 0, s, src, n_ptr, per_row, dst,
+                     cap_rows);
+  return hipGetLastError();
+}
+
+}  // namespace aiq

@@ -164,6 +164,13 @@ def make_query(query, probe: DeviceTable | None, build: DeviceTable | None, pref
     if getattr(query, "group_col", None):
         q.group_col = probe.index[query.group_col]
     q.n_group_keys = int(getattr(query, "n_group_keys", 0))
+    q.gen_tokens = int(getattr(query, "gen_tokens", 0))
+    q.eos_id = int(getattr(query, "eos_id", -1))
+    q.pad_id = int(getattr(query, "pad_id", 0))
+    like = tuple(getattr(query, "like", ()))
+    q.n_like = len(like)
+    for i, t in enumerate(like):
+        q.like[i] = int(t)
     return q
 
 
@@ -204,6 +211,8 @@ class DeviceQuery:
         self.grp_sum = torch.zeros(G, dtype=torch.int64, device=dev)
         self.grp_avg = torch.zeros(G, dtype=torch.float64, device=dev)
         self.sum_out = torch.zeros(1, dtype=torch.float64, device=dev)
+        self.gen = int(getattr(query, "gen_tokens", 0))
+        self.sel_gen = torch.zeros(max(n, 1) * max(self.gen, 1), dtype=torch.int32, device=dev)
         o = B.aiq_out()
         o.scalars, o.ids, o.ids_cap = _ptr(self.scalars), _ptr(self.ids), n
         o.sel_ids, o.sel_labels, o.sel_logits, o.sel_cap = (_ptr(self.sel_ids), _ptr(self.sel_labels),
@@ -212,6 +221,7 @@ class DeviceQuery:
                                                         _ptr(self.grp_sum), _ptr(self.grp_avg))
         o.grp_cap = G
         o.sum_out = _ptr(self.sum_out)
+        o.sel_gen = _ptr(self.sel_gen) if self.gen else None
         self.out = o
 
     def run(self, trace=None, stream=None) -> None:
@@ -231,6 +241,8 @@ class DeviceQuery:
              "logits": self.sel_logits[:n_sel * K].cpu().numpy().reshape(n_sel, K)}
         if self.query.agg == "sum_f32":
             r["sum"] = float(self.sum_out.cpu().item())
+        if self.gen:
+            r["gen"] = self.sel_gen[:n_sel * self.gen].cpu().numpy().astype(np.int64).reshape(n_sel, self.gen)
         if self.query.agg in ("avg_label_count_by", "count_by_payload"):
             r["groups"] = (self.grp_key[:n_groups].cpu().numpy().astype(np.int64),
                            self.grp_count[:n_groups].cpu().numpy(), self.grp_sum[:n_groups].cpu().numpy(),

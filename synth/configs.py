@@ -134,6 +134,10 @@ class Query:
     n_prefix: int = 0                 # prefix tokens drawn by the generator (stream 99)
     group_col: Optional[str] = None   # probe column for avg_label_count_by
     n_group_keys: int = 0             # dense key domain [0, n_group_keys)
+    gen_tokens: int = 0               # AI_TRANSFORM: tokens generated per selected row (0: AI_IF)
+    eos_id: int = -1
+    pad_id: int = 0
+    like: Tuple[int, ...] = ()        # LIKE '%pattern%' over the generated token ids
 
 
 @dataclass(frozen=True)
