@@ -134,6 +134,50 @@ def prefill_flops(spec, own: np.ndarray, n_labels: int, npre: int = 0, shared: b
     return per
 
 
+def generation_report(spec, q, tables, sel, kinds, B, ms_step) -> dict:
+    """AI_TRANSFORM: generated tokens/s over whole steps, per-step time, and
+    the decode attention's algorithmic bytes (every kept key and value row
+    read once per layer and step) against its traced time."""
+    G = int(q.gen_tokens)
+    n = len(sel)
+    P = tables["probe"]["len"][sel].astype(np.float64) + q.n_prefix   # prompt positions per row
+    d_kv = spec.n_kv_heads * spec.head_dim
+    steps = G - 1                        # the first token comes from the prefill's last position
+    # step k reads P + k earlier keys and values plus this token's, fp16
+    keys = float(np.sum(P)) * steps + n * (steps * (steps + 1) / 2.0)
+    attn_bytes = keys * 2 * d_kv * 2 * spec.n_layers
+    t_attn = float(np.sum(kinds.get(B.AIQ_K_DECODE_ATTN, [0.0])))
+    t_layers = float(np.sum(kinds.get(B.AIQ_K_DECODE, [0.0])))
+    t_head = float(np.sum(kinds.get(B.AIQ_K_DECODE_HEAD, [0.0])))
+    return {"tokens_per_row": G, "generated_tokens": n * G, "generated_tokens_per_s": round(n * G / (ms_step * 1e-3), 1),
+            "ms": {"layers": round(t_layers, 3), "attention": round(t_attn, 3), "vocab_head_argmax": round(t_head, 3)},
+            "ms_per_step": round((t_layers + t_attn + t_head) / max(G, 1), 4),
+            "attention_bytes": attn_bytes,
+            "attention_gbps": round(attn_bytes / (t_attn * 1e-3) / 1e9, 1) if t_attn > 0 else None}
+
+
+def time_query(tables, model, dm, q, B, torch, steps, warmup, n_rows) -> dict:
+    """Whole-query time of one more query of the workload (same tables, model)."""
+    from paper_2608_10139_amd.device import DeviceQuery
+    dq = DeviceQuery(tables, model, q, dmodel=dm)
+    for _ in range(max(warmup, 1)):
+        dq.run()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        dq.run()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) / steps * 1e3
+    r = dq.results()
+    dq.close()
+    out = {"predicate": " and ".join(f"{p.col} {p.op} {p.k}" for p in q.preds) or "none",
+           "selected": r["n_selected"], "kept": r["count"], "status": r["status"], "ms_per_step": round(ms, 3),
+           "rows_per_s": round(n_rows / (ms * 1e-3), 1)}
+    if getattr(q, "gen_tokens", 0):
+        out["generated_tokens_per_s"] = round(r["n_selected"] * q.gen_tokens / (ms * 1e-3), 1)
+    return out
+
+
 def host_select(cols: dict, preds) -> np.ndarray:
     """Split baseline's host WHERE: numpy masks, then the ascending row ids."""
     n = len(cols["id"])
@@ -335,6 +379,9 @@ def main(argv=None) -> int:
     ap.add_argument("--cpu-rows", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-split", action="store_true")
+    ap.add_argument("--query", type=int, default=0, help="index of the workload's query to time")
+    ap.add_argument("--all-queries", action="store_true",
+                    help="also time every query of the workload (e.g. the Q3 selectivity sweep)")
     ap.add_argument("--unshared-prefix", action="store_true",
                     help="recompute the prompt prefix inside every row (default: prefilled once and shared)")
     ap.add_argument("--relational-scale", action="store_true",
@@ -381,7 +428,8 @@ def main(argv=None) -> int:
 
     torch.cuda.set_device(0)
     w = WORKLOADS[a.workload]
-    q = w.queries[0]
+    q = w.queries[a.query]
+    gen = int(getattr(q, "gen_tokens", 0))
     spec = w.model
     log(f"[bench] generating {a.workload}: {w.description}")
     tables = make_tables(w)
@@ -433,7 +481,7 @@ def main(argv=None) -> int:
     peak = PEAK_F32_TFLOPS if dm.compute == "f32" else PEAK_BF16_TFLOPS   # fp16 and bf16 MFMA peaks are equal
 
     # ---- one untimed traced step for the stage breakdown
-    ev2 = HipEvents(2 * (passes * (8 * spec.n_layers + 2) + 64))
+    ev2 = HipEvents(2 * (passes * (gen + 1) * (8 * spec.n_layers + 16) + 64))
     tr2 = make_trace(B, ev2, 0xFFFFFFFF)
     dq.run(trace=tr2)
     torch.cuda.synchronize()
@@ -444,7 +492,8 @@ def main(argv=None) -> int:
     names = {B.AIQ_K_REL: "relational", B.AIQ_K_PACK: "pack", B.AIQ_K_EMBED: "embed", B.AIQ_K_NORM: "rmsnorm",
              B.AIQ_K_GEMM_QKV: "gemm_qkv_rope", B.AIQ_K_ATTN: "attention", B.AIQ_K_GEMM_O: "gemm_o_resid",
              B.AIQ_K_GEMM_UP: "gemm_gate_up_swiglu", B.AIQ_K_GEMM_DOWN: "gemm_down_resid", B.AIQ_K_HEAD: "head",
-             B.AIQ_K_AGG: "decision_agg"}
+             B.AIQ_K_AGG: "decision_agg", B.AIQ_K_DECODE: "gen_layers", B.AIQ_K_DECODE_ATTN: "gen_attention",
+             B.AIQ_K_DECODE_HEAD: "gen_vocab_head_argmax_like"}
     stages = {names[k]: round(float(np.sum(v)), 4) for k, v in sorted(kinds.items())}
     prefill_kinds = [B.AIQ_K_EMBED, B.AIQ_K_NORM, B.AIQ_K_GEMM_QKV, B.AIQ_K_ATTN, B.AIQ_K_GEMM_O,
                      B.AIQ_K_GEMM_UP, B.AIQ_K_GEMM_DOWN, B.AIQ_K_HEAD]
@@ -488,7 +537,14 @@ def main(argv=None) -> int:
                      "launches": n_up, "avg_launch_ms": round(up_avg_ms, 5),
                      "flops_per_launch": up_flops_per_launch},
     }
-    if not a.no_relational_scale:
+    if gen:
+        result["generation"] = generation_report(spec, q, tables, sel, kinds, B, ms_step)
+        if a.all_queries:
+            result["queries"] = [time_query(tables, model, dm, qq, B, torch, a.steps, a.warmup, n_rows)
+                                 for qq in w.queries]
+        a.no_cpu_baseline = a.no_split = True   # the oracle and the split baseline classify; no generation
+        result["cpu_baseline"] = None
+    if not a.no_relational_scale and not gen:
         result["relational_scale"] = relational_scale_leg(B, torch, [1 << 26], [10, 1000], steps=5)
     if not a.no_cpu_baseline:
         log("[bench] cpu baseline (oracle on a sample)")

@@ -308,7 +308,9 @@ enum {
   AIQ_K_GEMM_DOWN = 8,
   AIQ_K_HEAD = 9,
   AIQ_K_AGG = 10,
-  AIQ_K_DECODE = 11     /* AI_TRANSFORM: every kernel of a generation step, the LIKE match */
+  AIQ_K_DECODE = 11,      /* AI_TRANSFORM generation steps: embedding, projections, norms */
+  AIQ_K_DECODE_ATTN = 12, /* ... their attention over the kept keys and values */
+  AIQ_K_DECODE_HEAD = 13  /* ... the full-vocabulary head and argmax; the LIKE match */
 };
 
 typedef struct aiq_plan aiq_plan;

@@ -32,7 +32,8 @@ AIQ_MAX_PREDS, AIQ_MAX_IN_SET, AIQ_MAX_PREFIX, AIQ_MAX_LABELS = 8, 32, 64, 8
 AIQ_MAX_GEN, AIQ_MAX_LIKE = 512, 16
 
 (AIQ_K_REL, AIQ_K_PACK, AIQ_K_EMBED, AIQ_K_NORM, AIQ_K_GEMM_QKV, AIQ_K_ATTN, AIQ_K_GEMM_O,
- AIQ_K_GEMM_UP, AIQ_K_GEMM_DOWN, AIQ_K_HEAD, AIQ_K_AGG, AIQ_K_DECODE) = range(12)
+ AIQ_K_GEMM_UP, AIQ_K_GEMM_DOWN, AIQ_K_HEAD, AIQ_K_AGG, AIQ_K_DECODE, AIQ_K_DECODE_ATTN,
+ AIQ_K_DECODE_HEAD) = range(14)
 
 OPS = {"lt": AIQ_LT, "le": AIQ_LE, "gt": AIQ_GT, "ge": AIQ_GE, "eq": AIQ_EQ, "ne": AIQ_NE, "in": AIQ_IN}
 

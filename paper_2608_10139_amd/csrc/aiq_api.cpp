@@ -528,10 +528,10 @@ aiq_status enqueue_generation(const aiq_plan* p, void* ws, const Layout& L, cons
   auto next_tokens = [&](int step) -> aiq_status {
     for (int b = 0; b < p->gen_blocks; ++b) {
       const int64_t row0 = static_cast<int64_t>(b) * GEN_HEAD_ROWS;
-      TRACED(tr, AIQ_K_DECODE, gemm(EPI_STORE_F32, static_cast<const char*>(hf) + row0 * d * ab, d, cnt + b,
+      TRACED(tr, AIQ_K_DECODE_HEAD, gemm(EPI_STORE_F32, static_cast<const char*>(hf) + row0 * d * ab, d, cnt + b,
                                     std::min<int64_t>(su - row0, GEN_HEAD_ROWS), m.vocab, d, m.lm_head, nullptr,
                                     nullptr, logits, m.vocab, nullptr, false));
-      TRACED(tr, AIQ_K_DECODE, launch_gen_argmax(logits, m.vocab, cnt + b, row0, gd, step, G, q.eos_id, q.pad_id,
+      TRACED(tr, AIQ_K_DECODE_HEAD, launch_gen_argmax(logits, m.vocab, cnt + b, row0, gd, step, G, q.eos_id, q.pad_id,
                                                  tok, done, gen, s));
     }
     return AIQ_OK;
@@ -569,7 +569,7 @@ aiq_status enqueue_generation(const aiq_plan* p, void* ws, const Layout& L, cons
       ga.hd = p->hd;
       ga.out_act = p->act;
       ga.seq_ub = su;
-      TRACED(tr, AIQ_K_DECODE, launch_attention_gen(ga, s));
+      TRACED(tr, AIQ_K_DECODE_ATTN, launch_attention_gen(ga, s));
       TRACED(tr, AIQ_K_DECODE, gemm(EPI_RESID, att, p->d_q, n_rows, su, d, p->d_q, W.wo, nullptr, nullptr, nullptr,
                                     d, W.ffn_norm, true));
       TRACED(tr, AIQ_K_DECODE, launch_row_scale(gd, ssp, d / 64, d, eps, rs, su, s));
@@ -890,7 +890,7 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
     LikePattern pat{};
     pat.n = q.n_like;
     for (int k = 0; k < q.n_like; ++k) pat.tok[k] = q.like[k];
-    TRACED(tr, AIQ_K_DECODE, launch_gen_like(gen, ctr + C_SEL, n, p->gen, q.eos_id, pat, label, s));
+    TRACED(tr, AIQ_K_DECODE_HEAD, launch_gen_like(gen, ctr + C_SEL, n, p->gen, q.eos_id, pat, label, s));
   }
   // ---- decision -> kept ids, aggregates
   tr.begin(AIQ_K_AGG);

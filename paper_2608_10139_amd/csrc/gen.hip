@@ -105,27 +105,28 @@ hipError_t launch_gen_embed(const int64_t* gen_desc, const int64_t* cu, const in
 }
 
 // ------------------------------------------------------------------ decode attention
-// Workgroup per (sequence, K/V head): the rep = n_heads / n_kv query heads of
-// the group against every kept key of the sequence (prompt, earlier
-// generated tokens, this token).  Wave w takes the 64-key blocks w, w + 4,
-// ...: lane j scores key j against the group's queries (held in LDS, scaled
-// by log2(e) / sqrt(hd)), an online softmax runs per head, and for P V the
-// lanes switch to value dimensions, reading one value row per key (a
-// coalesced row read) with the key's probability broadcast by readlane.  The
-// four waves' partial states are merged through LDS.  The workgroup also
-// stores this step's key and value into the generated cache.
-template <int HD>
+// Wave per (sequence, K/V head): the REP = n_heads / n_kv query heads of the
+// group against every kept key of the sequence (prompt, earlier generated
+// tokens, this token).  A key row of HD fp16 values is read by LPK = HD / 8
+// lanes, 16 bytes each, so one wave load covers 64 / LPK whole rows; keys go
+// in blocks of 4 such loads (an online-softmax step), the next block's key
+// and value rows in flight while the current one is used.  Each lane keeps
+// its 8 query dims and 8 output dims per head; partial dot products meet
+// over the LPK lanes of a row, partial outputs over the key groups at the
+// end.  The wave also stores this step's key and value into the generated
+// cache.
+template <int HD, int REP>
 __global__ __launch_bounds__(256) void k_attn_gen(GenAttnArgs a) {
-  constexpr int DPL = HD / 64;   // value dimensions per lane
-  constexpr int RMAX = 8;        // query heads per K/V head (checked by the launcher)
-  __shared__ float qs[RMAX][HD];
-  __shared__ float mw[4][RMAX], lw[4][RMAX];
-  __shared__ float ow[4][RMAX][HD];
+  constexpr int LPK = HD / 8;     // lanes per key row
+  constexpr int KPI = 64 / LPK;   // key rows per wave load
+  constexpr int IT = 4;           // wave loads per block
+  constexpr int KB = KPI * IT;    // keys per online-softmax block
   const int64_t n = a.gen_desc[D_NSEQ], sb = a.gen_desc[D_SEQ_BEGIN], tb = a.chunk_desc[D_TOK_BEGIN];
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const int rep = a.n_heads / a.n_kv;
+  const int lane = threadIdx.x & 63, gk = lane / LPK, c = lane % LPK;
+  const int64_t wave = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6;
+  const int64_t n_waves = ((int64_t)gridDim.x * blockDim.x) >> 6;
   const int d_q = a.n_heads * HD, d_kv = a.n_kv * HD;
-  const float scale = 1.4426950408889634f / sqrtf(static_cast<float>(HD));
+  const float scale = 1.4426950408889634f / sqrtf(static_cast<float>(HD));   // log2(e) / sqrt(hd)
   const uint16_t* qkv = static_cast<const uint16_t*>(a.qkv);
   const uint16_t* kvc = static_cast<const uint16_t*>(a.kvc);
   const uint16_t* pkv = static_cast<const uint16_t*>(a.pkv);
@@ -134,7 +135,7 @@ __global__ __launch_bounds__(256) void k_attn_gen(GenAttnArgs a) {
   const int64_t ld = a.ld;
   const int64_t items = n * a.n_kv;
 
-  for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
+  for (int64_t item = wave; item < items; item += n_waves) {
     const int64_t i = item / a.n_kv;
     const int kvh = static_cast<int>(item % a.n_kv);
     const int64_t s0 = a.cu[sb + i] - tb;
@@ -143,147 +144,175 @@ __global__ __launch_bounds__(256) void k_attn_gen(GenAttnArgs a) {
     const uint16_t* qrow = qkv + i * ld;
     const int kc = d_q + kvh * HD, vc = d_q + d_kv + kvh * HD;   // key / value columns of a q|k|v row
     uint16_t* gslot = gkv + (i * a.gen + a.step) * (2 * d_kv);
-    for (int e = t; e < 2 * HD; e += 256)
-      gslot[e < HD ? kvh * HD + e : d_kv + kvh * HD + (e - HD)] = qrow[e < HD ? kc + e : vc + (e - HD)];
-    for (int e = t; e < rep * HD; e += 256) qs[e / HD][e % HD] = h2f(qrow[(kvh * rep + e / HD) * HD + e % HD]) * scale;
-    __syncthreads();
-
-    // key j's key and value rows
-    auto kv_of = [&](int j, const uint16_t*& kp, const uint16_t*& vp) {
+    if (lane < 2 * LPK) {
+      const bool isv = lane >= LPK;
+      const int cc = lane % LPK;
+      *reinterpret_cast<uint4*>(gslot + (isv ? d_kv : 0) + kvh * HD + cc * 8) =
+          *reinterpret_cast<const uint4*>(qrow + (isv ? vc : kc) + cc * 8);
+    }
+    float qf[REP][8];
+#pragma unroll
+    for (int r = 0; r < REP; ++r) {
+      const uint4 u = *reinterpret_cast<const uint4*>(qrow + (kvh * REP + r) * HD + c * 8);
+      const uint32_t uw[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        qf[r][2 * e] = h2f(static_cast<uint16_t>(uw[e] & 0xFFFFu)) * scale;
+        qf[r][2 * e + 1] = h2f(static_cast<uint16_t>(uw[e] >> 16)) * scale;
+      }
+    }
+    // this lane's 16-byte pieces of key j's key and value rows
+    auto rows_of = [&](int j, const uint16_t*& kp, const uint16_t*& vp) {
+      const uint16_t* row;
+      int ko = kc, vo = vc;
       if (j < a.npre) {
-        kp = pkv + static_cast<int64_t>(j) * ld + kc;
-        vp = pkv + static_cast<int64_t>(j) * ld + vc;
+        row = pkv + static_cast<int64_t>(j) * ld;
       } else if (j < P) {
-        const uint16_t* row = kvc + (s0 + j - a.npre) * ld;
-        kp = row + kc;
-        vp = row + vc;
+        row = kvc + (s0 + j - a.npre) * ld;
       } else if (j < P + a.step) {
-        const uint16_t* row = gkv + (i * a.gen + (j - P)) * (2 * d_kv);
-        kp = row + kvh * HD;
-        vp = row + d_kv + kvh * HD;
+        row = gkv + (i * a.gen + (j - P)) * (2 * d_kv);
+        ko = kvh * HD;
+        vo = d_kv + kvh * HD;
       } else {
-        kp = qrow + kc;
-        vp = qrow + vc;
+        row = qrow;
+      }
+      kp = row + ko + c * 8;
+      vp = row + vo + c * 8;
+    };
+    auto load_block = [&](int kb, uint4 (&kr)[IT], uint4 (&vr)[IT]) {
+#pragma unroll
+      for (int it = 0; it < IT; ++it) {
+        const int j = kb + it * KPI + gk;
+        kr[it] = make_uint4(0, 0, 0, 0);
+        vr[it] = make_uint4(0, 0, 0, 0);
+        if (j < N) {
+          const uint16_t *kp, *vp;
+          rows_of(j, kp, vp);
+          kr[it] = *reinterpret_cast<const uint4*>(kp);
+          vr[it] = *reinterpret_cast<const uint4*>(vp);
+        }
       }
     };
 
-    float m[RMAX], l[RMAX], o[RMAX][DPL];
+    float m[REP], l[REP], o[REP][8];
 #pragma unroll
-    for (int r = 0; r < RMAX; ++r) {
+    for (int r = 0; r < REP; ++r) {
       m[r] = -INFINITY;
       l[r] = 0.f;
 #pragma unroll
-      for (int e = 0; e < DPL; ++e) o[r][e] = 0.f;
+      for (int e = 0; e < 8; ++e) o[r][e] = 0.f;
     }
-    for (int blk = w; blk * 64 < N; blk += 4) {
-      // the queries stay in LDS: without this the compiler hoists all rep * HD
-      // of them into registers for the whole loop and spills
-      asm volatile("" ::: "memory");
-      const int j = blk * 64 + lane;
-      const bool valid = j < N;
-      float sc[RMAX];
+    uint4 kr[IT], vr[IT];
+    load_block(0, kr, vr);
+    for (int kb = 0; kb < N; kb += KB) {
+      uint4 kn[IT], vn[IT];
+      if (kb + KB < N) load_block(kb + KB, kn, vn);   // next block in flight
+      float s[REP][IT];
 #pragma unroll
-      for (int r = 0; r < RMAX; ++r) sc[r] = 0.f;
-      if (valid) {
-        const uint16_t *kp, *vp;
-        kv_of(j, kp, vp);
-#pragma unroll 2
-        for (int c = 0; c < HD; c += 8) {
-          const uint4 u = *reinterpret_cast<const uint4*>(kp + c);
-          const uint32_t uw[4] = {u.x, u.y, u.z, u.w};
-          float kf[8];
+      for (int it = 0; it < IT; ++it) {
+        const uint32_t uw[4] = {kr[it].x, kr[it].y, kr[it].z, kr[it].w};
+        float kf[8];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            kf[2 * e] = h2f(static_cast<uint16_t>(uw[e] & 0xFFFFu));
-            kf[2 * e + 1] = h2f(static_cast<uint16_t>(uw[e] >> 16));
-          }
+        for (int e = 0; e < 4; ++e) {
+          kf[2 * e] = h2f(static_cast<uint16_t>(uw[e] & 0xFFFFu));
+          kf[2 * e + 1] = h2f(static_cast<uint16_t>(uw[e] >> 16));
+        }
+        const bool ok = kb + it * KPI + gk < N;
 #pragma unroll
-          for (int r = 0; r < RMAX; ++r) {
-            if (r < rep) {
+        for (int r = 0; r < REP; ++r) {
+          float dot = 0.f;
 #pragma unroll
-              for (int e = 0; e < 8; ++e) sc[r] = fmaf(qs[r][c + e], kf[e], sc[r]);
-            }
-          }
+          for (int e = 0; e < 8; ++e) dot = fmaf(qf[r][e], kf[e], dot);
+#pragma unroll
+          for (int off = 1; off < LPK; off <<= 1) dot += __shfl_xor(dot, off);
+          s[r][it] = ok ? dot : -INFINITY;
         }
       }
-      float p[RMAX];
+      float vf[IT][8];
 #pragma unroll
-      for (int r = 0; r < RMAX; ++r) {
-        p[r] = 0.f;
-        if (r < rep) {
-          const float s = valid ? sc[r] : -INFINITY;
-          const float m_new = fmaxf(m[r], wave_max_g(s));   // finite: key blk * 64 is valid
-          const float alpha = exp2f(m[r] - m_new);
-          p[r] = valid ? exp2f(s - m_new) : 0.f;
-          l[r] = l[r] * alpha + wave_sum_g(p[r]);
+      for (int it = 0; it < IT; ++it) {
+        const uint32_t uw[4] = {vr[it].x, vr[it].y, vr[it].z, vr[it].w};
 #pragma unroll
-          for (int e = 0; e < DPL; ++e) o[r][e] *= alpha;
-          m[r] = m_new;
+        for (int e = 0; e < 4; ++e) {
+          vf[it][2 * e] = h2f(static_cast<uint16_t>(uw[e] & 0xFFFFu));
+          vf[it][2 * e + 1] = h2f(static_cast<uint16_t>(uw[e] >> 16));
         }
       }
-      const int nk = (N - blk * 64) < 64 ? (N - blk * 64) : 64;
-      for (int jj = 0; jj < nk; ++jj) {
-        const uint16_t *kp, *vp;
-        kv_of(blk * 64 + jj, kp, vp);
-        float v[DPL];
-        if constexpr (DPL == 1) {
-          v[0] = h2f(vp[lane]);
-        } else {
-          const uint32_t u = *reinterpret_cast<const uint32_t*>(vp + 2 * lane);
-          v[0] = h2f(static_cast<uint16_t>(u & 0xFFFFu));
-          v[DPL - 1] = h2f(static_cast<uint16_t>(u >> 16));
-        }
 #pragma unroll
-        for (int r = 0; r < RMAX; ++r) {
-          if (r < rep) {
-            const float pj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(p[r]), jj));
+      for (int r = 0; r < REP; ++r) {
+        float mx = s[r][0];
 #pragma unroll
-            for (int e = 0; e < DPL; ++e) o[r][e] = fmaf(pj, v[e], o[r][e]);
-          }
+        for (int it = 1; it < IT; ++it) mx = fmaxf(mx, s[r][it]);
+        const float m_new = fmaxf(m[r], wave_max_g(mx));   // finite: key kb is valid
+        const float alpha = exp2f(m[r] - m_new);
+        float p[IT], ps = 0.f;
+#pragma unroll
+        for (int it = 0; it < IT; ++it) {
+          p[it] = exp2f(s[r][it] - m_new);   // 0 for keys past the end (score -inf)
+          ps += p[it];
         }
+        // every key's probability sits in its LPK lanes: count it once
+        l[r] = l[r] * alpha + wave_sum_g(c == 0 ? ps : 0.f);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          float acc = o[r][e] * alpha;
+#pragma unroll
+          for (int it = 0; it < IT; ++it) acc = fmaf(p[it], vf[it][e], acc);
+          o[r][e] = acc;
+        }
+        m[r] = m_new;
       }
-    }
+      if (kb + KB < N) {
 #pragma unroll
-    for (int r = 0; r < RMAX; ++r) {
-      if (r < rep) {
-        if (lane == 0) {
-          mw[w][r] = m[r];
-          lw[w][r] = l[r];
+        for (int it = 0; it < IT; ++it) {
+          kr[it] = kn[it];
+          vr[it] = vn[it];
         }
-#pragma unroll
-        for (int e = 0; e < DPL; ++e) ow[w][r][lane * DPL + e] = o[r][e];
       }
     }
-    __syncthreads();
-    for (int e = t; e < rep * HD; e += 256) {
-      const int r = e / HD, dd = e % HD;
-      float M = mw[0][r];
+    // partial outputs of the key groups (lanes with the same dims) add up
 #pragma unroll
-      for (int u = 1; u < 4; ++u) M = fmaxf(M, mw[u][r]);
-      float O = 0.f, Ls = 0.f;
+    for (int r = 0; r < REP; ++r) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const float f = exp2f(mw[u][r] - M);   // 0 for a wave that saw no key
-        O += ow[u][r][dd] * f;
-        Ls += lw[u][r] * f;
+      for (int e = 0; e < 8; ++e)
+#pragma unroll
+        for (int off = LPK; off < 64; off <<= 1) o[r][e] += __shfl_xor(o[r][e], off);
+      if (gk == 0) {
+        const float inv = 1.0f / l[r];
+        uint32_t pk[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          pk[e] = f2act(o[r][2 * e] * inv, a.out_act) |
+                  (static_cast<uint32_t>(f2act(o[r][2 * e + 1] * inv, a.out_act)) << 16);
+        *reinterpret_cast<uint4*>(out + i * d_q + (kvh * REP + r) * HD + c * 8) = make_uint4(pk[0], pk[1], pk[2], pk[3]);
       }
-      out[i * d_q + (kvh * rep + r) * HD + dd] = f2act(O / Ls, a.out_act);
     }
-    __syncthreads();   // LDS reused by the next item
   }
 }
 
 hipError_t launch_attention_gen(const GenAttnArgs& a, hipStream_t s) {
-  if (a.n_kv <= 0 || a.n_heads % a.n_kv || a.n_heads / a.n_kv > 8 || a.npre < 0 || (a.npre > 0 && !a.pkv) ||
-      a.step < 0 || a.step >= a.gen || a.out_act == ACT_F32)
+  if (a.n_kv <= 0 || a.n_heads % a.n_kv || a.npre < 0 || (a.npre > 0 && !a.pkv) || a.step < 0 ||
+      a.step >= a.gen || a.out_act == ACT_F32)
     return hipErrorInvalidValue;
-  const int g = grid_for(a.seq_ub * a.n_kv, 1, 4096);
-  if (a.hd == 64)
-    hipLaunchKernelGGL(k_attn_gen<64>, dim3(g), dim3(256), 0, s, a);
-  else if (a.hd == 128)
-    hipLaunchKernelGGL(k_attn_gen<128>, dim3(g), dim3(256), 0, s, a);
-  else
+  const int rep = a.n_heads / a.n_kv;
+  const dim3 grid(grid_for(a.seq_ub * a.n_kv, 4, 8192)), block(256);
+#define AIQ_GEN_ATTN(HD_)                                                          \
+  switch (rep) {                                                                   \
+    case 1: hipLaunchKernelGGL((k_attn_gen<HD_, 1>), grid, block, 0, s, a); break; \
+    case 2: hipLaunchKernelGGL((k_attn_gen<HD_, 2>), grid, block, 0, s, a); break; \
+    case 3: hipLaunchKernelGGL((k_attn_gen<HD_, 3>), grid, block, 0, s, a); break; \
+    case 4: hipLaunchKernelGGL((k_attn_gen<HD_, 4>), grid, block, 0, s, a); break; \
+    case 8: hipLaunchKernelGGL((k_attn_gen<HD_, 8>), grid, block, 0, s, a); break; \
+    default: return hipErrorInvalidValue;                                          \
+  }
+  if (a.hd == 64) {
+    AIQ_GEN_ATTN(64)
+  } else if (a.hd == 128) {
+    AIQ_GEN_ATTN(128)
+  } else {
     return hipErrorInvalidValue;
+  }
+#undef AIQ_GEN_ATTN
   return hipGetLastError();
 }
 

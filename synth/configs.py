@@ -193,6 +193,25 @@ WORKLOADS = {
         queries=(Query(preds=(Pred("values_a", "ge", 30.0), Pred("rating", "ne", 4)), labels=_BINARY,
                        decision="binary_gt", agg="sum_f32", group_col="values_a"),),
     ),
+    # AI_TRANSFORM with a relational predicate (Q3): the selectivity sweep of
+    # the paper's Table 4 (values_a < 10 .. 90), a short prompt, 32 new tokens
+    "reviews_transform": Workload(
+        name="reviews_transform", description="Q3: AI_TRANSFORM of rows passing values_a < t (t = 10 .. 90), "
+                                              "32 generated tokens, 16,384 rows, 4-layer d512 bf16 decoder",
+        table=_REVIEWS_TABLE,
+        model=SMALL,
+        queries=tuple(Query(preds=(Pred("values_a", "lt", float(t)),), labels=(), decision="binary_gt",
+                            agg="count", n_prefix=8, gen_tokens=32) for t in (10, 30, 50, 70, 90)),
+    ),
+    # COUNT over long generations filtered by LIKE (Q5)
+    "reviews_like": Workload(
+        name="reviews_like", description="Q5: COUNT(*) WHERE AI_TRANSFORM(text) LIKE '%p%', 128 generated "
+                                         "tokens per row, 16,384 rows, 4-layer d512 bf16 decoder",
+        table=_REVIEWS_TABLE,
+        model=SMALL,
+        queries=(Query(preds=(), labels=(), decision="binary_gt", agg="count", n_prefix=12, gen_tokens=128,
+                       eos_id=2, pad_id=0, like=(17, 17)),),
+    ),
     "groupby1b": Workload(
         name="groupby1b", description="1B-class 5-way classify + GROUP BY movie_id, 131,072 rows",
         table=TableSpec(n_rows=131072, seed=2, length=_LOGN_120, tokens=_ZIPF_TOK, rating=_RATING_P,

@@ -255,3 +255,46 @@ def test_run_rejects_before_enqueue():
         assert lib.aiq_prefill_packed(p, FAKE, FAKE, 2, 10, B.AIQ_LOGITS_LABELS, FAKE, FAKE, 16, None) == B.AIQ_ENOSPC
     finally:
         B.aiq_plan_destroy(p)
+
+
+def _gen_query(**kw):
+    q = query(n_labels=0, gen_tokens=16, eos_id=2, pad_id=0)
+    for k, v in kw.items():
+        setattr(q, k, v)
+    return q
+
+
+def test_transform_plan_validation():
+    ok = B.AIQ_OK
+    # labels are not needed for generation
+    assert B.aiq_plan_create_status(model(), table(), None, _gen_query()) == ok
+    assert B.aiq_plan_create_status(model(), table(), None, _gen_query(gen_tokens=B.AIQ_MAX_GEN + 1)) == B.AIQ_EINVAL
+    assert B.aiq_plan_create_status(model(), table(), None, _gen_query(gen_tokens=-1)) == B.AIQ_EINVAL
+    assert B.aiq_plan_create_status(model(), table(), None, _gen_query(eos_id=32000)) == B.AIQ_EINVAL
+    q = _gen_query(n_like=2)
+    q.like[0], q.like[1] = 5, 32000
+    assert B.aiq_plan_create_status(model(), table(), None, q) == B.AIQ_EINVAL
+    q.like[1] = 6
+    assert B.aiq_plan_create_status(model(), table(), None, q) == ok
+    assert B.aiq_plan_create_status(model(), table(), None, _gen_query(n_like=B.AIQ_MAX_LIKE + 1)) == B.AIQ_EINVAL
+    # fp32 models and vocabularies that the full-vocabulary head cannot tile
+    assert B.aiq_plan_create_status(model(wdtype=B.AIQ_F32), table(), None, _gen_query()) == B.AIQ_EUNSUPPORTED
+    assert B.aiq_plan_create_status(model(vocab=32001), table(), None, _gen_query()) == B.AIQ_EUNSUPPORTED
+    # no label to average
+    q = _gen_query(agg=B.AIQ_AGG_AVG_LABEL_COUNT_BY, group_col=1, n_group_keys=4)
+    assert B.aiq_plan_create_status(model(), table(), None, q) == B.AIQ_EINVAL
+
+
+def test_transform_workspace_holds_the_generation_state():
+    plain = B.aiq_plan_create(model(), table(), None, query())
+    g16 = B.aiq_plan_create(model(), table(), None, _gen_query(gen_tokens=16))
+    g32 = B.aiq_plan_create(model(), table(), None, _gen_query(gen_tokens=32))
+    try:
+        wp, w16, w32 = (B.aiq_workspace_size(p) for p in (plain, g16, g32))
+        assert wp < w16 < w32
+        # 16 more slots per row in the generated-token cache: 2 layers x 1000
+        # rows x 16 x 2 * 512 fp16 values, and 16 more token ids per row
+        assert w32 - w16 >= 2 * 1000 * 16 * 2 * 512 * 2 + 1000 * 16 * 4
+    finally:
+        for p in (plain, g16, g32):
+            B.aiq_plan_destroy(p)
