@@ -138,6 +138,7 @@ class Query:
     eos_id: int = -1
     pad_id: int = 0
     like: Tuple[int, ...] = ()        # LIKE '%pattern%' over the generated token ids
+    pair_key: Optional[str] = None    # Q4: classify pairs of selected rows with equal keys in this column
 
 
 @dataclass(frozen=True)
