@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define AIQ_ABI_VERSION 3
+#define AIQ_ABI_VERSION 4
 
 typedef enum aiq_status {
   AIQ_OK = 0,
@@ -90,6 +90,8 @@ typedef enum aiq_logits_mode { AIQ_LOGITS_LABELS = 1, AIQ_LOGITS_FULL_VOCAB = 2 
 #define AIQ_DEV_GROUP_RANGE 0x10  /* group key outside [0, n_group_keys): skipped   */
 #define AIQ_DEV_LIST_LEN    0x20  /* a row's list longer than max_list_len          */
 #define AIQ_DEV_GROUP_CAP   0x40  /* more groups than aiq_out.grp_cap               */
+#define AIQ_DEV_PAIR_CAP    0x80  /* more candidate pairs than aiq_query.max_pairs:
+                                     the pairs past it are dropped                  */
 
 /* indices into aiq_out.scalars (int64, device) */
 #define AIQ_S_SELECTED 0   /* rows passing WHERE (and the join)                      */
@@ -97,6 +99,7 @@ typedef enum aiq_logits_mode { AIQ_LOGITS_LABELS = 1, AIQ_LOGITS_FULL_VOCAB = 2 
 #define AIQ_S_TOKENS   2   /* total prefill tokens (prefix + row tokens)             */
 #define AIQ_S_STATUS   3   /* OR of AIQ_DEV_* bits                                   */
 #define AIQ_S_GROUPS   4   /* number of non-empty groups written                     */
+#define AIQ_S_PAIRS    5   /* pairs mode: candidate pairs classified (<= max_pairs)  */
 #define AIQ_N_SCALARS  8
 
 #define AIQ_MAX_PREDS 8
@@ -211,6 +214,20 @@ typedef struct aiq_query {
   int32_t pad_id;
   int32_t n_like;                      /* 0..AIQ_MAX_LIKE */
   int32_t like[AIQ_MAX_LIKE];
+  /* Pairs of rows (Section 4, Q4: a self-join on the movie id that classifies
+     [A.text, B.text]).  pairs = 1: the candidates are every two selected rows
+     A < B (row order) with equal values of probe column pair_key_col, whose
+     values must lie in [0, n_group_keys) (n_group_keys <= 16384; others are
+     flagged AIQ_DEV_GROUP_RANGE and left out); each pair's sequence is the
+     prefix, A's tokens, then B's tokens, classified with the binary decision.
+     Candidates are numbered ascending by (A, B); at most max_pairs are kept
+     (AIQ_DEV_PAIR_CAP otherwise).  out->ids receives the numbers of the pairs
+     the decision keeps, out->pair_a / pair_b their rows; sel_labels and
+     sel_logits are per candidate pair.  Requires no join, no generation,
+     agg COUNT and decision BINARY_GT. */
+  int32_t pairs;
+  int32_t pair_key_col;
+  int64_t max_pairs;
 } aiq_query;
 
 typedef struct aiq_plan_opts {
@@ -277,6 +294,12 @@ typedef struct aiq_out {
   /* optional, AI_TRANSFORM: [sel_cap, gen_tokens] generated tokens of each
      selected row (same order as sel_ids), pad_id after a row's end */
   int32_t* sel_gen;
+  /* optional, pairs mode: rows A and B of the kept pairs (capacity ids_cap)
+     and of every candidate pair (capacity sel_cap), in pair order */
+  int32_t* pair_a;
+  int32_t* pair_b;
+  int32_t* cand_a;
+  int32_t* cand_b;
 } aiq_out;
 
 /*

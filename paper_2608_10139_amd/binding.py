@@ -13,7 +13,7 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libaiq.so")
 
-AIQ_ABI_VERSION = 3   # the struct layouts below
+AIQ_ABI_VERSION = 4   # the struct layouts below
 AIQ_OK, AIQ_EINVAL, AIQ_EUNSUPPORTED, AIQ_ENOSPC, AIQ_EHIP, AIQ_ENOMEM = 0, -1, -2, -3, -4, -5
 AIQ_I8, AIQ_I16, AIQ_I32, AIQ_F32, AIQ_BF16, AIQ_F16 = 1, 2, 3, 4, 5, 6
 AIQ_LT, AIQ_LE, AIQ_GT, AIQ_GE, AIQ_EQ, AIQ_NE, AIQ_IN = range(7)
@@ -25,8 +25,8 @@ AIQ_PLAN_RELATIONAL_ONLY = 1
 AIQ_PLAN_UNSHARED_PREFIX = 2
 
 AIQ_DEV_TOKEN_RANGE, AIQ_DEV_DUP_KEY, AIQ_DEV_HASH_FULL, AIQ_DEV_IDS_CAP = 0x01, 0x02, 0x04, 0x08
-AIQ_DEV_GROUP_RANGE, AIQ_DEV_LIST_LEN, AIQ_DEV_GROUP_CAP = 0x10, 0x20, 0x40
-AIQ_S_SELECTED, AIQ_S_KEPT, AIQ_S_TOKENS, AIQ_S_STATUS, AIQ_S_GROUPS = range(5)
+AIQ_DEV_GROUP_RANGE, AIQ_DEV_LIST_LEN, AIQ_DEV_GROUP_CAP, AIQ_DEV_PAIR_CAP = 0x10, 0x20, 0x40, 0x80
+AIQ_S_SELECTED, AIQ_S_KEPT, AIQ_S_TOKENS, AIQ_S_STATUS, AIQ_S_GROUPS, AIQ_S_PAIRS = range(6)
 AIQ_N_SCALARS = 8
 AIQ_MAX_PREDS, AIQ_MAX_IN_SET, AIQ_MAX_PREFIX, AIQ_MAX_LABELS = 8, 32, 64, 8
 AIQ_MAX_GEN, AIQ_MAX_LIKE = 512, 16
@@ -75,7 +75,8 @@ class aiq_query(C.Structure):
                 ("n_labels", C.c_int32), ("label_ids", C.c_int32 * AIQ_MAX_LABELS),
                 ("decision", C.c_int32), ("agg", C.c_int32), ("group_col", C.c_int32),
                 ("n_group_keys", C.c_int32), ("gen_tokens", C.c_int32), ("eos_id", C.c_int32),
-                ("pad_id", C.c_int32), ("n_like", C.c_int32), ("like", C.c_int32 * AIQ_MAX_LIKE)]
+                ("pad_id", C.c_int32), ("n_like", C.c_int32), ("like", C.c_int32 * AIQ_MAX_LIKE),
+                ("pairs", C.c_int32), ("pair_key_col", C.c_int32), ("max_pairs", C.c_int64)]
 
 
 class aiq_plan_opts(C.Structure):
@@ -88,7 +89,8 @@ class aiq_out(C.Structure):
                 ("sel_ids", C.c_void_p), ("sel_labels", C.c_void_p), ("sel_logits", C.c_void_p),
                 ("sel_cap", C.c_int64), ("grp_key", C.c_void_p), ("grp_count", C.c_void_p),
                 ("grp_sum", C.c_void_p), ("grp_avg", C.c_void_p), ("grp_cap", C.c_int64),
-                ("sum_out", C.c_void_p), ("sel_gen", C.c_void_p)]
+                ("sum_out", C.c_void_p), ("sel_gen", C.c_void_p), ("pair_a", C.c_void_p),
+                ("pair_b", C.c_void_p), ("cand_a", C.c_void_p), ("cand_b", C.c_void_p)]
 
 
 class aiq_trace(C.Structure):

@@ -26,6 +26,8 @@ struct aiq_plan {
   // shared by every row (16-bit models, unless AIQ_PLAN_UNSHARED_PREFIX)
   bool share_prefix = false;
   int32_t gen = 0;        // AI_TRANSFORM: tokens generated per selected row (0: AI_IF)
+  bool pairs = false;     // Q4: the sequences are candidate pairs of selected rows
+  int64_t n_seq_ub = 0;   // upper bound on sequences: selected rows, or max_pairs
   int32_t gen_blocks = 0; // row blocks of the full-vocabulary head
   aiq_table probe{}, build{};
   std::vector<aiq_col> probe_cols, build_cols;
@@ -145,7 +147,8 @@ aiq_status validate_model(const aiq_model* m) {
 struct Layout {
   size_t ctr, mask, blk_cnt, blk_off, sel, payload, lens, label, logits, cu, blk_tok, tok_off, packed, hkeys, hvals,
       bins, desc, rcos, rsin, rrev, x, delta, h, qkv, att, ffn, pos, hf, ssp, rs, pkv, ptok, pcu, pdesc, pxlast,
-      kvc, gkv, glog, gtok, gdone, gen, gdesc, gcnt, total;
+      kvc, gkv, glog, gtok, gdone, gen, gdesc, gcnt, kcount, koff, prank, psorted, pcnt, poff, pscan, pa, pb,
+      total;
 };
 
 size_t act_bytes(const aiq_plan* p) { return p->bf16 ? 2 : 4; }
@@ -180,7 +183,8 @@ Layout run_layout(const aiq_plan* p) {
   Layout L{};
   Carver c;
   const int64_t n = p->n_rows;
-  const int64_t nb = (n + REL_ROWS_PER_BLOCK - 1) / REL_ROWS_PER_BLOCK + 1;
+  const int64_t ns = std::max<int64_t>(n, p->n_seq_ub);   // rows, or candidate pairs, whichever is more
+  const int64_t nb = (ns + REL_ROWS_PER_BLOCK - 1) / REL_ROWS_PER_BLOCK + 1;
   const int d = p->model.d_model;
   const size_t ab = act_bytes(p);
   L.ctr = c.take(C_COUNT * 8);
@@ -189,10 +193,10 @@ Layout run_layout(const aiq_plan* p) {
   L.blk_off = c.take(static_cast<size_t>(nb + 1) * 8);
   L.sel = c.take(static_cast<size_t>(n + 1) * 4);
   L.payload = c.take(static_cast<size_t>(n + 1) * 4);
-  L.lens = c.take(static_cast<size_t>(n + 24) * 4);   // read in 16-entry groups from an 8-aligned start
-  L.label = c.take(static_cast<size_t>(n + 1) * 4);
-  L.logits = c.take(static_cast<size_t>(n + 1) * p->q.n_labels * 4);
-  L.cu = c.take(static_cast<size_t>(n + 1) * 8);
+  L.lens = c.take(static_cast<size_t>(ns + 24) * 4);   // read in 16-entry groups from an 8-aligned start
+  L.label = c.take(static_cast<size_t>(ns + 1) * 4);
+  L.logits = c.take(static_cast<size_t>(ns + 1) * p->q.n_labels * 4);
+  L.cu = c.take(static_cast<size_t>(ns + 1) * 8);
   L.blk_tok = c.take(static_cast<size_t>(nb) * 8);
   L.tok_off = c.take(static_cast<size_t>(nb + 1) * 8);
   const size_t hcap = p->hash_log2 ? (size_t(1) << p->hash_log2) : 1;
@@ -218,6 +222,18 @@ Layout run_layout(const aiq_plan* p) {
     L.pcu = c.take(2 * 8);
     L.pdesc = c.take(D_STRIDE * 8);
     L.pxlast = c.take(static_cast<size_t>(d) * 4);
+  }
+  if (p->pairs) {   // key histogram and offsets, ranks, the rows sorted by key, partner counts, pair lists
+    const size_t nk = static_cast<size_t>(p->q.n_group_keys);
+    L.kcount = c.take(nk * 4);
+    L.koff = c.take((nk + 1) * 8);
+    L.prank = c.take(static_cast<size_t>(n + 1) * 4);
+    L.psorted = c.take(static_cast<size_t>(n + 1) * 4);
+    L.pcnt = c.take(static_cast<size_t>(n + 1) * 4);
+    L.poff = c.take(static_cast<size_t>(n + 1) * 8);
+    L.pscan = c.take(static_cast<size_t>(2 * (std::max<int64_t>(ns, static_cast<int64_t>(nk)) / REL_ROWS_PER_BLOCK + 3)) * 8);
+    L.pa = c.take(static_cast<size_t>(p->n_seq_ub) * 4);
+    L.pb = c.take(static_cast<size_t>(p->n_seq_ub) * 4);
   }
   if (p->gen > 0) {   // AI_TRANSFORM: kept prompt keys / values, generated-token cache, head, tokens
     const size_t G = static_cast<size_t>(p->gen), su = static_cast<size_t>(p->seq_ub);
@@ -684,6 +700,17 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
       p->hash_log2 = lg;
     }
     if (p->rel_only && q.agg != AIQ_AGG_COUNT) return fail(AIQ_EINVAL);
+    if (q.pairs != 0 && q.pairs != 1) return fail(AIQ_EINVAL);
+    if (q.pairs) {   // Q4 pairs: binary AI_IF over every two selected rows of a key
+      if (p->rel_only || q.join || p->gen > 0 || q.agg != AIQ_AGG_COUNT || q.decision != AIQ_DECIDE_BINARY_GT)
+        return fail(AIQ_EINVAL);
+      if (q.pair_key_col < 0 || q.pair_key_col >= static_cast<int>(p->probe_cols.size())) return fail(AIQ_EINVAL);
+      if (!int_dtype(p->probe_cols[q.pair_key_col].dtype)) return fail(AIQ_EUNSUPPORTED);
+      if (q.n_group_keys <= 0) return fail(AIQ_EINVAL);
+      if (q.n_group_keys > PAIR_MAX_KEYS) return fail(AIQ_EUNSUPPORTED);
+      if (q.max_pairs <= 0 || q.max_pairs > INT32_MAX) return fail(AIQ_EINVAL);
+      p->pairs = true;
+    }
     switch (q.agg) {
       case AIQ_AGG_COUNT: break;
       case AIQ_AGG_AVG_LABEL_COUNT_BY:
@@ -704,11 +731,16 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
     p->n_rows = p->probe.n_rows;
     p->share_prefix = p->bf16 && q.n_prefix > 0 && p->n_layers > 0 && !p->rel_only &&
                       !(opts && (opts->flags & AIQ_PLAN_UNSHARED_PREFIX));
-    // packed tokens: the row lists, plus the prefix per row unless it is shared
-    p->t_ub = p->probe.n_list_tokens + (p->share_prefix ? 0 : p->n_rows * q.n_prefix);
-    p->max_seq = p->probe.max_list_len + q.n_prefix;   // positions (rotary table rows)
+    // packed tokens: the row lists (two per pair), plus the prefix per sequence
+    // unless it is shared
+    const int64_t npre_packed = p->share_prefix ? 0 : q.n_prefix;
+    const int64_t max_own = (p->pairs ? 2 : 1) * static_cast<int64_t>(p->probe.max_list_len);
+    p->n_seq_ub = p->pairs ? q.max_pairs : p->n_rows;
+    p->t_ub = p->pairs ? q.max_pairs * (max_own + npre_packed)
+                       : p->probe.n_list_tokens + p->n_rows * npre_packed;
+    p->max_seq = static_cast<int32_t>(max_own + q.n_prefix);   // positions (rotary table rows)
     // longest packed sequence: a chunk must hold one whole
-    const int64_t max_packed = p->share_prefix ? std::max<int64_t>(p->probe.max_list_len, q.n_prefix) : p->max_seq;
+    const int64_t max_packed = p->share_prefix ? std::max<int64_t>(max_own, q.n_prefix) : p->max_seq;
     // default chunk: about 48 GB of per-token activations (a fraction of one
     // MI355X's 288 GB), at most 4M tokens
     // (+ every layer's kept q|k|v rows when the rows go on to generate)
@@ -729,7 +761,7 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
       p->seq_ub = std::min<int64_t>(p->n_rows, ct);
     } else {
       p->n_chunks = std::max<int64_t>((p->t_ub + ct - 1) / ct, 1);
-      p->seq_ub = std::min<int64_t>(p->n_rows, p->t_cap);
+      p->seq_ub = std::min<int64_t>(p->n_seq_ub, p->t_cap);
     }
     p->gen_blocks = p->gen > 0 ? static_cast<int32_t>((p->seq_ub + GEN_HEAD_ROWS - 1) / GEN_HEAD_ROWS) : 0;
     p->prefix.n = q.n_prefix;
@@ -824,12 +856,46 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
                                 out->sel_cap > 0 ? out->sel_ids : nullptr, out->sel_cap, sl));
   else
     HIP_TRY(launch_scatter_rows(mask, blk_off, nullptr, n, nullptr, sel, n, pkey, pkey_dt, h, p->has_build,
-                                payload, ctr, s, nullptr, 0, sl));
+                                payload, ctr, s, nullptr, 0, p->pairs ? ScatterLens{} : sl));
   tr.end();
-  // ---- token offsets of the selected rows
+  // the sequences: the selected rows, or the candidate pairs
+  const int64_t* n_seq = ctr + (p->pairs ? C_PAIRS : C_SEL);
+  const int64_t ns_ub = p->n_seq_ub;
+  int32_t* pa = p->pairs ? at<int32_t>(ws, L.pa) : nullptr;
+  int32_t* pb = p->pairs ? at<int32_t>(ws, L.pb) : nullptr;
+  Prefix row_prefix{};
+  if (!p->share_prefix) row_prefix = p->prefix;
   tr.begin(AIQ_K_PACK);
-  HIP_TRY(launch_scan_blocks64(blk_tok, nullptr, n, tok_off, ctr + C_TOK, s));
-  HIP_TRY(launch_cu_from_blocks(lens, blk_off, tok_off, n, cu, s));
+  if (p->pairs) {
+    // ---- candidate pairs: rows sorted stably by key, partners, numbering, packing
+    const aiq_col& kc = p->probe_cols[q.pair_key_col];
+    const int32_t nk = q.n_group_keys;
+    int32_t* kcount = at<int32_t>(ws, L.kcount);
+    int64_t* koff = at<int64_t>(ws, L.koff);
+    int32_t* prank = at<int32_t>(ws, L.prank);
+    int32_t* psorted = at<int32_t>(ws, L.psorted);
+    int32_t* pcnt = at<int32_t>(ws, L.pcnt);
+    int64_t* poff = at<int64_t>(ws, L.poff);
+    int64_t* pscan = at<int64_t>(ws, L.pscan);
+    HIP_TRY(launch_fill_i32(kcount, nk, 0, s));
+    HIP_TRY(launch_pair_key_count(sel, ctr + C_SEL, n, kc.data, kc.dtype, nk, kcount, ctr, s));
+    HIP_TRY(launch_scan_i32_i64(kcount, nullptr, nk, koff, pscan, ctr + C_SCRATCH, s));
+    HIP_TRY(launch_pair_rank(sel, ctr + C_SEL, kc.data, kc.dtype, nk, koff, prank, psorted, s));
+    HIP_TRY(launch_pair_partners(sel, ctr + C_SEL, n, kc.data, kc.dtype, nk, kcount, prank, pcnt, s));
+    HIP_TRY(launch_scan_i32_i64(pcnt, ctr + C_SEL, n, poff, pscan, ctr + C_SCRATCH, s));
+    HIP_TRY(launch_pair_total(ctr + C_SCRATCH, ns_ub, ctr, s));
+    HIP_TRY(launch_pair_emit(sel, ctr + C_SEL, n, kc.data, kc.dtype, nk, koff, prank, psorted, pcnt, poff, ns_ub,
+                             pa, pb, s));
+    HIP_TRY(launch_pair_lens(pa, pb, sel, p->probe.list_offsets, p->probe.max_list_len, row_prefix.n, ns_ub, lens,
+                             ctr, s));
+    HIP_TRY(launch_scan_i32_i64(lens, n_seq, ns_ub, cu, pscan, ctr + C_TOK, s));
+    HIP_TRY(launch_pair_gather(pa, pb, sel, p->probe.list_offsets, p->probe.list_tokens, cu, row_prefix,
+                               p->probe.max_list_len, p->model.vocab, p->t_ub, ns_ub, packed, ctr, s));
+  } else {
+    // ---- token offsets of the selected rows
+    HIP_TRY(launch_scan_blocks64(blk_tok, nullptr, n, tok_off, ctr + C_TOK, s));
+    HIP_TRY(launch_cu_from_blocks(lens, blk_off, tok_off, n, cu, s));
+  }
   if (p->rel_only) {
     // relational part only: every selected id is kept
     tr.end();
@@ -840,11 +906,10 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
     return AIQ_OK;
   }
   // ---- pack: tokens, chunk descriptors
-  Prefix row_prefix{};
-  if (!p->share_prefix) row_prefix = p->prefix;
-  HIP_TRY(launch_gather_tokens(sel, ctr + C_SEL, n, p->probe.list_offsets, p->probe.list_tokens, cu, row_prefix,
-                               p->model.vocab, p->t_ub, packed, ctr, s));
-  HIP_TRY(launch_chunk_desc(cu, ctr + C_SEL, p->chunk_tokens, p->n_chunks, p->t_ub, desc, s, p->gen > 0 ? 1 : 0));
+  if (!p->pairs)
+    HIP_TRY(launch_gather_tokens(sel, ctr + C_SEL, n, p->probe.list_offsets, p->probe.list_tokens, cu, row_prefix,
+                                 p->model.vocab, p->t_ub, packed, ctr, s));
+  HIP_TRY(launch_chunk_desc(cu, n_seq, p->chunk_tokens, p->n_chunks, p->t_ub, desc, s, p->gen > 0 ? 1 : 0));
   HIP_TRY(launch_rope_table(p->max_seq, p->hd / 2, p->model.rope_theta, p->hd, at<float>(ws, L.rcos),
                             at<float>(ws, L.rsin), at<float>(ws, L.rrev), s));
   tr.end();
@@ -895,11 +960,14 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
   // ---- decision -> kept ids, aggregates
   tr.begin(AIQ_K_AGG);
   const bool binary = q.decision == AIQ_DECIDE_BINARY_GT || p->gen > 0;   // label = keep flag
-  if (binary) {
-    HIP_TRY(launch_label_mask(label, ctr + C_SEL, n, mask, blk_cnt, s));
-    HIP_TRY(launch_scan_blocks(blk_cnt, ctr + C_SEL, n, blk_off, ctr + C_KEPT, s));
-    HIP_TRY(launch_scatter_rows(mask, blk_off, ctr + C_SEL, n, sel, out->ids, out->ids_cap, nullptr, AIQ_I32, h, 0,
-                                nullptr, ctr, s));
+  if (binary) {   // kept rows (their ids), or kept pairs (their numbers)
+    const int64_t ub = p->pairs ? ns_ub : n;
+    HIP_TRY(launch_label_mask(label, n_seq, ub, mask, blk_cnt, s));
+    HIP_TRY(launch_scan_blocks(blk_cnt, n_seq, ub, blk_off, ctr + C_KEPT, s));
+    HIP_TRY(launch_scatter_rows(mask, blk_off, n_seq, ub, p->pairs ? nullptr : sel, out->ids, out->ids_cap, nullptr,
+                                AIQ_I32, h, 0, nullptr, ctr, s));
+    if (p->pairs && (out->pair_a || out->pair_b))
+      HIP_TRY(launch_pair_rows(out->ids, ctr + C_KEPT, ub, pa, pb, sel, out->pair_a, out->pair_b, out->ids_cap, s));
   } else {
     HIP_TRY(launch_copy_ids(sel, ctr + C_SEL, n, out->ids, out->ids_cap, ctr, 1, s));
   }
@@ -917,15 +985,17 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
   if (q.agg == AIQ_AGG_SUM_F32)
     HIP_TRY(launch_sum_f32(sel, label, ctr + C_SEL, static_cast<const float*>(p->probe_cols[q.group_col].data),
                            binary, at<double>(ws, L.bins), out->sum_out, s));
-  if (out->sel_cap > 0) {
+  if (out->sel_cap > 0) {   // labels and logits are per sequence (row, or candidate pair)
     if (out->sel_ids) HIP_TRY(launch_copy_ids(sel, ctr + C_SEL, n, out->sel_ids, out->sel_cap, ctr, 0, s));
-    if (out->sel_labels) HIP_TRY(launch_copy_ids(label, ctr + C_SEL, n, out->sel_labels, out->sel_cap, ctr, 0, s));
+    if (out->sel_labels) HIP_TRY(launch_copy_ids(label, n_seq, ns_ub, out->sel_labels, out->sel_cap, ctr, 0, s));
     if (out->sel_logits && p->gen == 0)
-      HIP_TRY(launch_copy_f32(logits, ctr + C_SEL, n, q.n_labels, out->sel_logits, out->sel_cap, s));
+      HIP_TRY(launch_copy_f32(logits, n_seq, ns_ub, q.n_labels, out->sel_logits, out->sel_cap, s));
+    if (p->pairs && (out->cand_a || out->cand_b))
+      HIP_TRY(launch_pair_rows(nullptr, n_seq, ns_ub, pa, pb, sel, out->cand_a, out->cand_b, out->sel_cap, s));
     if (out->sel_gen && p->gen > 0)
       HIP_TRY(launch_copy_rows_i32(gen, ctr + C_SEL, n, p->gen, out->sel_gen, out->sel_cap, s));
   }
-  HIP_TRY(launch_finalize(ctr, out->scalars, s, p->share_prefix ? q.n_prefix : 0));
+  HIP_TRY(launch_finalize(ctr, out->scalars, s, p->share_prefix ? q.n_prefix : 0, p->pairs ? C_PAIRS : C_SEL));
   tr.end();
   return AIQ_OK;
 }

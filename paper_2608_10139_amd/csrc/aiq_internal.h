@@ -18,6 +18,7 @@ enum Ctr : int {
   C_GROUPS = 4,   // non-empty groups
   C_SCRATCH = 5,  // scan totals land here before being copied
   C_NSEQ = 6,     // prefill-only: number of sequences
+  C_PAIRS = 7,    // pairs mode: candidate pairs (the sequences)
   C_COUNT = 16
 };
 
@@ -109,9 +110,10 @@ hipError_t launch_copy_ids(const int32_t* src, const int64_t* n_ptr, int64_t n_u
                            int64_t cap, int64_t* ctr, int set_kept, hipStream_t s);
 hipError_t launch_copy_f32(const float* src, const int64_t* n_ptr, int64_t n_ub, int32_t per_row,
                            float* dst, int64_t cap_rows, hipStream_t s);
-// scalars[AIQ_S_TOKENS] adds tok_per_row tokens per selected row to
-// ctr[C_TOK] (the shared prompt prefix, which is packed once, not per row).
-hipError_t launch_finalize(const int64_t* ctr, int64_t* scalars, hipStream_t s, int32_t tok_per_row = 0);
+// scalars[AIQ_S_TOKENS] adds tok_per_row tokens per sequence (ctr[seq_ctr])
+// to ctr[C_TOK] (the shared prompt prefix, which is packed once, not per row).
+hipError_t launch_finalize(const int64_t* ctr, int64_t* scalars, hipStream_t s, int32_t tok_per_row = 0,
+                           int32_t seq_ctr = C_SEL);
 // SUM_F32: fp64 sum of col[sel[i]] over the selected rows i < n_sel with
 // label[i] == 1 (binary decision) or all of them (argmax), in a fixed order:
 // SUM_BLOCKS fixed ranges of i, each reduced in a fixed tree, then the block
@@ -240,6 +242,50 @@ struct HeadArgs {
                              // sequences with no own token (null: such sequences get 0 logits)
 };
 hipError_t launch_head(const HeadArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- pairs (Q4 self-join)
+// Exclusive scan of v[0..n) (n = *n_ptr, or n_ub when n_ptr is null) into
+// out[0..n] as int64, out[n] = *total_out = the sum.  blk: scratch of
+// n_ub / 8192 + 2 int64 values for the block sums and their offsets (x2).
+hipError_t launch_scan_i32_i64(const int32_t* v, const int64_t* n_ptr, int64_t n_ub, int64_t* out, int64_t* blk,
+                               int64_t* total_out, hipStream_t s);
+// kcount[k] += 1 for the key of every selected row (keys outside
+// [0, n_keys) flagged AIQ_DEV_GROUP_RANGE and skipped)
+hipError_t launch_pair_key_count(const int32_t* sel, const int64_t* n_ptr, int64_t n_ub, const void* key_col,
+                                 int32_t key_dt, int32_t n_keys, int32_t* kcount, int64_t* ctr, hipStream_t s);
+// Stable counting sort of the selected rows by key: rank[i] = number of
+// earlier selected rows with the same key, sorted[koff[key] + rank[i]] = i.
+// One workgroup, 1024 rows per round; n_keys <= PAIR_MAX_KEYS.
+constexpr int PAIR_MAX_KEYS = 16384;
+hipError_t launch_pair_rank(const int32_t* sel, const int64_t* n_ptr, const void* key_col, int32_t key_dt,
+                            int32_t n_keys, const int64_t* koff, int32_t* rank, int32_t* sorted, hipStream_t s);
+// cnt[i] = later selected rows with the same key (0 for a key out of range)
+hipError_t launch_pair_partners(const int32_t* sel, const int64_t* n_ptr, int64_t n_ub, const void* key_col,
+                                int32_t key_dt, int32_t n_keys, const int32_t* kcount, const int32_t* rank,
+                                int32_t* cnt, hipStream_t s);
+// ctr[C_PAIRS] = min(*total, cap), AIQ_DEV_PAIR_CAP when above
+hipError_t launch_pair_total(const int64_t* total, int64_t cap, int64_t* ctr, hipStream_t s);
+// pair numbers poff[i] .. poff[i] + cnt[i] - 1 below cap: (pa, pb) = (i, the
+// later rows of i's key in order), as selected-row indices
+hipError_t launch_pair_emit(const int32_t* sel, const int64_t* n_ptr, int64_t n_ub, const void* key_col,
+                            int32_t key_dt, int32_t n_keys, const int64_t* koff, const int32_t* rank,
+                            const int32_t* sorted, const int32_t* cnt, const int64_t* poff, int64_t cap,
+                            int32_t* pa, int32_t* pb, hipStream_t s);
+// lens[q] = n_prefix + len(A) + len(B) of pair q < ctr[C_PAIRS] (a list
+// longer than max_len flagged AIQ_DEV_LIST_LEN and cut to max_len)
+hipError_t launch_pair_lens(const int32_t* pa, const int32_t* pb, const int32_t* sel, const int64_t* off,
+                            int32_t max_len, int32_t n_prefix, int64_t cap, int32_t* lens, int64_t* ctr,
+                            hipStream_t s);
+// packed[cu[q] ..] = prefix, A's tokens, B's tokens (wave per pair)
+hipError_t launch_pair_gather(const int32_t* pa, const int32_t* pb, const int32_t* sel, const int64_t* off,
+                              const int32_t* tokens, const int64_t* cu, const Prefix& prefix, int32_t max_len,
+                              int32_t vocab, int64_t t_ub, int64_t cap, int32_t* packed, int64_t* ctr,
+                              hipStream_t s);
+// rows of pairs: out_a[j] = sel[pa[q]], out_b[j] = sel[pb[q]] with q = ids[j]
+// (ids null: q = j), j < min(*n_ptr, cap)
+hipError_t launch_pair_rows(const int32_t* ids, const int64_t* n_ptr, int64_t n_ub, const int32_t* pa,
+                            const int32_t* pb, const int32_t* sel, int32_t* out_a, int32_t* out_b, int64_t cap,
+                            hipStream_t s);
 
 // ---------------------------------------------------------------- AI_TRANSFORM generation
 // A generation step works on one row per sequence of the chunk: its

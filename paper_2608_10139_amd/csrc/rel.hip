@@ -788,14 +788,15 @@ hipError_t launch_group_emit(const int64_t* bins, int32_t n_keys, int32_t* key_o
 
 // ------------------------------------------------------------------ finalize
 
-__global__ void k_finalize(const int64_t* ctr, int64_t* scalars, int32_t tok_per_row) {
+__global__ void k_finalize(const int64_t* ctr, int64_t* scalars, int32_t tok_per_row, int32_t seq_ctr) {
   const int i = threadIdx.x;
   if (i >= AIQ_N_SCALARS) return;
   int64_t v = 0;
   switch (i) {
     case AIQ_S_SELECTED: v = ctr[C_SEL]; break;
     case AIQ_S_KEPT: v = ctr[C_KEPT]; break;
-    case AIQ_S_TOKENS: v = ctr[C_TOK] + static_cast<int64_t>(tok_per_row) * ctr[C_SEL]; break;
+    case AIQ_S_TOKENS: v = ctr[C_TOK] + static_cast<int64_t>(tok_per_row) * ctr[seq_ctr]; break;
+    case AIQ_S_PAIRS: v = ctr[C_PAIRS]; break;
     case AIQ_S_STATUS: v = ctr[C_STATUS]; break;
     case AIQ_S_GROUPS: v = ctr[C_GROUPS]; break;
     default: v = 0;
@@ -803,8 +804,9 @@ __global__ void k_finalize(const int64_t* ctr, int64_t* scalars, int32_t tok_per
   scalars[i] = v;
 }
 
-hipError_t launch_finalize(const int64_t* ctr, int64_t* scalars, hipStream_t s, int32_t tok_per_row) {
-  hipLaunchKernelGGL(k_finalize, dim3(1), dim3(64), 0, s, ctr, scalars, tok_per_row);
+hipError_t launch_finalize(const int64_t* ctr, int64_t* scalars, hipStream_t s, int32_t tok_per_row,
+                           int32_t seq_ctr) {
+  hipLaunchKernelGGL(k_finalize, dim3(1), dim3(64), 0, s, ctr, scalars, tok_per_row, seq_ctr);
   return hipGetLastError();
 }
 

@@ -171,6 +171,10 @@ def make_query(query, probe: DeviceTable | None, build: DeviceTable | None, pref
     q.n_like = len(like)
     for i, t in enumerate(like):
         q.like[i] = int(t)
+    if getattr(query, "pair_key", None):
+        q.pairs = 1
+        q.pair_key_col = probe.index[query.pair_key]
+        q.max_pairs = int(query.max_pairs)
     return q
 
 
@@ -200,6 +204,8 @@ class DeviceQuery:
         n = self.probe.n_rows
         K = len(query.labels)
         dev = self.device
+        self.pairs = bool(getattr(query, "pair_key", None))
+        n = max(n, int(query.max_pairs)) if self.pairs else n   # outputs per row, or per pair
         self.scalars = torch.zeros(B.AIQ_N_SCALARS, dtype=torch.int64, device=dev)
         self.ids = torch.zeros(max(n, 1), dtype=torch.int32, device=dev)
         self.sel_ids = torch.zeros(max(n, 1), dtype=torch.int32, device=dev)
@@ -222,6 +228,13 @@ class DeviceQuery:
         o.grp_cap = G
         o.sum_out = _ptr(self.sum_out)
         o.sel_gen = _ptr(self.sel_gen) if self.gen else None
+        if self.pairs:
+            self.pair_a = torch.zeros(n, dtype=torch.int32, device=dev)
+            self.pair_b = torch.zeros(n, dtype=torch.int32, device=dev)
+            self.cand_a = torch.zeros(n, dtype=torch.int32, device=dev)
+            self.cand_b = torch.zeros(n, dtype=torch.int32, device=dev)
+            o.pair_a, o.pair_b, o.cand_a, o.cand_b = (_ptr(self.pair_a), _ptr(self.pair_b), _ptr(self.cand_a),
+                                                      _ptr(self.cand_b))
         self.out = o
 
     def run(self, trace=None, stream=None) -> None:
@@ -243,6 +256,15 @@ class DeviceQuery:
             r["sum"] = float(self.sum_out.cpu().item())
         if self.gen:
             r["gen"] = self.sel_gen[:n_sel * self.gen].cpu().numpy().astype(np.int64).reshape(n_sel, self.gen)
+        if self.pairs:   # labels / logits are per candidate pair; ids are kept pair numbers
+            P = int(sc[B.AIQ_S_PAIRS])
+            r.update(n_pairs=P, kept_pairs=r["kept_ids"],
+                     pair_a=self.pair_a[:n_kept].cpu().numpy().astype(np.int64),
+                     pair_b=self.pair_b[:n_kept].cpu().numpy().astype(np.int64),
+                     cand_a=self.cand_a[:P].cpu().numpy().astype(np.int64),
+                     cand_b=self.cand_b[:P].cpu().numpy().astype(np.int64),
+                     labels=self.sel_labels[:P].cpu().numpy().astype(np.int64),
+                     logits=self.sel_logits[:P * K].cpu().numpy().reshape(P, K))
         if self.query.agg in ("avg_label_count_by", "count_by_payload"):
             r["groups"] = (self.grp_key[:n_groups].cpu().numpy().astype(np.int64),
                            self.grp_count[:n_groups].cpu().numpy(), self.grp_sum[:n_groups].cpu().numpy(),

@@ -139,6 +139,7 @@ class Query:
     pad_id: int = 0
     like: Tuple[int, ...] = ()        # LIKE '%pattern%' over the generated token ids
     pair_key: Optional[str] = None    # Q4: classify pairs of selected rows with equal keys in this column
+    max_pairs: int = 0                # Q4: capacity for candidate pairs
 
 
 @dataclass(frozen=True)

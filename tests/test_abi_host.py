@@ -298,3 +298,36 @@ def test_transform_workspace_holds_the_generation_state():
     finally:
         for p in (plain, g16, g32):
             B.aiq_plan_destroy(p)
+
+
+def _pair_query(**kw):
+    q = query(pairs=1, pair_key_col=1, n_group_keys=100, max_pairs=5000)
+    for k, v in kw.items():
+        setattr(q, k, v)
+    return q
+
+
+def test_pairs_plan_validation():
+    ok = B.AIQ_OK
+    assert B.aiq_plan_create_status(model(), table(), None, _pair_query()) == ok
+    assert B.aiq_plan_create_status(model(), table(), None, _pair_query(pairs=2)) == B.AIQ_EINVAL
+    assert B.aiq_plan_create_status(model(), table(), None, _pair_query(pair_key_col=2)) == B.AIQ_EINVAL
+    assert B.aiq_plan_create_status(model(), table(), None, _pair_query(max_pairs=0)) == B.AIQ_EINVAL
+    assert B.aiq_plan_create_status(model(), table(), None, _pair_query(n_group_keys=0)) == B.AIQ_EINVAL
+    assert B.aiq_plan_create_status(model(), table(), None, _pair_query(n_group_keys=16385)) == B.AIQ_EUNSUPPORTED
+    assert B.aiq_plan_create_status(model(), table(), None,
+                                    _pair_query(decision=B.AIQ_DECIDE_ARGMAX)) == B.AIQ_EINVAL
+    assert B.aiq_plan_create_status(model(), table(), None, _pair_query(gen_tokens=4)) == B.AIQ_EINVAL
+    assert B.aiq_plan_create_status(model(), table(), None, _pair_query(),
+                                    _opts(B.AIQ_PLAN_RELATIONAL_ONLY)) == B.AIQ_EINVAL
+
+
+def test_pairs_workspace_follows_max_pairs():
+    small = B.aiq_plan_create(model(), table(), None, _pair_query(max_pairs=1000))
+    big = B.aiq_plan_create(model(), table(), None, _pair_query(max_pairs=2000))
+    try:
+        # 1000 more pairs of up to 2 x 512 tokens each, packed as int32
+        assert B.aiq_workspace_size(big) - B.aiq_workspace_size(small) >= 1000 * 1024 * 4
+    finally:
+        B.aiq_plan_destroy(small)
+        B.aiq_plan_destroy(big)
