@@ -430,6 +430,7 @@ def main(argv=None) -> int:
     w = WORKLOADS[a.workload]
     q = w.queries[a.query]
     gen = int(getattr(q, "gen_tokens", 0))
+    pairs = bool(getattr(q, "pair_key", None))
     spec = w.model
     log(f"[bench] generating {a.workload}: {w.description}")
     tables = make_tables(w)
@@ -447,7 +448,11 @@ def main(argv=None) -> int:
         raise RuntimeError(f"device status {res['status']:#x}")
     n_rows = len(tables["probe"]["id"])
     sel = res["sel_ids"]
-    own = tables["probe"]["len"][sel].astype(np.float64)
+    if pairs:   # the sequences are the candidate pairs: both rows' tokens
+        ltab = tables["probe"]["len"]
+        own = (ltab[res["cand_a"]] + ltab[res["cand_b"]]).astype(np.float64)
+    else:
+        own = tables["probe"]["len"][sel].astype(np.float64)
     lens = own + q.n_prefix
     T = int(lens.sum())
     assert T == res["n_tokens"]
@@ -544,7 +549,12 @@ def main(argv=None) -> int:
                                  for qq in w.queries]
         a.no_cpu_baseline = a.no_split = True   # the oracle and the split baseline classify; no generation
         result["cpu_baseline"] = None
-    if not a.no_relational_scale and not gen:
+    if pairs:
+        result["pairs"] = {"candidates": res["n_pairs"], "kept": res["count"],
+                           "pairs_per_s": round(res["n_pairs"] / (ms_step * 1e-3), 1)}
+        a.no_cpu_baseline = a.no_split = True   # both classify single rows
+        result["cpu_baseline"] = None
+    if not a.no_relational_scale and not gen and not pairs:
         result["relational_scale"] = relational_scale_leg(B, torch, [1 << 26], [10, 1000], steps=5)
     if not a.no_cpu_baseline:
         log("[bench] cpu baseline (oracle on a sample)")

@@ -214,6 +214,17 @@ WORKLOADS = {
         queries=(Query(preds=(), labels=(), decision="binary_gt", agg="count", n_prefix=12, gen_tokens=128,
                        eos_id=2, pad_id=0, like=(17, 17)),),
     ),
+    # classification of pairs of reviews of the same movie (Q4): a self-join on
+    # the movie id, AI_IF over both texts
+    "reviews_pairs": Workload(
+        name="reviews_pairs", description="Q4: AI_IF over pairs of reviews of the same movie among rows passing "
+                                          "values_a < 40, 16,384 rows, 4-layer d512 bf16 decoder",
+        table=TableSpec(n_rows=16384, seed=1, length=_LOGN_120, tokens=_ZIPF_TOK, rating=_RATING_P,
+                        values_a=(0.0, 100.0), movie_id=("zipf", 0.5, 4096)),
+        model=SMALL,
+        queries=(Query(preds=(Pred("values_a", "lt", 40.0),), labels=_BINARY, decision="binary_gt", agg="count",
+                       n_prefix=8, pair_key="movie_id", n_group_keys=4096, max_pairs=65536),),
+    ),
     "groupby1b": Workload(
         name="groupby1b", description="1B-class 5-way classify + GROUP BY movie_id, 131,072 rows",
         table=TableSpec(n_rows=131072, seed=2, length=_LOGN_120, tokens=_ZIPF_TOK, rating=_RATING_P,
