@@ -18,6 +18,8 @@
 #include "aiq_internal.h"
 #include "dev_util.h"
 
+#include <type_traits>
+
 namespace aiq {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -260,57 +262,65 @@ __device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4
     // rotary frequency of this lane's lower-half dim, in revolutions per position
     rev_per_pos = hh ? rev.y : rev.x;
   }
-  constexpr int COLS = EPI == EPI_SWIGLU ? 32 : 64;
+  // q / k columns (rotary) or v columns: chosen once per wave (a per-element
+  // choice costs exec-mask branches around every element)
+  auto emit = [&](auto rot_tag) {
+    constexpr bool ROT = decltype(rot_tag)::value;
 #pragma unroll
-  for (int h2 = 0; h2 < 2; ++h2) {
+    for (int h2 = 0; h2 < 2; ++h2) {
 #pragma unroll
-    for (int ii = 0; ii < 2; ++ii) {
-      const int i = h2 * 2 + ii;
+      for (int ii = 0; ii < 2; ++ii) {
+        const int i = h2 * 2 + ii;
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int tr = wm * 128 + i * 32 + g * 8 + hi * 4;   // tile row of e = 0
-        int4 p4 = make_int4(0, 0, 0, 0);
-        if (EPI == EPI_QKV_ROPE && !is_v)   // positions of the 4 rows e = 0..3
-          p4 = *reinterpret_cast<const int4*>(pl + tr);
-        const int pe[4] = {p4.x, p4.y, p4.z, p4.w};
-        float4 r4 = make_float4(1.f, 1.f, 1.f, 1.f);
-        if (a.rs) r4 = *reinterpret_cast<const float4*>(rl + tr);   // RMSNorm row scales
-        const float re[4] = {r4.x, r4.y, r4.z, r4.w};
+        for (int g = 0; g < 4; ++g) {
+          const int tr = wm * 128 + i * 32 + g * 8 + hi * 4;   // tile row of e = 0
+          int4 p4 = make_int4(0, 0, 0, 0);
+          if (EPI == EPI_QKV_ROPE && ROT)   // positions of the 4 rows e = 0..3
+            p4 = *reinterpret_cast<const int4*>(pl + tr);
+          const int pe[4] = {p4.x, p4.y, p4.z, p4.w};
+          float4 r4 = make_float4(1.f, 1.f, 1.f, 1.f);
+          if (a.rs) r4 = *reinterpret_cast<const float4*>(rl + tr);   // RMSNorm row scales
+          const float re[4] = {r4.x, r4.y, r4.z, r4.w};
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = ii * 32 + g * 8 + hi * 4 + e;   // row inside the 64-row slab
-          const float v0 = acc[i][0][4 * g + e] * re[e], v1 = acc[i][1][4 * g + e] * re[e];
-          if (EPI == EPI_SWIGLU) {
-            slice[r * 32 + l32] = Op16<H>::cvt(silu_fast(v0) * v1);
-          } else if (EPI == EPI_QKV_ROPE && !is_v) {
-            // angle pos * theta^(-2i/hd), in revolutions (hardware sin/cos take revolutions)
-            const float rev = static_cast<float>(pe[e]) * rev_per_pos;
-            const float frac = rev - floorf(rev);
-            const float cs = __builtin_amdgcn_cosf(frac), sn = __builtin_amdgcn_sinf(frac);
-            slice[r * 64 + l32] = f2h(v0 * cs - v1 * sn);        // lower half dims
-            slice[r * 64 + 32 + l32] = f2h(v1 * cs + v0 * sn);   // upper half dims
-          } else if (EPI == EPI_QKV_ROPE) {   // v
-            slice[r * 64 + l32] = f2h(v0);
-            slice[r * 64 + 32 + l32] = f2h(v1);
-          } else {
-            slice[r * 64 + l32] = Op16<H>::cvt(v0);
-            slice[r * 64 + 32 + l32] = Op16<H>::cvt(v1);
+          for (int e = 0; e < 4; ++e) {
+            const int r = ii * 32 + g * 8 + hi * 4 + e;   // row inside the 64-row slab
+            const float v0 = acc[i][0][4 * g + e] * re[e], v1 = acc[i][1][4 * g + e] * re[e];
+            if (EPI == EPI_SWIGLU) {
+              slice[r * 32 + l32] = Op16<H>::cvt(silu_fast(v0) * v1);
+            } else if (EPI == EPI_QKV_ROPE && ROT) {
+              // angle pos * theta^(-2i/hd), in revolutions (hardware sin/cos take revolutions)
+              const float rev = static_cast<float>(pe[e]) * rev_per_pos;
+              const float frac = rev - floorf(rev);
+              const float cs = __builtin_amdgcn_cosf(frac), sn = __builtin_amdgcn_sinf(frac);
+              slice[r * 64 + l32] = f2h(v0 * cs - v1 * sn);        // lower half dims
+              slice[r * 64 + 32 + l32] = f2h(v1 * cs + v0 * sn);   // upper half dims
+            } else if (EPI == EPI_QKV_ROPE && !ROT) {   // v
+              slice[r * 64 + l32] = f2h(v0);
+              slice[r * 64 + 32 + l32] = f2h(v1);
+            } else {
+              slice[r * 64 + l32] = Op16<H>::cvt(v0);
+              slice[r * 64 + 32 + l32] = Op16<H>::cvt(v1);
+            }
           }
         }
       }
+      const int64_t m_first = mw + h2 * 64;
+      if (EPI == EPI_SWIGLU) {
+        flush_slab<uint16_t>(slice, 64, 32, C, a.ldc, m_first, M, lane, [&](int c) { return nw / 2 + c; });
+      } else if (EPI == EPI_QKV_ROPE && ROT) {
+        // slab columns 0..31: lower-half dims hh*32.., 32..63: the matching upper-half dims
+        const int base = sbase + head * a.hd + hh * 32;
+        flush_slab<uint16_t>(slice, 64, 64, C, a.ldc, m_first, M, lane,
+                             [&](int c) { return base + (c < 32 ? c : half + c - 32); });
+      } else {
+        flush_slab<uint16_t>(slice, 64, 64, C, a.ldc, m_first, M, lane, [&](int c) { return nw + c; });
+      }
     }
-    const int64_t m_first = mw + h2 * 64;
-    if (EPI == EPI_SWIGLU) {
-      flush_slab<uint16_t>(slice, 64, 32, C, a.ldc, m_first, M, lane, [&](int c) { return nw / 2 + c; });
-    } else if (EPI == EPI_QKV_ROPE && !is_v) {
-      // slab columns 0..31: lower-half dims hh*32.., 32..63: the matching upper-half dims
-      const int base = sbase + head * a.hd + hh * 32;
-      flush_slab<uint16_t>(slice, 64, 64, C, a.ldc, m_first, M, lane,
-                           [&](int c) { return base + (c < 32 ? c : half + c - 32); });
-    } else {
-      flush_slab<uint16_t>(slice, 64, 64, C, a.ldc, m_first, M, lane, [&](int c) { return nw + c; });
-    }
-  }
+  };
+  if (EPI == EPI_QKV_ROPE && !is_v)
+    emit(std::true_type{});
+  else
+    emit(std::false_type{});
 }
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
