@@ -240,7 +240,7 @@ Layout run_layout(const aiq_plan* p) {
     L.kvc = c.take(static_cast<size_t>(p->n_layers) * p->t_cap * p->n_qkv * ab);
     L.gkv = c.take(static_cast<size_t>(p->n_layers) * su * G * 2 * p->d_kv * ab);
     L.hf = c.take(su * d * ab);
-    L.glog = c.take(std::min<size_t>(su, GEN_HEAD_ROWS) * p->model.vocab * 4);
+    L.glog = c.take(std::min<size_t>(su, GEN_HEAD_ROWS) * (p->model.vocab / 64) * 8);   // per-64-column maxima
     L.gtok = c.take(su * 4);
     L.gdone = c.take(su * 4);
     L.gen = c.take(static_cast<size_t>(n + 1) * G * 4);
@@ -544,9 +544,9 @@ aiq_status enqueue_generation(const aiq_plan* p, void* ws, const Layout& L, cons
   auto next_tokens = [&](int step) -> aiq_status {
     for (int b = 0; b < p->gen_blocks; ++b) {
       const int64_t row0 = static_cast<int64_t>(b) * GEN_HEAD_ROWS;
-      TRACED(tr, AIQ_K_DECODE_HEAD, gemm(EPI_STORE_F32, static_cast<const char*>(hf) + row0 * d * ab, d, cnt + b,
-                                    std::min<int64_t>(su - row0, GEN_HEAD_ROWS), m.vocab, d, m.lm_head, nullptr,
-                                    nullptr, logits, m.vocab, nullptr, false));
+      TRACED(tr, AIQ_K_DECODE_HEAD, gemm(EPI_ARGMAX, static_cast<const char*>(hf) + row0 * d * ab, d, cnt + b,
+                                         std::min<int64_t>(su - row0, GEN_HEAD_ROWS), m.vocab, d, m.lm_head,
+                                         nullptr, nullptr, logits, m.vocab / 64, nullptr, false));
       TRACED(tr, AIQ_K_DECODE_HEAD, launch_gen_argmax(logits, m.vocab, cnt + b, row0, gd, step, G, q.eos_id, q.pad_id,
                                                  tok, done, gen, s));
     }

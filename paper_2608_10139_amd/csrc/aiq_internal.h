@@ -166,7 +166,12 @@ hipError_t launch_row_scale(const int64_t* desc, const float* ssp, int32_t n_par
 hipError_t launch_rmsnorm(const int64_t* desc, float* x, const float* delta, const float* g, int32_t d,
                           float eps, void* out, int32_t out_act, int64_t t_cap, hipStream_t s);
 
-enum Epi : int { EPI_STORE_F32 = 0, EPI_QKV_ROPE = 1, EPI_SWIGLU = 3, EPI_GELU = 4, EPI_STORE_ACT = 5, EPI_RESID = 6 };
+// EPI_ARGMAX (MFMA path): no output matrix; C = int2 [M][N / 64] of
+// (fp32 bits of the maximum, its column) over each 64-column slice of a row,
+// the lowest column among equal maxima.
+enum Epi : int {
+  EPI_STORE_F32 = 0, EPI_QKV_ROPE = 1, EPI_SWIGLU = 3, EPI_GELU = 4, EPI_STORE_ACT = 5, EPI_RESID = 6, EPI_ARGMAX = 7
+};
 
 struct GemmArgs {
   const void* A;             // [M, K] activations (bf16 or f32), row stride lda
@@ -322,10 +327,11 @@ hipError_t launch_attention_gen(const GenAttnArgs& a, hipStream_t s);
 // hf[i] = x[i] / rms * g in 16 bits, i < gen_desc[D_NSEQ]
 hipError_t launch_norm_rows(const int64_t* gen_desc, const float* x, const float* g, int32_t d, float eps, void* hf,
                             int32_t act, int64_t seq_ub, hipStream_t s);
-// Argmax over a block of full-vocabulary logits rows (ties to the lowest id):
+// Argmax over a block of full-vocabulary rows given as the head GEMM's
+// EPI_ARGMAX partials (int2 [rows][vocab / 64]; ties to the lowest id):
 // row r is sequence i = row0 + r; its token goes to gen[(seq_begin + i) * G +
 // step] (pad_id once the sequence has ended), tok[i] and done[i].
-hipError_t launch_gen_argmax(const float* logits, int32_t vocab, const int64_t* cnt, int64_t row0,
+hipError_t launch_gen_argmax(const void* part, int32_t vocab, const int64_t* cnt, int64_t row0,
                              const int64_t* gen_desc, int32_t step, int32_t G, int32_t eos, int32_t pad,
                              int32_t* tok, int32_t* done, int32_t* gen, hipStream_t s);
 struct LikePattern {

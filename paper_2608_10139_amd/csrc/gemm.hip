@@ -230,6 +230,39 @@ __device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4
     return;
   }
   prefetch();
+  if (EPI == EPI_ARGMAX) {
+    // row maxima over this wave's 64 columns: a row's values sit in the 32
+    // lanes of one half-wave (column lane % 32, two 32-column blocks j); the
+    // lanes meet in a butterfly that keeps the lower column on ties
+    int2* P = static_cast<int2*>(a.C);
+    const int chunk = nw >> 6;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float v = acc[i][0][4 * g + e];
+          int c = nw + l32;
+          const float v1 = acc[i][1][4 * g + e];
+          if (v1 > v) {   // column + 32 only if strictly greater
+            v = v1;
+            c += 32;
+          }
+#pragma unroll
+          for (int o = 1; o < 32; o <<= 1) {
+            const float ov = __shfl_xor(v, o);
+            const int oc = __shfl_xor(c, o);
+            if (ov > v || (ov == v && oc < c)) {
+              v = ov;
+              c = oc;
+            }
+          }
+          const int64_t m = mw + i * 32 + 8 * g + 4 * hi + e;
+          if (l32 == 0 && m < M) P[m * a.ldc + chunk] = make_int2(__float_as_int(v), c);
+        }
+    return;
+  }
   if (EPI == EPI_STORE_F32) {
     // fp32: four slabs of 32 rows x 64 columns (8 KB each)
     float* slab = reinterpret_cast<float*>(slice);
@@ -520,6 +553,10 @@ hipError_t launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t s) {
   } while (0)
   switch (epi) {
     case EPI_STORE_F32: AIQ_LAUNCH_GEMM(EPI_STORE_F32); break;
+    case EPI_ARGMAX:
+      if (a.ldc != a.N / 64) return hipErrorInvalidValue;
+      AIQ_LAUNCH_GEMM(EPI_ARGMAX);
+      break;
     case EPI_STORE_ACT: AIQ_LAUNCH_GEMM(EPI_STORE_ACT); break;
     case EPI_SWIGLU: AIQ_LAUNCH_GEMM(EPI_SWIGLU); break;
     case EPI_QKV_ROPE: AIQ_LAUNCH_GEMM(EPI_QKV_ROPE); break;

@@ -5,7 +5,8 @@
 // A generation step runs one row per sequence of the chunk through the same
 // projections as the prefill (M = number of sequences), a decode attention
 // kernel over the sequence's kept keys and values, and the full-vocabulary
-// head as a GEMM into fp32 logits followed by a row argmax.  Keys and values
+// head as a GEMM whose epilogue keeps only each row's maximum per 64 columns,
+// followed by a row argmax over those.  Keys and values
 // of the prompt stay where the prefill put them (the chunk's per-layer q|k|v
 // rows, plus the shared prefix's rows); those of generated tokens go to a
 // per-layer cache [sequence][step][2 d_kv].  Everything runs on the launch
@@ -342,7 +343,10 @@ hipError_t launch_norm_rows(const int64_t* gen_desc, const float* x, const float
 }
 
 // ------------------------------------------------------------------ argmax of the next token
-__global__ __launch_bounds__(256) void k_gen_argmax(const float* logits, int32_t vocab, const int64_t* cnt,
+// The head GEMM leaves, per row, the maximum and its column over every 64
+// columns (lowest column on ties); a wave per row picks the largest, again
+// the lowest column among equals, and records the token.
+__global__ __launch_bounds__(256) void k_gen_argmax(const int2* part, int32_t n_chunk, const int64_t* cnt,
                                                     int64_t row0, const int64_t* gd, int32_t step, int32_t G,
                                                     int32_t eos, int32_t pad, int32_t* tok, int32_t* done,
                                                     int32_t* gen) {
@@ -351,14 +355,15 @@ __global__ __launch_bounds__(256) void k_gen_argmax(const float* logits, int32_t
   const int64_t wave = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6;
   const int64_t n_waves = ((int64_t)gridDim.x * blockDim.x) >> 6;
   for (int64_t r = wave; r < rows; r += n_waves) {
-    const float* lr = logits + r * vocab;
+    const int2* pr = part + r * n_chunk;
     float best = -INFINITY;
     int32_t bi = INT32_MAX;
-    for (int c = lane; c < vocab; c += 64) {   // ascending ids: strict > keeps each lane's first maximum
-      const float v = lr[c];
+    for (int c = lane; c < n_chunk; c += 64) {   // ascending columns: strict > keeps each lane's first maximum
+      const int2 p = pr[c];
+      const float v = __int_as_float(p.x);
       if (v > best) {
         best = v;
-        bi = c;
+        bi = p.y;
       }
     }
 #pragma unroll
@@ -381,11 +386,13 @@ __global__ __launch_bounds__(256) void k_gen_argmax(const float* logits, int32_t
   }
 }
 
-hipError_t launch_gen_argmax(const float* logits, int32_t vocab, const int64_t* cnt, int64_t row0,
+hipError_t launch_gen_argmax(const void* part, int32_t vocab, const int64_t* cnt, int64_t row0,
                              const int64_t* gen_desc, int32_t step, int32_t G, int32_t eos, int32_t pad,
                              int32_t* tok, int32_t* done, int32_t* gen, hipStream_t s) {
-  hipLaunchKernelGGL(k_gen_argmax, dim3(grid_for(GEN_HEAD_ROWS, 4, 1024)), dim3(256), 0, s, logits, vocab, cnt,
-                     row0, gen_desc, step, G, eos, pad, tok, done, gen);
+  if (vocab % 64) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_gen_argmax, dim3(grid_for(GEN_HEAD_ROWS, 4, 1024)), dim3(256), 0, s,
+                     static_cast<const int2*>(part), vocab / 64, cnt, row0, gen_desc, step, G, eos, pad, tok, done,
+                     gen);
   return hipGetLastError();
 }
 

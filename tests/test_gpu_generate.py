@@ -163,3 +163,27 @@ def test_generation_chunking_and_repeat_bitwise():
     np.testing.assert_array_equal(one["gen"], many["gen"])
     np.testing.assert_array_equal(one["gen"], again["gen"])
     np.testing.assert_array_equal(one["kept_ids"], many["kept_ids"])
+
+
+def test_first_token_is_the_argmax_of_the_full_vocabulary_logits():
+    """The generation head keeps only per-64-column maxima; its first token
+    must equal the argmax (lowest id on ties) of the full fp32 logits that
+    the prefill-only entry point writes for the same prompts."""
+    from paper_2608_10139_amd.device import DevicePrefill
+    say("case: first generated token vs full-vocabulary logits")
+    m, dm = model("hd64")
+    t = tables(200, 59)
+    q = query(3)
+    r = run(t, m, dm, q)
+    rows, _ = relational(t, q)
+    off, tok = t["probe"]["offsets"], t["probe"]["tokens"]
+    seqs = [tok[off[x]:off[x + 1]] for x in rows]
+    cu = np.zeros(len(seqs) + 1, dtype=np.int32)
+    cu[1:] = np.cumsum([len(s) for s in seqs])
+    pf = DevicePrefill(m, max_tokens=int(cu[-1]), dmodel=dm)
+    lg = pf.run(torch.from_numpy(np.concatenate(seqs).astype(np.int32)).cuda(), torch.from_numpy(cu).cuda(),
+                full_vocab=True)
+    torch.cuda.synchronize()
+    lg = lg.cpu().numpy()
+    pf.close()
+    np.testing.assert_array_equal(r["gen"][:, 0], lg.argmax(axis=1))
