@@ -29,6 +29,7 @@ namespace aiq {
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
 
 static int grid_cap(int64_t items, int cap) {
   int64_t g = items;
@@ -43,6 +44,7 @@ template <int HD>
 __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   constexpr int KB = 64;            // keys per block
   constexpr int CH = HD / 8;        // 16-byte chunks per K row
+  constexpr int PER = KB * CH / 256;   // chunks of K (and of V) per thread per block
   __shared__ __attribute__((aligned(16))) uint16_t Ks[KB * HD];
   __shared__ __attribute__((aligned(16))) uint16_t Vt[HD * KB];
 
@@ -51,158 +53,208 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   const int t = threadIdx.x, lane = t & 63, w = t >> 6, g = lane >> 4, c16 = lane & 15;
   const int rep = a.n_heads / a.n_kv;
   const int d_q = a.n_heads * HD, d_kv = a.n_kv * HD;
+  const int np = a.npre;
   const float scale = 1.4426950408889634f / sqrtf(static_cast<float>(HD));   // log2(e) / sqrt(hd)
   const uint16_t* qkv = static_cast<const uint16_t*>(a.qkv);
   const uint16_t* pkv = static_cast<const uint16_t*>(a.pkv);
   uint16_t* out = static_cast<uint16_t*>(a.out);
 
-  for (int64_t item = blockIdx.x; item < n_items; item += gridDim.x) {
-    const int64_t si = item / a.n_heads;
-    const int h = static_cast<int>(item % a.n_heads);
-    const int kvh = h / rep;
-    const int64_t s0 = a.cu[sb + si] - tb;
-    const int np = a.npre;
-    const int Lo = static_cast<int>(a.cu[sb + si + 1] - a.cu[sb + si]);   // own rows
-    if (Lo == 0) continue;
-    const int L = Lo + np;   // positions 0 .. L-1, the first np in pkv
-    const int qcol = h * HD, kcol = d_q + kvh * HD, vcol = d_q + d_kv + kvh * HD;
-    // row of position p: the prefix's rows, then the sequence's own rows
-    auto row_of = [&](int p) { return p < np ? pkv + static_cast<int64_t>(p) * a.ld : qkv + (s0 + p - np) * a.ld; };
-
-    for (int qb = np / KB; qb * KB < L; ++qb) {
-      const int qi = qb * KB + w * 16 + c16;   // this lane's query position (column of S^T)
-      const bool q_own = qi >= np && qi < L;
-      half8 qf[HD / 32];
-#pragma unroll
-      for (int kc = 0; kc < HD / 32; ++kc) {
-        if (q_own)
-          qf[kc] = *reinterpret_cast<const half8*>(qkv + (s0 + qi - np) * a.ld + qcol + kc * 32 + g * 8);
-        else
-          qf[kc] = half8{};
+  // A task is one 64-query block of one (sequence, head) item.  The first
+  // key block and the queries of the next task are read while the last key
+  // block of the current one is consumed.
+  struct Task {
+    int64_t item, s0;   // item, first packed row of the sequence's own rows
+    int L, qb, h;       // positions (prefix + own), query block, query head
+  };
+  // first task of the first item at or after `item` that has own rows
+  auto item_task = [&](int64_t item, Task& tk) -> bool {
+    for (; item < n_items; item += gridDim.x) {
+      const int64_t si = item / a.n_heads;
+      const int64_t c0 = a.cu[sb + si], c1 = a.cu[sb + si + 1];
+      if (c1 > c0) {
+        tk.item = item;
+        tk.s0 = c0 - tb;
+        tk.L = static_cast<int>(c1 - c0) + np;
+        tk.qb = np / KB;
+        tk.h = static_cast<int>(item % a.n_heads);
+        return true;
       }
-      f32x4 o[HD / 16];
+    }
+    return false;
+  };
+  auto advance = [&](const Task& c, Task& n) -> bool {
+    if ((c.qb + 1) * KB < c.L) {
+      n = c;
+      n.qb = c.qb + 1;
+      return true;
+    }
+    return item_task(c.item + gridDim.x, n);
+  };
+  // row of position p: the prefix's rows, then the sequence's own rows
+  auto row_of = [&](const Task& tk, int p) {
+    return p < np ? pkv + static_cast<int64_t>(p) * a.ld : qkv + (tk.s0 + p - np) * a.ld;
+  };
+  // this thread's K and V chunks of key block kb (zeros past L)
+  uint4 kr[PER], vr[PER];
+  auto fetch = [&](const Task& tk, int kb) {
+    const int kvh = tk.h / rep;
+    const int kcol = d_q + kvh * HD, vcol = d_q + d_kv + kvh * HD;
 #pragma unroll
-      for (int db = 0; db < HD / 16; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
-      float m_run = -INFINITY, l_run = 0.f;
+    for (int u = 0; u < PER; ++u) {
+      const int id = t + u * 256, r = id / CH, ch = id % CH;
+      const int kk = kb * KB + r;
+      kr[u] = make_uint4(0, 0, 0, 0);
+      vr[u] = make_uint4(0, 0, 0, 0);
+      if (kk < tk.L) {
+        const uint16_t* row = row_of(tk, kk);
+        kr[u] = *reinterpret_cast<const uint4*>(row + kcol + ch * 8);
+        vr[u] = *reinterpret_cast<const uint4*>(row + vcol + ch * 8);
+      }
+    }
+  };
+  // this lane's query (column of S^T): 8 dims per 32-dim chunk, zeros unless own
+  auto load_q = [&](const Task& tk, half8 (&qf)[HD / 32]) {
+    const int qi = tk.qb * KB + w * 16 + c16;
+    const bool own = qi >= np && qi < tk.L;
+#pragma unroll
+    for (int kc = 0; kc < HD / 32; ++kc) {
+      if (own)
+        qf[kc] = *reinterpret_cast<const half8*>(qkv + (tk.s0 + qi - np) * a.ld + tk.h * HD + kc * 32 + g * 8);
+      else
+        qf[kc] = half8{};
+    }
+  };
 
-      // this thread's K and V chunks of a key block (zeros past L); the next
-      // block's are read into registers while the current block is consumed
-      constexpr int PER = KB * CH / 256;
-      uint4 kr[PER], vr[PER];
-      auto fetch = [&](int kb) {
+  Task cur;
+  if (!item_task(blockIdx.x, cur)) return;
+  half8 qf[HD / 32];
+  load_q(cur, qf);
+  fetch(cur, 0);
+  half8 ones;
 #pragma unroll
-        for (int u = 0; u < PER; ++u) {
-          const int id = t + u * 256, r = id / CH, ch = id % CH;
-          const int kk = kb * KB + r;
-          kr[u] = make_uint4(0, 0, 0, 0);
-          vr[u] = make_uint4(0, 0, 0, 0);
-          if (kk < L) {
-            const uint16_t* row = row_of(kk);
-            kr[u] = *reinterpret_cast<const uint4*>(row + kcol + ch * 8);
-            vr[u] = *reinterpret_cast<const uint4*>(row + vcol + ch * 8);
-          }
-        }
-      };
-      fetch(0);
-      for (int kb = 0; kb <= qb; ++kb) {
-        __syncthreads();   // previous key block fully consumed
-#pragma unroll
-        for (int u = 0; u < PER; ++u) {
-          const int id = t + u * 256, r = id / CH, ch = id % CH;
-          *reinterpret_cast<uint4*>(Ks + r * HD + ((ch ^ (r & 7)) << 3)) = kr[u];
-          const uint32_t vw[4] = {vr[u].x, vr[u].y, vr[u].z, vr[u].w};
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const int dim = ch * 8 + j;
-            const uint16_t e = static_cast<uint16_t>(vw[j >> 1] >> ((j & 1) * 16));
-            Vt[dim * KB + ((((r >> 2) ^ (dim & 15)) << 2) | (r & 3))] = e;
-          }
-        }
-        __syncthreads();
-        if (kb < qb) fetch(kb + 1);
+  for (int i = 0; i < 8; ++i) ones[i] = static_cast<_Float16>(1.0f);
 
-        // S^T block j: keys 16j.., lane holds keys 16j + 4g + e for query c16
-        f32x4 sacc[4];
+  for (;;) {
+    const int qb = cur.qb, L = cur.L;
+    const int qi = qb * KB + w * 16 + c16;
+    f32x4 o[HD / 16];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          sacc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-          const int krow = j * 16 + c16;
+    for (int db = 0; db < HD / 16; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // softmax denominator: the P V product against a block of ones, so it
+    // sums exactly the fp16 probabilities the numerator uses
+    f32x4 ol = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m_run = -INFINITY;   // running maximum of the scaled scores
+    Task nxt;
+    bool has_next = false;
+    half8 qn[HD / 32];
+
+    for (int kb = 0; kb <= qb; ++kb) {
+      __syncthreads();   // previous key block fully consumed
 #pragma unroll
-          for (int kc = 0; kc < HD / 32; ++kc) {
-            const half8 kf = *reinterpret_cast<const half8*>(Ks + krow * HD + (((kc * 4 + g) ^ (krow & 7)) << 3));
-            sacc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf, qf[kc], sacc[j], 0, 0, 0);
-          }
+      for (int u = 0; u < PER; ++u) {
+        const int id = t + u * 256, r = id / CH, ch = id % CH;
+        *reinterpret_cast<uint4*>(Ks + r * HD + ((ch ^ (r & 7)) << 3)) = kr[u];
+        const uint32_t vw[4] = {vr[u].x, vr[u].y, vr[u].z, vr[u].w};
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int dim = ch * 8 + j;
+          const uint16_t e = static_cast<uint16_t>(vw[j >> 1] >> ((j & 1) * 16));
+          Vt[dim * KB + ((((r >> 2) ^ (dim & 15)) << 2) | (r & 3))] = e;
         }
-        float mx = -INFINITY;
-        float sv[16];
+      }
+      __syncthreads();
+      if (kb < qb) {
+        fetch(cur, kb + 1);
+      } else {
+        has_next = advance(cur, nxt);
+        if (has_next) {
+          fetch(nxt, 0);
+          load_q(nxt, qn);
+        }
+      }
+
+      // S^T block j: keys 16j.., lane holds keys 16j + 4g + e for query c16
+      f32x4 sacc[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        sacc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        const int krow = j * 16 + c16;
+#pragma unroll
+        for (int kc = 0; kc < HD / 32; ++kc) {
+          const half8 kf = *reinterpret_cast<const half8*>(Ks + krow * HD + (((kc * 4 + g) ^ (krow & 7)) << 3));
+          sacc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf, qf[kc], sacc[j], 0, 0, 0);
+        }
+      }
+      // Only the diagonal block has keys after some query or past the end
+      // (every key of an earlier block precedes every query of this one).
+      if (kb == qb) {
 #pragma unroll
         for (int j = 0; j < 4; ++j)
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const int key = kb * KB + j * 16 + 4 * g + e;
-            const bool valid = key <= qi && key < L;
-            const float s = valid ? sacc[j][e] * scale : -INFINITY;
-            sv[j * 4 + e] = s;
-            mx = fmaxf(mx, s);
+            if (!(key <= qi && key < L)) sacc[j][e] = -INFINITY;
           }
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m_run, mx);
-        const float alpha = (m_new == -INFINITY) ? 1.f : exp2f(m_run - m_new);
-        float psum = 0.f;
-        uint16_t ph[16];   // fp16 probabilities fed to the P V product
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const float pf = (m_new == -INFINITY || sv[i] == -INFINITY) ? 0.f : exp2f(sv[i] - m_new);
-          ph[i] = f2h(pf);
-          psum += h2f(ph[i]);
-        }
-        l_run = l_run * alpha + psum;
-        m_run = m_new;
-#pragma unroll
-        for (int db = 0; db < HD / 16; ++db) o[db] *= alpha;
-
-        // O^T += V^T P^T over two 32-key halves
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          half8 pb;
-          {
-            uint16_t tmp[8];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              tmp[e] = ph[(2 * u) * 4 + e];
-              tmp[4 + e] = ph[(2 * u + 1) * 4 + e];
-            }
-            pb = *reinterpret_cast<const half8*>(tmp);
-          }
-#pragma unroll
-          for (int db = 0; db < HD / 16; ++db) {
-            const int dim = db * 16 + c16;
-            const uint16_t* vrow = Vt + dim * KB;
-            const uint2 lo = *reinterpret_cast<const uint2*>(vrow + (((8 * u + g) ^ (dim & 15)) << 2));
-            const uint2 hi = *reinterpret_cast<const uint2*>(vrow + (((8 * u + 4 + g) ^ (dim & 15)) << 2));
-            const uint4 vv = make_uint4(lo.x, lo.y, hi.x, hi.y);
-            const half8 vf = *reinterpret_cast<const half8*>(&vv);
-            o[db] = __builtin_amdgcn_mfma_f32_16x16x32_f16(vf, pb, o[db], 0, 0, 0);
-          }
-        }
       }
-      float l_tot = l_run;
-      l_tot += __shfl_xor(l_tot, 16);
-      l_tot += __shfl_xor(l_tot, 32);
-      if (q_own) {
-        const float inv = 1.0f / l_tot;
-        uint16_t* orow = out + (s0 + qi - np) * a.ldo + h * HD;
+      float mx = sacc[0][0];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) mx = fmaxf(mx, sacc[j][e]);
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      // scale > 0, so the maximum of the scaled scores is the scaled maximum;
+      // it is finite: each block holds a key at or before every query
+      const float m_new = fmaxf(m_run, mx * scale);
+      const float alpha = exp2f(m_run - m_new);   // 0 on the first block
+      m_run = m_new;
+      half8 pb[2];   // fp16 probabilities of keys 32u + {4g + e, 16 + 4g + e}
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        f32x8 pf;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          pf[e] = exp2f(fmaf(sacc[2 * u][e], scale, -m_new));
+          pf[4 + e] = exp2f(fmaf(sacc[2 * u + 1][e], scale, -m_new));
+        }
+        pb[u] = __builtin_convertvector(pf, half8);
+      }
+#pragma unroll
+      for (int db = 0; db < HD / 16; ++db) o[db] *= alpha;
+      ol *= alpha;
+
+      // O^T += V^T P^T over two 32-key halves
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
 #pragma unroll
         for (int db = 0; db < HD / 16; ++db) {
-          const f32x4 v = o[db];
-          uint2 pk;
-          pk.x = f2act(v[0] * inv, a.out_act) | (static_cast<uint32_t>(f2act(v[1] * inv, a.out_act)) << 16);
-          pk.y = f2act(v[2] * inv, a.out_act) | (static_cast<uint32_t>(f2act(v[3] * inv, a.out_act)) << 16);
-          *reinterpret_cast<uint2*>(orow + db * 16 + 4 * g) = pk;
+          const int dim = db * 16 + c16;
+          const uint16_t* vrow = Vt + dim * KB;
+          const uint2 lo = *reinterpret_cast<const uint2*>(vrow + (((8 * u + g) ^ (dim & 15)) << 2));
+          const uint2 hi = *reinterpret_cast<const uint2*>(vrow + (((8 * u + 4 + g) ^ (dim & 15)) << 2));
+          const uint4 vv = make_uint4(lo.x, lo.y, hi.x, hi.y);
+          const half8 vf = *reinterpret_cast<const half8*>(&vv);
+          o[db] = __builtin_amdgcn_mfma_f32_16x16x32_f16(vf, pb[u], o[db], 0, 0, 0);
         }
+        ol = __builtin_amdgcn_mfma_f32_16x16x32_f16(ones, pb[u], ol, 0, 0, 0);
       }
     }
+    if (qi >= np && qi < L) {
+      const float inv = 1.0f / ol[0];
+      uint16_t* orow = out + (cur.s0 + qi - np) * a.ldo + cur.h * HD;
+#pragma unroll
+      for (int db = 0; db < HD / 16; ++db) {
+        const f32x4 v = o[db];
+        uint2 pk;
+        pk.x = f2act(v[0] * inv, a.out_act) | (static_cast<uint32_t>(f2act(v[1] * inv, a.out_act)) << 16);
+        pk.y = f2act(v[2] * inv, a.out_act) | (static_cast<uint32_t>(f2act(v[3] * inv, a.out_act)) << 16);
+        *reinterpret_cast<uint2*>(orow + db * 16 + 4 * g) = pk;
+      }
+    }
+    if (!has_next) break;
+    cur = nxt;
+#pragma unroll
+    for (int kc = 0; kc < HD / 32; ++kc) qf[kc] = qn[kc];
   }
 }
 
