@@ -31,6 +31,14 @@ CXXFLAGS = [
 ]
 
 
+# Per-source additions.  attn.hip: MFMA accumulators in ordinary VGPRs, so the
+# online-softmax rescale of the output accumulators needs no copies between
+# register files (and the 128-dim kernel fits two waves per SIMD).
+EXTRA_FLAGS = {
+    "attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+}
+
+
 def hipcc() -> str:
     for c in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
         if c and os.path.exists(c):
@@ -40,7 +48,7 @@ def hipcc() -> str:
 
 def _compile(src: str, verbose: bool) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [hipcc(), *CXXFLAGS, "-c", src, "-o", obj]
+    cmd = [hipcc(), *CXXFLAGS, *EXTRA_FLAGS.get(os.path.basename(src), []), "-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -25,6 +25,8 @@
 #include "aiq_internal.h"
 #include "dev_util.h"
 
+#include <type_traits>
+
 namespace aiq {
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
@@ -69,14 +71,14 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   // first task of the first item at or after `item` that has own rows
   auto item_task = [&](int64_t item, Task& tk) -> bool {
     for (; item < n_items; item += gridDim.x) {
-      const int64_t si = item / a.n_heads;
+      const int64_t si = static_cast<int32_t>(item) / a.n_heads;   // items < 2^31 (checked at launch)
       const int64_t c0 = a.cu[sb + si], c1 = a.cu[sb + si + 1];
       if (c1 > c0) {
         tk.item = item;
         tk.s0 = c0 - tb;
         tk.L = static_cast<int>(c1 - c0) + np;
         tk.qb = np / KB;
-        tk.h = static_cast<int>(item % a.n_heads);
+        tk.h = static_cast<int>(item - si * a.n_heads);
         return true;
       }
     }
@@ -206,7 +208,9 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
       // scale > 0, so the maximum of the scaled scores is the scaled maximum;
       // it is finite: each block holds a key at or before every query
       const float m_new = fmaxf(m_run, mx * scale);
-      const float alpha = exp2f(m_run - m_new);   // 0 on the first block
+      // v_exp_f32: results below 2^-126 flush to zero, far below the fp16
+      // probabilities they feed
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);   // 0 on the first block
       m_run = m_new;
       half8 pb[2];   // fp16 probabilities of keys 32u + {4g + e, 16 + 4g + e}
 #pragma unroll
@@ -214,8 +218,8 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
         f32x8 pf;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          pf[e] = exp2f(fmaf(sacc[2 * u][e], scale, -m_new));
-          pf[4 + e] = exp2f(fmaf(sacc[2 * u + 1][e], scale, -m_new));
+          pf[e] = __builtin_amdgcn_exp2f(fmaf(sacc[2 * u][e], scale, -m_new));
+          pf[4 + e] = __builtin_amdgcn_exp2f(fmaf(sacc[2 * u + 1][e], scale, -m_new));
         }
         pb[u] = __builtin_convertvector(pf, half8);
       }
@@ -242,14 +246,23 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
     if (qi >= np && qi < L) {
       const float inv = 1.0f / ol[0];
       uint16_t* orow = out + (cur.s0 + qi - np) * a.ldo + cur.h * HD;
+      // output type chosen once, not per element
+      auto store = [&](auto f16_tag) {
+        constexpr bool F16 = decltype(f16_tag)::value;
+        auto cv = [](float f) { return F16 ? f2h(f) : f2bf(f); };
 #pragma unroll
-      for (int db = 0; db < HD / 16; ++db) {
-        const f32x4 v = o[db];
-        uint2 pk;
-        pk.x = f2act(v[0] * inv, a.out_act) | (static_cast<uint32_t>(f2act(v[1] * inv, a.out_act)) << 16);
-        pk.y = f2act(v[2] * inv, a.out_act) | (static_cast<uint32_t>(f2act(v[3] * inv, a.out_act)) << 16);
-        *reinterpret_cast<uint2*>(orow + db * 16 + 4 * g) = pk;
-      }
+        for (int db = 0; db < HD / 16; ++db) {
+          const f32x4 v = o[db];
+          uint2 pk;
+          pk.x = cv(v[0] * inv) | (static_cast<uint32_t>(cv(v[1] * inv)) << 16);
+          pk.y = cv(v[2] * inv) | (static_cast<uint32_t>(cv(v[3] * inv)) << 16);
+          *reinterpret_cast<uint2*>(orow + db * 16 + 4 * g) = pk;
+        }
+      };
+      if (a.out_act == ACT_F16)
+        store(std::true_type{});
+      else
+        store(std::false_type{});
     }
     if (!has_next) break;
     cur = nxt;
@@ -260,6 +273,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
 
 hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s) {
   if (a.npre < 0 || (a.npre > 0 && !a.pkv)) return hipErrorInvalidValue;
+  if (a.seq_ub * a.n_heads >= (int64_t(1) << 31)) return hipErrorInvalidValue;   // 32-bit item numbers
   const int g = grid_cap(a.seq_ub * a.n_heads, 4096);
   if (a.hd == 64)
     hipLaunchKernelGGL(k_attn_bf16<64>, dim3(g), dim3(256), 0, s, a);
