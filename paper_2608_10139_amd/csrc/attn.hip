@@ -13,8 +13,8 @@
 // products run on v_mfma_f32_16x16x32_f16 (fp16 keeps 3 more mantissa bits
 // than bf16 at the same rate).  S^T = K Q^T puts one query per lane column and
 // 4 keys per lane, which is exactly the operand layout the P V product needs
-// for P^T, so probabilities never leave registers; V is staged transposed in
-// LDS.  The softmax denominator sums the fp16-rounded probabilities that the
+// for P^T, so probabilities never leave registers; V is staged row-major in
+// LDS and read transposed by gfx950's ds_read_b64_tr_b16.  The softmax denominator sums the fp16-rounded probabilities that the
 // P V product actually uses.
 //
 // Shared prompt prefix (MFMA path): a sequence is then the prefix's npre
@@ -32,6 +32,13 @@ namespace aiq {
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+typedef __attribute__((address_space(3))) uint16_t lds_u16;
+
+// 16-byte chunk `ch` of LDS row r (see k_attn_bf16)
+__device__ __forceinline__ int kswz(int r, int ch) { return ch ^ ((r >> 1) & 7); }
+__device__ __forceinline__ int vswz(int r, int ch) { return ch ^ (r & 7); }
 
 static int grid_cap(int64_t items, int cap) {
   int64_t g = items;
@@ -47,9 +54,13 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   constexpr int KB = 64;            // keys per block
   constexpr int CH = HD / 8;        // 16-byte chunks per K row
   constexpr int PER = KB * CH / 256;   // chunks of K (and of V) per thread per block
+  // K and V of one key block, row-major, 16-byte chunks XOR-swizzled by row
+  // bits (K: rows 2i and 2i+1 share a pattern, so the 16 rows of a fragment
+  // read hit distinct banks; V: the rows of a transposed read do)
   __shared__ __attribute__((aligned(16))) uint16_t Ks[KB * HD];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[HD * KB];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[KB * HD];
 
+  lds_u16* const vs_lds = (lds_u16*)(Vs);   // LDS address space, for the transposing reads
   const int64_t tb = a.desc[D_TOK_BEGIN], sb = a.desc[D_SEQ_BEGIN], ns = a.desc[D_NSEQ];
   const int64_t n_items = ns * a.n_heads;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6, g = lane >> 4, c16 = lane & 15;
@@ -155,14 +166,8 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
 #pragma unroll
       for (int u = 0; u < PER; ++u) {
         const int id = t + u * 256, r = id / CH, ch = id % CH;
-        *reinterpret_cast<uint4*>(Ks + r * HD + ((ch ^ (r & 7)) << 3)) = kr[u];
-        const uint32_t vw[4] = {vr[u].x, vr[u].y, vr[u].z, vr[u].w};
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int dim = ch * 8 + j;
-          const uint16_t e = static_cast<uint16_t>(vw[j >> 1] >> ((j & 1) * 16));
-          Vt[dim * KB + ((((r >> 2) ^ (dim & 15)) << 2) | (r & 3))] = e;
-        }
+        *reinterpret_cast<uint4*>(Ks + r * HD + (kswz(r, ch) << 3)) = kr[u];
+        *reinterpret_cast<uint4*>(Vs + r * HD + (vswz(r, ch) << 3)) = vr[u];
       }
       __syncthreads();
       if (kb < qb) {
@@ -183,7 +188,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
         const int krow = j * 16 + c16;
 #pragma unroll
         for (int kc = 0; kc < HD / 32; ++kc) {
-          const half8 kf = *reinterpret_cast<const half8*>(Ks + krow * HD + (((kc * 4 + g) ^ (krow & 7)) << 3));
+          const half8 kf = *reinterpret_cast<const half8*>(Ks + krow * HD + (kswz(krow, kc * 4 + g) << 3));
           sacc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf, qf[kc], sacc[j], 0, 0, 0);
         }
       }
@@ -227,17 +232,26 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
       for (int db = 0; db < HD / 16; ++db) o[db] *= alpha;
       ol *= alpha;
 
-      // O^T += V^T P^T over two 32-key halves
+      // O^T += V^T P^T over two 32-key halves.  V^T fragments come from the
+      // row-major V block through transposing LDS reads: in each 16-lane
+      // group, lane 4a + b receives element b of the 8-byte pieces addressed
+      // by lanes a, a + 4, a + 8, a + 12.  Lane i of group g therefore
+      // addresses key row 32u + 16h + 4g + i/4 at dims 16db + 4(i%4), and lane
+      // c16 receives dim 16db + c16 of those four keys: the keys its pb half h
+      // holds.
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
 #pragma unroll
         for (int db = 0; db < HD / 16; ++db) {
-          const int dim = db * 16 + c16;
-          const uint16_t* vrow = Vt + dim * KB;
-          const uint2 lo = *reinterpret_cast<const uint2*>(vrow + (((8 * u + g) ^ (dim & 15)) << 2));
-          const uint2 hi = *reinterpret_cast<const uint2*>(vrow + (((8 * u + 4 + g) ^ (dim & 15)) << 2));
-          const uint4 vv = make_uint4(lo.x, lo.y, hi.x, hi.y);
-          const half8 vf = *reinterpret_cast<const half8*>(&vv);
+          v4i16 part[2];
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int vrow = 32 * u + 16 * h + 4 * g + (c16 >> 2);
+            const int dim = db * 16 + 4 * (c16 & 3);
+            const int el = vrow * HD + (vswz(vrow, dim >> 3) << 3) + (dim & 7);
+            part[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(reinterpret_cast<lds_v4i16*>(vs_lds + el));
+          }
+          const half8 vf = __builtin_bit_cast(half8, __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5, 6, 7));
           o[db] = __builtin_amdgcn_mfma_f32_16x16x32_f16(vf, pb[u], o[db], 0, 0, 0);
         }
         ol = __builtin_amdgcn_mfma_f32_16x16x32_f16(ones, pb[u], ol, 0, 0, 0);
