@@ -261,13 +261,15 @@ def split_baseline_leg(tables, model, q, dm, B, torch, micro=128) -> dict:
             "micro_batch": micro, "logits": f"fp32 [{micro}, {V}] per micro-batch, D2H"}
 
 
-def relational_scale_leg(B, torch, sizes, thresholds, steps: int = 5) -> list:
+def relational_scale_leg(B, torch, sizes, thresholds, steps: int = 5, multipass: bool = False) -> list:
     """The relational part alone (WHERE c < k, stable compaction, per-row
     token counts) on the 1M-row sweep table's generator scaled to `sizes` rows
     (columns c and offsets; no token list), through a relational-only plan.
-    Algorithmic bytes per run: 4 B of c per row + per selected row 4 B id
-    written, 16 B of offsets read, 8 B of cu_seqlens written.  The counts are
-    checked against numpy on the host."""
+    Algorithmic bytes per run: 4 B of c per row, 4 B per selected id written,
+    8 B per distinct offset entry read (off[r] and off[r + 1] of every
+    selected row r: 16 B per row when the selected rows are isolated, 8 B
+    when they are adjacent), 8 B per cu_seqlens entry written.  The counts
+    are checked against numpy on the host."""
     import dataclasses
     from paper_2608_10139_amd.device import DeviceModel, DeviceQuery
     from synth import WORKLOADS
@@ -284,12 +286,15 @@ def relational_scale_leg(B, torch, sizes, thresholds, steps: int = 5) -> list:
         tables = {"probe": probe, "build": None, "prefix": np.zeros(0, np.int32)}
         for k in thresholds:
             q = Query(preds=(Pred("c", "lt", k),), labels=(1, 2), decision="binary_gt", agg="count")
-            dq = DeviceQuery(tables, tiny, q, dmodel=dm, relational_only=True, want_sel=False)
+            dq = DeviceQuery(tables, tiny, q, dmodel=dm, relational_only=True, want_sel=False,
+                             multipass_compact=multipass)
             dq.run()
             torch.cuda.synchronize()
             res = dq.results()
             want = probe["c"] < k
             n_sel = int(np.count_nonzero(want))
+            # offset entries read: r and r + 1 of every selected row r
+            n_off = n_sel + int(np.count_nonzero(want & ~np.concatenate(([False], want[:-1]))))
             if res["status"] != 0 or res["n_selected"] != n_sel or res["n_tokens"] != int(probe["len"][want].sum()):
                 raise RuntimeError(f"relational scale run disagrees with numpy at n={n}, c < {k}")
             ev = HipEvents(2 * 8 * steps)
@@ -305,7 +310,7 @@ def relational_scale_leg(B, torch, sizes, thresholds, steps: int = 5) -> list:
             rel = float(np.sum(kinds.get(B.AIQ_K_REL, []))) / steps
             pack = float(np.sum(kinds.get(B.AIQ_K_PACK, []))) / steps
             agg = float(np.sum(kinds.get(B.AIQ_K_AGG, []))) / steps
-            nbytes = 4 * n + 28 * n_sel
+            nbytes = 4 * n + 4 * n_sel + 8 * n_off + 8 * (n_sel + 1)
             gbps = nbytes / ((rel + pack) * 1e-3) / 1e9
             out.append({"rows": n, "predicate": f"c < {k}", "selected": n_sel, "tokens": res["n_tokens"],
                         "where_compact_ms": round(rel, 4), "token_counts_ms": round(pack, 4),
@@ -324,8 +329,9 @@ def pack_config_leg(B, torch, steps: int = 3) -> list:
     with every row selected (c < 1000) and the 131k-row group-by table (no
     predicate).  Runs the whole query with no decoder layer (a 0-layer fp32
     model: embedding -> head) and reads the pack stage's HIP-event time.
-    Algorithmic bytes: per selected row 8 B of offsets + 4 B of cu_seqlens,
-    per token 4 B read + 4 B written (+ 4 B per prefix token written)."""
+    Algorithmic bytes: per selected row 4 B of its row id + 8 B of offsets
+    (its list start) + 8 B of cu_seqlens read, per token 4 B read + 4 B
+    written."""
     from paper_2608_10139_amd.device import DeviceModel, DeviceQuery
     from synth import WORKLOADS
     from synth.configs import ModelSpec
@@ -357,7 +363,7 @@ def pack_config_leg(B, torch, steps: int = 3) -> list:
         pack = float(np.sum(per_kind_ms(B, tr, ev).get(B.AIQ_K_PACK, []))) / steps
         ev.close()
         n_sel, n_tok = res["n_selected"], res["n_tokens"]
-        nbytes = 12 * n_sel + 8 * n_tok
+        nbytes = 20 * n_sel + 8 * n_tok
         gbps = nbytes / (pack * 1e-3) / 1e9
         out.append({"table": name, "rows": len(probe["id"]), "selected": n_sel, "tokens": n_tok,
                     "pack_ms": round(pack, 4), "algorithmic_bytes": nbytes, "gbps": round(gbps, 1),
@@ -386,6 +392,8 @@ def main(argv=None) -> int:
                     help="recompute the prompt prefix inside every row (default: prefilled once and shared)")
     ap.add_argument("--relational-scale", action="store_true",
                     help="only the relational part at 2^26 and 2^28 rows (relational-only plans); one JSON line")
+    ap.add_argument("--multipass-compact", action="store_true",
+                    help="with --relational-scale: separate mask / scan / scatter launches instead of one")
     ap.add_argument("--no-relational-scale", action="store_true",
                     help="skip the 2^26-row relational run of the default line")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -411,14 +419,16 @@ def main(argv=None) -> int:
     from paper_2608_10139_amd.device import DeviceModel, DeviceQuery
     if a.relational_scale:
         torch.cuda.set_device(0)
-        runs = relational_scale_leg(B, torch, [1 << 26, 1 << 28], [10, 1000], steps=a.steps)
+        runs = relational_scale_leg(B, torch, [1 << 26, 1 << 28], [10, 1000], steps=a.steps,
+                                    multipass=a.multipass_compact)
         packs = pack_config_leg(B, torch)
         best = max(runs, key=lambda r: r["gbps"])
         print(json.dumps({"metric": "relational stages (WHERE + stable compaction + token counts) HBM GB/s",
                           "value": best["gbps"], "unit": "GB/s", "n_gpus": 1, "steps": a.steps, "warmup": 1,
                           "higher_is_better": True, "dtype": "int32", "data": "synthetic",
                           "config": {"workload": "sweep-table generator scaled to 2^26 and 2^28 rows, "
-                                                 "c and offsets only, relational-only plans"},
+                                                 "c and offsets only, relational-only plans",
+                                     "compaction": "multipass" if a.multipass_compact else "one launch"},
                           "roofline": {"bound": "hbm", "achieved": best["gbps"], "peak": PEAK_HBM_GBPS,
                                        "unit": "GB/s", "frac": best["hbm_frac"], "traffic": None},
                           "runs": runs, "pack_at_config_size": packs}), flush=True)

@@ -92,6 +92,8 @@ typedef enum aiq_logits_mode { AIQ_LOGITS_LABELS = 1, AIQ_LOGITS_FULL_VOCAB = 2 
 #define AIQ_DEV_GROUP_CAP   0x40  /* more groups than aiq_out.grp_cap               */
 #define AIQ_DEV_PAIR_CAP    0x80  /* more candidate pairs than aiq_query.max_pairs:
                                      the pairs past it are dropped                  */
+#define AIQ_DEV_SCAN_WAIT   0x100 /* a compaction block waited too long for an
+                                     earlier block's totals: outputs invalid       */
 
 /* indices into aiq_out.scalars (int64, device) */
 #define AIQ_S_SELECTED 0   /* rows passing WHERE (and the join)                      */
@@ -266,6 +268,15 @@ typedef struct aiq_plan_opts {
  * once per selected row in both modes.
  */
 #define AIQ_PLAN_UNSHARED_PREFIX 2
+
+/*
+ * The WHERE (+ join) compaction and the selected rows' token offsets run as
+ * one launch (decoupled look-back across blocks of rows) whenever a block's
+ * token sum is bounded below 2^31 (8192 x (max_list_len + n_prefix)).
+ * AIQ_PLAN_MULTIPASS_COMPACT: run them as separate mask, scan and scatter
+ * launches instead.  Both give identical outputs.
+ */
+#define AIQ_PLAN_MULTIPASS_COMPACT 4
 
 /*
  * Outputs, all device buffers owned by the caller.  Optional buffers may be

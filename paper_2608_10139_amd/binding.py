@@ -23,9 +23,11 @@ AIQ_AGG_COUNT, AIQ_AGG_AVG_LABEL_COUNT_BY, AIQ_AGG_COUNT_BY_PAYLOAD, AIQ_AGG_SUM
 AIQ_LOGITS_LABELS, AIQ_LOGITS_FULL_VOCAB = 1, 2
 AIQ_PLAN_RELATIONAL_ONLY = 1
 AIQ_PLAN_UNSHARED_PREFIX = 2
+AIQ_PLAN_MULTIPASS_COMPACT = 4
 
 AIQ_DEV_TOKEN_RANGE, AIQ_DEV_DUP_KEY, AIQ_DEV_HASH_FULL, AIQ_DEV_IDS_CAP = 0x01, 0x02, 0x04, 0x08
 AIQ_DEV_GROUP_RANGE, AIQ_DEV_LIST_LEN, AIQ_DEV_GROUP_CAP, AIQ_DEV_PAIR_CAP = 0x10, 0x20, 0x40, 0x80
+AIQ_DEV_SCAN_WAIT = 0x100
 AIQ_S_SELECTED, AIQ_S_KEPT, AIQ_S_TOKENS, AIQ_S_STATUS, AIQ_S_GROUPS, AIQ_S_PAIRS = range(6)
 AIQ_N_SCALARS = 8
 AIQ_MAX_PREDS, AIQ_MAX_IN_SET, AIQ_MAX_PREFIX, AIQ_MAX_LABELS = 8, 32, 64, 8

@@ -22,6 +22,7 @@ struct aiq_plan {
   std::vector<aiq_layer> layers;
   bool has_probe = false, has_build = false, has_query = false;
   bool rel_only = false;   // AIQ_PLAN_RELATIONAL_ONLY
+  bool lb_compact = false; // single-launch compaction (not AIQ_PLAN_MULTIPASS_COMPACT)
   // the prompt prefix is prefilled once per run and its keys / values are
   // shared by every row (16-bit models, unless AIQ_PLAN_UNSHARED_PREFIX)
   bool share_prefix = false;
@@ -148,7 +149,7 @@ struct Layout {
   size_t ctr, mask, blk_cnt, blk_off, sel, payload, lens, label, logits, cu, blk_tok, tok_off, packed, hkeys, hvals,
       bins, desc, rcos, rsin, rrev, x, delta, h, qkv, att, ffn, pos, hf, ssp, rs, pkv, ptok, pcu, pdesc, pxlast,
       kvc, gkv, glog, gtok, gdone, gen, gdesc, gcnt, kcount, koff, prank, psorted, pcnt, poff, pscan, pa, pb,
-      total;
+      lb, total;
 };
 
 size_t act_bytes(const aiq_plan* p) { return p->bf16 ? 2 : 4; }
@@ -199,6 +200,7 @@ Layout run_layout(const aiq_plan* p) {
   L.cu = c.take(static_cast<size_t>(ns + 1) * 8);
   L.blk_tok = c.take(static_cast<size_t>(nb) * 8);
   L.tok_off = c.take(static_cast<size_t>(nb + 1) * 8);
+  L.lb = c.take(static_cast<size_t>((ns + LB_MIN_ROWS - 1) / LB_MIN_ROWS + 1) * 4 * 8);
   const size_t hcap = p->hash_log2 ? (size_t(1) << p->hash_log2) : 1;
   L.hkeys = c.take(hcap * 4);
   L.hvals = c.take(hcap * 4);
@@ -673,7 +675,8 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
     if (!query) return fail(AIQ_EINVAL);
     p->has_probe = true;
     p->rel_only = opts && (opts->flags & AIQ_PLAN_RELATIONAL_ONLY);
-    if (opts && (opts->flags & ~(AIQ_PLAN_RELATIONAL_ONLY | AIQ_PLAN_UNSHARED_PREFIX))) return fail(AIQ_EINVAL);
+    if (opts && (opts->flags & ~(AIQ_PLAN_RELATIONAL_ONLY | AIQ_PLAN_UNSHARED_PREFIX | AIQ_PLAN_MULTIPASS_COMPACT)))
+      return fail(AIQ_EINVAL);
     st = copy_table(probe, &p->probe, &p->probe_cols, p->rel_only ? 1 : 2);
     if (st != AIQ_OK) return fail(st);
     const aiq_query& q = p->q;
@@ -734,6 +737,9 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
     // packed tokens: the row lists (two per pair), plus the prefix per sequence
     // unless it is shared
     const int64_t npre_packed = p->share_prefix ? 0 : q.n_prefix;
+    // one-launch compaction when a block's token sum fits 32 bits
+    p->lb_compact = !(opts && (opts->flags & AIQ_PLAN_MULTIPASS_COMPACT)) &&
+                    static_cast<int64_t>(REL_ROWS_PER_BLOCK) * (p->probe.max_list_len + npre_packed) < (int64_t(1) << 31);
     const int64_t max_own = (p->pairs ? 2 : 1) * static_cast<int64_t>(p->probe.max_list_len);
     p->n_seq_ub = p->pairs ? q.max_pairs : p->n_rows;
     p->t_ub = p->pairs ? q.max_pairs * (max_own + npre_packed)
@@ -844,19 +850,25 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
     const aiq_col& pc = p->build_cols[q.build_payload_col];
     HIP_TRY(launch_hash_build(p->build_preds, kc.data, kc.dtype, pc.data, pc.dtype, p->build.n_rows, h, ctr, s));
   }
-  HIP_TRY(launch_row_mask(p->probe_preds, n, pkey, pkey_dt, h, p->has_build, mask, blk_cnt, s));
-  HIP_TRY(launch_scan_blocks(blk_cnt, nullptr, n, blk_off, ctr + C_SEL, s));
-  // compaction: selected ids (straight into the caller's ids when nothing
-  // else follows), join payloads, token counts and per-block token sums
   const int32_t npre_rows = p->share_prefix ? 0 : q.n_prefix;   // prefix tokens packed into each row
-  ScatterLens sl{p->probe.list_offsets, p->probe.max_list_len, npre_rows, lens, blk_tok};
-  if (p->rel_only)
-    HIP_TRY(launch_scatter_rows(mask, blk_off, nullptr, n, nullptr, out->ids, out->ids_cap, pkey, pkey_dt, h,
-                                p->has_build, payload, ctr, s,
-                                out->sel_cap > 0 ? out->sel_ids : nullptr, out->sel_cap, sl));
-  else
-    HIP_TRY(launch_scatter_rows(mask, blk_off, nullptr, n, nullptr, sel, n, pkey, pkey_dt, h, p->has_build,
-                                payload, ctr, s, nullptr, 0, p->pairs ? ScatterLens{} : sl));
+  // selected ids go straight into the caller's ids when nothing else follows
+  int32_t* ids1 = p->rel_only ? out->ids : sel;
+  const int64_t cap1 = p->rel_only ? out->ids_cap : n;
+  int32_t* ids2 = p->rel_only && out->sel_cap > 0 ? out->sel_ids : nullptr;
+  const int64_t cap2 = p->rel_only ? out->sel_cap : 0;
+  if (p->lb_compact) {
+    // masks, compaction, join payloads and token offsets in one launch
+    HIP_TRY(launch_select_lb(p->probe_preds, n, pkey, pkey_dt, h, p->has_build, ids1, cap1, ids2, cap2, payload,
+                             p->pairs ? nullptr : p->probe.list_offsets, p->probe.max_list_len, npre_rows, cu,
+                             at<int64_t>(ws, L.lb), ctr, s));
+  } else {
+    HIP_TRY(launch_row_mask(p->probe_preds, n, pkey, pkey_dt, h, p->has_build, mask, blk_cnt, s));
+    HIP_TRY(launch_scan_blocks(blk_cnt, nullptr, n, blk_off, ctr + C_SEL, s));
+    // compaction: selected ids, join payloads, token counts and per-block token sums
+    ScatterLens sl{p->probe.list_offsets, p->probe.max_list_len, npre_rows, lens, blk_tok};
+    HIP_TRY(launch_scatter_rows(mask, blk_off, nullptr, n, nullptr, ids1, cap1, pkey, pkey_dt, h, p->has_build,
+                                payload, ctr, s, ids2, cap2, p->pairs ? ScatterLens{} : sl));
+  }
   tr.end();
   // the sequences: the selected rows, or the candidate pairs
   const int64_t* n_seq = ctr + (p->pairs ? C_PAIRS : C_SEL);
@@ -891,7 +903,7 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
     HIP_TRY(launch_scan_i32_i64(lens, n_seq, ns_ub, cu, pscan, ctr + C_TOK, s));
     HIP_TRY(launch_pair_gather(pa, pb, sel, p->probe.list_offsets, p->probe.list_tokens, cu, row_prefix,
                                p->probe.max_list_len, p->model.vocab, p->t_ub, ns_ub, packed, ctr, s));
-  } else {
+  } else if (!p->lb_compact) {
     // ---- token offsets of the selected rows
     HIP_TRY(launch_scan_blocks64(blk_tok, nullptr, n, tok_off, ctr + C_TOK, s));
     HIP_TRY(launch_cu_from_blocks(lens, blk_off, tok_off, n, cu, s));

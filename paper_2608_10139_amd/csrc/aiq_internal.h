@@ -53,6 +53,9 @@ constexpr int REL_THREADS = 256;
 constexpr int REL_ROWS_PER_THREAD = 32;
 constexpr int REL_ROWS_PER_BLOCK = REL_THREADS * REL_ROWS_PER_THREAD;   // 8192
 constexpr int REL_WORDS_PER_BLOCK = REL_ROWS_PER_BLOCK / 64;             // 128
+// the one-launch compaction's blocks hold at least this many rows (its look-back
+// state is 4 int64 per block)
+constexpr int LB_MIN_ROWS = 4096;
 
 // ---------------------------------------------------------------- launchers
 // Every launcher enqueues on `s` and returns hipGetLastError().
@@ -97,6 +100,18 @@ hipError_t launch_scatter_rows(const uint64_t* mask, const int64_t* blk_off, con
 // per-block token offsets of the compaction (tok_off = scan of blk_tok).
 hipError_t launch_cu_from_blocks(const int32_t* lens, const int64_t* blk_off, const int64_t* tok_off,
                                  int64_t n_ub, int64_t* cu, hipStream_t s);
+// WHERE (+ join), stable compaction and token offsets in one launch (decoupled
+// look-back over `lb`, 4 int64 per block of at least LB_MIN_ROWS rows,
+// cleared here first): out_ids
+// (and out_ids2) as launch_scatter_rows, ctr[C_SEL] = the count; with `off`
+// also cu[0..n_sel] (cu[i] = tokens of the selected rows before i, token
+// count = min(list length, max_len) + n_prefix) and ctr[C_TOK] = the total.
+// A block's token sum must stay below 2^31: REL_ROWS_PER_BLOCK *
+// (max_len + n_prefix) < 2^31.
+hipError_t launch_select_lb(const DPredList& preds, int64_t n_rows, const void* probe_key, int32_t probe_key_dtype,
+                            HashArgs h, int join, int32_t* out_ids, int64_t out_cap, int32_t* out_ids2,
+                            int64_t out_cap2, int32_t* out_payload, const int64_t* off, int32_t max_len,
+                            int32_t n_prefix, int64_t* cu, int64_t* lb, int64_t* ctr, hipStream_t s);
 // ctr[C_KEPT] = ctr[C_SEL] (every selected row kept), flagged if above cap.
 hipError_t launch_keep_selected(int64_t* ctr, int64_t cap, hipStream_t s);
 hipError_t launch_group_accumulate(const int32_t* sel, const int32_t* label, const int32_t* payload,

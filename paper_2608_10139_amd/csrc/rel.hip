@@ -263,6 +263,31 @@ __device__ __forceinline__ uint32_t atom16f(const DPred& P, int64_t r0, int64_t 
   }
 }
 
+// The mask word of one pass (see above): rows r0 .. r0 + 15 of this lane and
+// of the next three lanes; valid in lanes with lane % 4 == 0, whose word goes
+// to index pass * 64 + w * 16 + lane / 4 of the block.
+__device__ __forceinline__ uint64_t pass_word(const DPredList& preds, int64_t r0, int64_t n_rows,
+                                              const void* probe_key, int32_t pk_dt, const HashArgs& h, int join) {
+  uint32_t keep = 0;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) keep |= static_cast<uint32_t>(r0 + k < n_rows) << k;
+  for (int i = 0; i < preds.n; ++i) {   // uniform over the grid
+    const DPred& P = preds.p[i];
+    if (P.dtype == AIQ_I8) keep &= atom16<int8_t>(P, r0, n_rows);
+    else if (P.dtype == AIQ_I16) keep &= atom16<int16_t>(P, r0, n_rows);
+    else if (P.dtype == AIQ_F32) keep &= atom16f(P, r0, n_rows);
+    else keep &= atom16<int32_t>(P, r0, n_rows);
+  }
+  if (join) {
+    for (int k = 0; k < 16; ++k)
+      if ((keep >> k) & 1u)
+        if (hash_find(h, static_cast<int32_t>(load_int(probe_key, pk_dt, r0 + k))) < 0) keep &= ~(1u << k);
+  }
+  const uint32_t k1 = __shfl_down(keep, 1), k2 = __shfl_down(keep, 2), k3 = __shfl_down(keep, 3);
+  return static_cast<uint64_t>(keep) | (static_cast<uint64_t>(k1) << 16) | (static_cast<uint64_t>(k2) << 32) |
+         (static_cast<uint64_t>(k3) << 48);
+}
+
 __global__ __launch_bounds__(REL_THREADS) void k_row_mask(DPredList preds, int64_t n_rows,
                                                           const void* probe_key, int32_t pk_dt,
                                                           HashArgs h, int join, uint64_t* mask,
@@ -273,25 +298,8 @@ __global__ __launch_bounds__(REL_THREADS) void k_row_mask(DPredList preds, int64
 #pragma unroll
   for (int pass = 0; pass < 2; ++pass) {
     const int64_t r0 = base + pass * 4096 + w * 1024 + lane * 16;
-    uint32_t keep = 0;
-#pragma unroll
-    for (int k = 0; k < 16; ++k) keep |= static_cast<uint32_t>(r0 + k < n_rows) << k;
-    for (int i = 0; i < preds.n; ++i) {   // uniform over the grid
-      const DPred& P = preds.p[i];
-      if (P.dtype == AIQ_I8) keep &= atom16<int8_t>(P, r0, n_rows);
-      else if (P.dtype == AIQ_I16) keep &= atom16<int16_t>(P, r0, n_rows);
-      else if (P.dtype == AIQ_F32) keep &= atom16f(P, r0, n_rows);
-      else keep &= atom16<int32_t>(P, r0, n_rows);
-    }
-    if (join) {
-      for (int k = 0; k < 16; ++k)
-        if ((keep >> k) & 1u)
-          if (hash_find(h, static_cast<int32_t>(load_int(probe_key, pk_dt, r0 + k))) < 0) keep &= ~(1u << k);
-    }
-    const uint32_t k1 = __shfl_down(keep, 1), k2 = __shfl_down(keep, 2), k3 = __shfl_down(keep, 3);
+    const uint64_t word = pass_word(preds, r0, n_rows, probe_key, pk_dt, h, join);
     if ((lane & 3) == 0) {
-      const uint64_t word = static_cast<uint64_t>(keep) | (static_cast<uint64_t>(k1) << 16) |
-                            (static_cast<uint64_t>(k2) << 32) | (static_cast<uint64_t>(k3) << 48);
       mask[blockIdx.x * REL_WORDS_PER_BLOCK + pass * 64 + w * 16 + (lane >> 2)] = word;
       cnt += __popcll(word);
     }
@@ -629,6 +637,289 @@ hipError_t launch_cu_from_blocks(const int32_t* lens, const int64_t* blk_off, co
   if (nb == 0) return hipSuccess;
   hipLaunchKernelGGL(k_cu_from_blocks, dim3(static_cast<unsigned>(nb)), dim3(256), 0, s, lens, blk_off, tok_off,
                      cu);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ single-pass compaction
+// WHERE (+ join) masks, stable compaction and the selected rows' token
+// offsets in one launch (decoupled look-back).  Block b (LB_ROWS rows,
+// 16 per thread) builds its mask words and survivor list in LDS, reads the
+// survivors' list offsets, publishes its survivor count and token sum, and
+// finds the totals of all earlier blocks by looking back over the published
+// values: a predecessor that has already published its inclusive prefix
+// ends the walk, one that has published only its own totals is added and the
+// walk goes on.  Outputs are then written at their final positions: ids, join
+// payloads and cu[pos] = tokens of all earlier selected rows; the last block
+// writes the totals (ctr[C_SEL], ctr[C_TOK], cu[n_selected]).  Each row's
+// column values and offsets are read once; nothing per row goes back through
+// memory.
+//
+// A block waits only for lower-numbered blocks.  Workgroups are handed to
+// each XCD's dispatcher in increasing order and each dispatcher starts them
+// in that order, so a block that is waiting never holds the slot that a
+// lower-numbered, not yet started block needs.  The wait is still bounded:
+// past LB_SPIN_LIMIT polls the block flags AIQ_DEV_SCAN_WAIT and goes on
+// with what it has (outputs then invalid).
+
+constexpr int LB_THREADS = 512;
+constexpr int LB_ROWS = 16 * LB_THREADS;       // rows per block, 16 per thread
+constexpr int LB_WORDS = LB_ROWS / 64;
+constexpr int LB_WAVES = LB_THREADS / 64;
+static_assert(LB_ROWS >= LB_MIN_ROWS && LB_ROWS <= REL_ROWS_PER_BLOCK && LB_WORDS <= 128, "look-back block size");
+constexpr int64_t LB_SET = static_cast<int64_t>(1ull << 63);   // marks a published word
+constexpr int LB_SPIN_LIMIT = 1 << 22;
+
+// token counts stored with one spare slot per 16 entries: thread t's 16
+// consecutive entries then start in distinct banks
+__device__ __forceinline__ int lb_pad(int i) { return i + (i >> 4); }
+
+// Look-back words of block b at lb + 4b: [0] the block's own totals packed as
+// tokens << 14 | count (count <= 8192, tokens < 2^31), [1] the inclusive
+// count and [2] the inclusive tokens through the block.  Every word carries
+// its own published bit, so no ordering between them is needed (relaxed
+// device-scope atomics; no other data passes between blocks).
+__device__ __forceinline__ int64_t lb_get(const int64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void lb_put(int64_t* p, int64_t v) {
+  __hip_atomic_store(p, v | LB_SET, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ int64_t wave_sum64(int64_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__global__ __launch_bounds__(LB_THREADS) void k_select_lb(
+    DPredList preds, int64_t n_rows, int64_t nb, const void* probe_key, int32_t pk_dt, HashArgs h, int join,
+    int32_t* out_ids, int64_t out_cap, int32_t* out_ids2, int64_t out_cap2, int32_t* out_payload,
+    const int64_t* off, int32_t max_len, int32_t n_prefix, int64_t* cu, int64_t* lb, int64_t* ctr) {
+  __shared__ uint64_t words[LB_WORDS];
+  __shared__ int32_t wpre[LB_WORDS + 1];
+  __shared__ int32_t wtot;
+  __shared__ uint16_t rows[LB_ROWS];                      // block-relative row of each survivor, in order
+  __shared__ int32_t tx[LB_ROWS + LB_ROWS / 16];          // token counts, then their prefix
+  __shared__ int64_t red[LB_WAVES];
+  __shared__ int32_t tscan[LB_WAVES];
+  __shared__ int64_t sb[2];                               // count and tokens of all earlier blocks
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int64_t b = blockIdx.x;
+  const int64_t base = b * LB_ROWS;
+  // masks of the block's rows into LDS (lane l of wave w: rows w*1024 + 16l ..),
+  // then their popcount prefix
+  {
+    const uint64_t word = pass_word(preds, base + w * 1024 + lane * 16, n_rows, probe_key, pk_dt, h, join);
+    if ((lane & 3) == 0) words[w * 16 + (lane >> 2)] = word;
+  }
+  __syncthreads();
+  int32_t pc = 0;
+  if (t < LB_WORDS) pc = __popcll(words[t]);
+  int32_t x = pc;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int32_t y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (LB_WORDS > 64) {
+    if (t == 63) wtot = x;
+    __syncthreads();
+  }
+  if (t < LB_WORDS) {
+    const int32_t incl = x + (t >= 64 ? wtot : 0);
+    wpre[t] = incl - pc;
+    if (t == LB_WORDS - 1) wpre[LB_WORDS] = incl;
+  }
+  __syncthreads();
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    const int wi = j * LB_WAVES + w;   // word of rows 64 wi .. 64 wi + 63; this lane's row is 64 wi + lane
+    const uint64_t word = words[wi];
+    if ((word >> lane) & 1ull)
+      rows[wpre[wi] + __popcll(word & below)] = static_cast<uint16_t>(j * LB_THREADS + t);
+  }
+  __syncthreads();
+  const int32_t cnt = wpre[LB_WORDS];
+  // token count of every survivor (list length from the low 32 bits of both
+  // offsets, exact below 2^31), eight loads per thread in flight
+  int64_t tok = 0;
+  if (off) {
+    bool bad_len = false;
+    const uint32_t* off32 = reinterpret_cast<const uint32_t*>(off);
+    constexpr int U = 8;
+    for (int i0 = 0; i0 < cnt; i0 += LB_THREADS * U) {
+      uint32_t lo0[U], lo1[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int i = i0 + u * LB_THREADS + t;
+        lo0[u] = lo1[u] = 0;
+        if (i < cnt) {
+          const int64_t r = base + rows[i];
+          lo0[u] = off32[2 * r];
+          lo1[u] = off32[2 * r + 2];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int i = i0 + u * LB_THREADS + t;
+        if (i >= cnt) continue;
+        int32_t len = static_cast<int32_t>(lo1[u] - lo0[u]);
+        if (len < 0 || len > max_len) {
+          bad_len = true;
+          len = len < 0 ? 0 : max_len;
+        }
+        tx[lb_pad(i)] = len + n_prefix;
+        tok += len + n_prefix;
+      }
+    }
+    if (bad_len) set_status(ctr, AIQ_DEV_LIST_LEN);
+    tok = wave_sum64(tok);
+    if (lane == 0) red[w] = tok;
+  }
+  __syncthreads();
+  if (off) {
+    tok = 0;
+#pragma unroll
+    for (int i = 0; i < LB_WAVES; ++i) tok += red[i];
+  }
+  // publish this block's totals: block 0 has no predecessor, so its totals
+  // are already its inclusive prefix
+  int64_t* me = lb + 4 * b;
+  if (t == 0) {
+    if (b == 0) {
+      lb_put(me + 1, cnt);
+      lb_put(me + 2, tok);
+    } else {
+      lb_put(me, (tok << 14) | cnt);
+    }
+  }
+  // exclusive prefix of the token counts inside the block: thread t owns
+  // entries 16t .. 16t + 15, 32-bit sums (the plan bounds a block's tokens
+  // below 2^31)
+  if (off) {
+    const int first = t * 16;
+    const int lim = cnt - first < 16 ? cnt - first : 16;
+    int32_t own = 0;
+    for (int k = 0; k < lim; ++k) own += tx[lb_pad(first + k)];
+    int32_t y = own;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int32_t z = __shfl_up(y, o);
+      if (lane >= o) y += z;
+    }
+    if (lane == 63) tscan[w] = y;
+    __syncthreads();
+    int32_t run = y - own;
+    for (int i = 0; i < w; ++i) run += tscan[i];
+    for (int k = 0; k < lim; ++k) {
+      const int a = lb_pad(first + k);
+      const int32_t v = tx[a];
+      tx[a] = run;
+      run += v;
+    }
+  }
+  // look-back over the predecessors: lane l of wave 0 reads block j - l.
+  // When the nearest inclusive prefix is not in reach yet, the leading run of
+  // published blocks is consumed and the walk continues behind it.
+  if (w == 0) {
+    int64_t ec = 0, et = 0;
+    if (b > 0) {
+      int64_t j = b - 1;
+      int spins = 0;
+      for (;;) {
+        const int64_t idx = j - lane;
+        int state = 2;   // 2: inclusive prefix, 1: block totals only, 0: nothing yet
+        int64_t vc = 0, vt = 0;
+        if (idx >= 0) {   // idx < 0: the empty prefix before block 0
+          const int64_t* q = lb + 4 * idx;
+          const int64_t ag = lb_get(q), ic = lb_get(q + 1), it = lb_get(q + 2);
+          if (ic < 0 && it < 0) {
+            vc = ic & ~LB_SET;
+            vt = it & ~LB_SET;
+          } else if (ag < 0) {
+            state = 1;
+            vc = ag & 0x3FFF;
+            vt = (ag >> 14) & 0x7FFFFFFF;
+          } else {
+            state = 0;
+          }
+        }
+        const uint64_t incl = __ballot(state == 2), ready = __ballot(state != 0);
+        const int p = incl ? __ffsll(static_cast<unsigned long long>(incl)) - 1 : 63;
+        const uint64_t need = p == 63 ? ~0ull : ((1ull << (p + 1)) - 1);
+        if ((ready & need) == need) {
+          ec += wave_sum64(lane <= p ? vc : 0);
+          et += wave_sum64(lane <= p ? vt : 0);
+          if (incl) break;
+          j -= 64;
+        } else {
+          // lanes below the first unpublished one hold block totals only
+          const int q = __ffsll(static_cast<unsigned long long>(~ready)) - 1;
+          if (q > 0) {
+            ec += wave_sum64(lane < q ? vc : 0);
+            et += wave_sum64(lane < q ? vt : 0);
+            j -= q;
+          } else if (++spins > LB_SPIN_LIMIT) {
+            if (lane == 0) set_status(ctr, AIQ_DEV_SCAN_WAIT);
+            break;
+          } else {
+            __builtin_amdgcn_s_sleep(1);
+          }
+        }
+      }
+      if (lane == 0) {
+        lb_put(me + 1, ec + cnt);
+        lb_put(me + 2, et + tok);
+      }
+    }
+    if (lane == 0) {
+      sb[0] = ec;
+      sb[1] = et;
+    }
+  }
+  __syncthreads();
+  const int64_t cb = sb[0], tb = sb[1];
+  bool overflow = false;
+  for (int i = t; i < cnt; i += LB_THREADS) {
+    const int64_t pos = cb + i;
+    const int32_t id = static_cast<int32_t>(base + rows[i]);
+    if (pos < out_cap) out_ids[pos] = id;
+    else overflow = true;
+    if (out_ids2) {
+      if (pos < out_cap2) out_ids2[pos] = id;
+      else overflow = true;
+    }
+    if (off) cu[pos] = tb + tx[lb_pad(i)];
+  }
+  if (join && out_payload) {   // the build payload of each survivor's match
+    for (int i = t; i < cnt; i += LB_THREADS) {
+      const int64_t r = base + rows[i];
+      const int32_t slot = hash_find(h, static_cast<int32_t>(load_int(probe_key, pk_dt, r)));
+      out_payload[cb + i] = slot >= 0 ? h.vals[slot] : 0;
+    }
+  }
+  if (overflow) set_status(ctr, AIQ_DEV_IDS_CAP);
+  if (b == nb - 1 && t == 0) {
+    ctr[C_SEL] = cb + cnt;
+    if (off) {
+      ctr[C_TOK] = tb + tok;
+      cu[cb + cnt] = tb + tok;
+    }
+  }
+}
+
+hipError_t launch_select_lb(const DPredList& preds, int64_t n_rows, const void* probe_key, int32_t probe_key_dtype,
+                            HashArgs h, int join, int32_t* out_ids, int64_t out_cap, int32_t* out_ids2,
+                            int64_t out_cap2, int32_t* out_payload, const int64_t* off, int32_t max_len,
+                            int32_t n_prefix, int64_t* cu, int64_t* lb, int64_t* ctr, hipStream_t s) {
+  const int64_t nb = (n_rows + LB_ROWS - 1) / LB_ROWS;
+  if (nb == 0) return hipSuccess;
+  hipError_t e = launch_fill_i64(lb, 4 * nb, 0, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_select_lb, dim3(static_cast<unsigned>(nb)), dim3(LB_THREADS), 0, s, preds, n_rows, nb,
+                     probe_key, probe_key_dtype, h, join, out_ids, out_cap, out_ids2, out_cap2, out_payload, off,
+                     max_len, n_prefix, cu, lb, ctr);
   return hipGetLastError();
 }
 

@@ -183,7 +183,7 @@ class DeviceQuery:
 
     def __init__(self, tables: dict, model, query, device="cuda", chunk_tokens: int = 0,
                  n_layers: int | None = None, dmodel: DeviceModel | None = None, relational_only: bool = False,
-                 want_sel: bool = True, share_prefix: bool = True):
+                 want_sel: bool = True, share_prefix: bool = True, multipass_compact: bool = False):
         self.device = torch.device(device)
         self.query = query
         self.dm = dmodel if dmodel is not None else DeviceModel(model, device)
@@ -194,7 +194,8 @@ class DeviceQuery:
         opts.chunk_tokens = int(chunk_tokens)
         opts.n_layers_override = _layers_opt(n_layers)
         opts.flags = (B.AIQ_PLAN_RELATIONAL_ONLY if relational_only else 0) | \
-            (0 if share_prefix else B.AIQ_PLAN_UNSHARED_PREFIX)
+            (0 if share_prefix else B.AIQ_PLAN_UNSHARED_PREFIX) | \
+            (B.AIQ_PLAN_MULTIPASS_COMPACT if multipass_compact else 0)
         self.plan = B.aiq_plan_create(self.dm.struct, self.probe.struct,
                                       self.build.struct if self.build else None, self.q, opts)
         self.ws_bytes = B.aiq_workspace_size(self.plan)

@@ -179,7 +179,9 @@ def test_relational_only_plan_validation():
     assert B.aiq_plan_create_status(model(), table(), None, q) == B.AIQ_OK
     assert B.aiq_plan_create_status(model(), table(), None, q, _opts(B.AIQ_PLAN_RELATIONAL_ONLY)) == B.AIQ_EINVAL
     # unknown flag bits
-    assert B.aiq_plan_create_status(model(), table(), None, query(), _opts(4)) == B.AIQ_EINVAL
+    assert B.aiq_plan_create_status(model(), table(), None, query(), _opts(8)) == B.AIQ_EINVAL
+    assert B.aiq_plan_create_status(model(), table(), None, query(),
+                                    _opts(B.AIQ_PLAN_MULTIPASS_COMPACT)) == B.AIQ_OK
     assert B.aiq_plan_create_status(model(), table(), None, query(), _opts(B.AIQ_PLAN_UNSHARED_PREFIX)) == B.AIQ_OK
 
 
