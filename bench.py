@@ -43,16 +43,23 @@ PEAK_HBM_GBPS = 8000.0
 # profiles/reviews_pipeline_hbm_traffic.md.  Valid only for the kernel source
 # it was measured on: reported as null once gemm.hip, dev_util.h or the
 # GemmArgs declaration change.
-GATE_UP_TRAFFIC = {"workload": "reviews", "tokens": 472953, "bytes": 4855867160,
-                   "source_sha256": "c566ae79b62ac4b9cd44d1a6a980ff9b29bce0908cec8a9405de6f35c11c3e47"}
+GATE_UP_TRAFFIC = {"workload": "reviews", "tokens": 472953, "bytes": 4852882149,
+                   "source_sha256": "d3cdcca5580dd5c36e6123776470b623383dffd8a5bd569f32b76c3d96eb90a0"}
 
 
 def gemm_source_sha256() -> str:
+    """Hash of the projection GEMM's sources: gemm.hip, dev_util.h and the
+    GemmArgs declaration in aiq_internal.h."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("gemm.hip", "aiq_internal.h", "dev_util.h"):
-        with open(os.path.join(ROOT, "paper_2608_10139_amd", "csrc", f), "rb") as fh:
+    csrc = os.path.join(ROOT, "paper_2608_10139_amd", "csrc")
+    for f in ("gemm.hip", "dev_util.h"):
+        with open(os.path.join(csrc, f), "rb") as fh:
             h.update(fh.read())
+    with open(os.path.join(csrc, "aiq_internal.h")) as fh:
+        text = fh.read()
+    start = text.index("struct GemmArgs")
+    h.update(text[start:text.index("};", start)].encode())
     return h.hexdigest()
 
 
@@ -450,9 +457,13 @@ def main(argv=None) -> int:
     dq = DeviceQuery(tables, model, q, dmodel=dm, share_prefix=not a.unshared_prefix)
     log(f"[bench] workspace {dq.ws_bytes / 2**30:.2f} GiB; warmup {a.warmup}")
 
-    for _ in range(a.warmup):
+    step_s = 0.0
+    for i in range(a.warmup):
+        t_w = time.perf_counter()
         dq.run()
-    torch.cuda.synchronize()
+        torch.cuda.synchronize()
+        step_s = time.perf_counter() - t_w
+        log(f"[bench] warm-up step {i + 1}/{a.warmup} done in {step_s:.3f} s")
     res = dq.results()
     if res["status"] != 0:
         raise RuntimeError(f"device status {res['status']:#x}")
@@ -477,8 +488,12 @@ def main(argv=None) -> int:
     log(f"[bench] timing {a.steps} steps")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(a.steps):
+    long_steps = step_s > 30.0   # minutes-long queries: report each step as it ends
+    for i in range(a.steps):
         dq.run(trace=trace)
+        if long_steps:
+            torch.cuda.synchronize()
+            log(f"[bench] timed step {i + 1}/{a.steps} done at {time.perf_counter() - t0:.1f} s")
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     ms_step = dt / a.steps * 1e3
