@@ -113,30 +113,50 @@ def per_kind_ms(B, trace, events) -> dict:
 
 
 # ------------------------------------------------------------------ algorithmic work
-def prefill_flops(spec, own: np.ndarray, n_labels: int, npre: int = 0, shared: bool = False) -> dict:
+def prefill_flops(spec, own: np.ndarray, n_labels: int, npre: int = 0, shared: bool = False,
+                  last_rows_only: bool = False) -> dict:
     """Algorithmic FLOPs of the prefill (no padding): the four projections,
     causal attention (unmasked half: QK^T and PV), and the label head.
     own: each selected row's token count; npre: prompt prefix length, packed
     into every row, or with ``shared`` prefilled once and attended to by
-    every row's own positions npre.. ."""
+    every row's own positions npre.. .  With ``last_rows_only`` the last
+    layer needs keys and values at every position but its query, attention
+    (one query over the sequence's keys), O projection and FFN at the last
+    position of each sequence only ("last"; the shared prefix pass is one
+    more sequence).  Keys qkv / o / up / down / attn cover the launches
+    traced under those kinds."""
     own = np.asarray(own, dtype=np.float64)
+    n = float(len(own))
     d, dq, dkv, f, L = spec.d_model, spec.d_q, spec.d_kv, spec.d_ff, spec.n_layers
     n_ffn = 3 if spec.act == "swiglu" else 2
     if shared and npre > 0:
-        T = float(own.sum()) + npre
-        attn = float(np.sum(2.0 * dq * (2.0 * npre * own + own * (own + 1.0)))) + 2.0 * dq * npre * (npre + 1.0)
+        T_rows, T_pre = float(own.sum()), float(npre)
+        attn_rows = float(np.sum(2.0 * dq * (2.0 * npre * own + own * (own + 1.0))))
+        attn_pre = 2.0 * dq * npre * (npre + 1.0)
+        keys = own + npre
     else:
         lens = own + npre
-        T = float(lens.sum())
-        attn = float(np.sum(2.0 * dq * lens * (lens + 1.0)))
+        T_rows, T_pre = float(lens.sum()), 0.0
+        attn_rows, attn_pre = float(np.sum(2.0 * dq * lens * (lens + 1.0))), 0.0
+        keys = lens
+    Lf = L - 1 if last_rows_only else L   # layers run on every position
+    T_full = (T_rows + T_pre) * Lf
     per = {
-        "qkv": 2 * T * d * (dq + 2 * dkv) * L,
-        "o": 2 * T * dq * d * L,
-        "up": 2 * T * d * f * (n_ffn - 1) * L,
-        "down": 2 * T * f * d * L,
-        "attn": attn * L,
-        "head": 2.0 * len(own) * n_labels * d,
+        "qkv": 2 * d * (dq + 2 * dkv) * T_full,
+        "o": 2 * dq * d * T_full,
+        "up": 2 * d * f * (n_ffn - 1) * T_full,
+        "down": 2 * f * d * T_full,
+        "attn": (attn_rows + attn_pre) * Lf,
+        "last": 0.0,
+        "head": 2.0 * n * n_labels * d,
     }
+    if last_rows_only and L > 0:
+        n_last = n + (1.0 if T_pre else 0.0)   # the prefix pass's own last position
+        keys_all = float(np.sum(keys)) + T_pre
+        # keys and values everywhere, the query at the last positions only
+        per["qkv"] += 2 * d * 2 * dkv * (T_rows + T_pre) + 2 * d * dq * n_last
+        # one query over each sequence's keys (QK^T and PV), O, FFN on those rows
+        per["last"] = 4.0 * dq * keys_all + n_last * (2 * dq * d + 2 * d * f * (n_ffn - 1) + 2 * f * d)
     per["total"] = sum(per.values())
     return per
 
@@ -401,6 +421,9 @@ def main(argv=None) -> int:
                     help="only the relational part at 2^26 and 2^28 rows (relational-only plans); one JSON line")
     ap.add_argument("--multipass-compact", action="store_true",
                     help="with --relational-scale: separate mask / scan / scatter launches instead of one")
+    ap.add_argument("--full-last-layer", action="store_true",
+                    help="run the last layer on every position (default: its attention, O projection and FFN "
+                         "for the last position of each sequence only)")
     ap.add_argument("--no-relational-scale", action="store_true",
                     help="skip the 2^26-row relational run of the default line")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -454,7 +477,8 @@ def main(argv=None) -> int:
     model = make_model(spec)
     dm = DeviceModel(model, compute=a.compute)
     shared = q.n_prefix > 0 and dm.compute != "f32" and not a.unshared_prefix
-    dq = DeviceQuery(tables, model, q, dmodel=dm, share_prefix=not a.unshared_prefix)
+    dq = DeviceQuery(tables, model, q, dmodel=dm, share_prefix=not a.unshared_prefix,
+                     full_last_layer=a.full_last_layer)
     log(f"[bench] workspace {dq.ws_bytes / 2**30:.2f} GiB; warmup {a.warmup}")
 
     step_s = 0.0
@@ -482,7 +506,10 @@ def main(argv=None) -> int:
     # every prefill pass (chunk, or the shared prefix) launches the gate/up GEMM once per layer
     chunks, pre_pass = B.aiq_plan_passes(dq.plan)
     passes = chunks + pre_pass
-    launches_per_step = spec.n_layers * passes
+    last_rows_only = B.aiq_plan_last_layer_rows(dq.plan)
+    # with the last layer on the last positions only, each pass's last gate/up
+    # runs on those rows and is traced as part of that layer
+    launches_per_step = (spec.n_layers - (1 if last_rows_only else 0)) * passes
     ev = HipEvents(2 * a.steps * launches_per_step)
     trace = make_trace(B, ev, 1 << B.AIQ_K_GEMM_UP)
     log(f"[bench] timing {a.steps} steps")
@@ -501,7 +528,7 @@ def main(argv=None) -> int:
         raise RuntimeError(f"traced {trace.count} gate/up launches, expected {a.steps * launches_per_step}")
     up = per_kind_ms(B, trace, ev).get(B.AIQ_K_GEMM_UP, [])
     ev.close()
-    fl = prefill_flops(spec, own, len(q.labels), q.n_prefix, shared)
+    fl = prefill_flops(spec, own, len(q.labels), q.n_prefix, shared, last_rows_only)
     # every launch of the gate/up GEMM covers one chunk (or the shared prefix);
     # chunks the selection leaves empty are launched and do no work
     n_up = len(up)
@@ -511,7 +538,8 @@ def main(argv=None) -> int:
     peak = PEAK_F32_TFLOPS if dm.compute == "f32" else PEAK_BF16_TFLOPS   # fp16 and bf16 MFMA peaks are equal
 
     # ---- one untimed traced step for the stage breakdown
-    ev2 = HipEvents(2 * (passes * (gen + 1) * (8 * spec.n_layers + 16) + 64))
+    last_blocks = 8 * (n_rows // 65536 + 1)   # the last layer's row blocks (at most 65,536 sequences each)
+    ev2 = HipEvents(2 * (passes * (gen + 1) * (8 * spec.n_layers + 16 + last_blocks) + 64))
     tr2 = make_trace(B, ev2, 0xFFFFFFFF)
     dq.run(trace=tr2)
     torch.cuda.synchronize()
@@ -523,10 +551,10 @@ def main(argv=None) -> int:
              B.AIQ_K_GEMM_QKV: "gemm_qkv_rope", B.AIQ_K_ATTN: "attention", B.AIQ_K_GEMM_O: "gemm_o_resid",
              B.AIQ_K_GEMM_UP: "gemm_gate_up_swiglu", B.AIQ_K_GEMM_DOWN: "gemm_down_resid", B.AIQ_K_HEAD: "head",
              B.AIQ_K_AGG: "decision_agg", B.AIQ_K_DECODE: "gen_layers", B.AIQ_K_DECODE_ATTN: "gen_attention",
-             B.AIQ_K_DECODE_HEAD: "gen_vocab_head_argmax_like"}
+             B.AIQ_K_DECODE_HEAD: "gen_vocab_head_argmax_like", B.AIQ_K_LAST: "last_layer_last_positions"}
     stages = {names[k]: round(float(np.sum(v)), 4) for k, v in sorted(kinds.items())}
     prefill_kinds = [B.AIQ_K_EMBED, B.AIQ_K_NORM, B.AIQ_K_GEMM_QKV, B.AIQ_K_ATTN, B.AIQ_K_GEMM_O,
-                     B.AIQ_K_GEMM_UP, B.AIQ_K_GEMM_DOWN, B.AIQ_K_HEAD]
+                     B.AIQ_K_GEMM_UP, B.AIQ_K_GEMM_DOWN, B.AIQ_K_HEAD, B.AIQ_K_LAST]
     prefill_ms = sum(float(np.sum(kinds.get(k, []))) for k in prefill_kinds)
     gemm = {"gemm_qkv_rope": ("qkv", B.AIQ_K_GEMM_QKV), "gemm_o_resid": ("o", B.AIQ_K_GEMM_O),
             "gemm_gate_up_swiglu": ("up", B.AIQ_K_GEMM_UP), "gemm_down_resid": ("down", B.AIQ_K_GEMM_DOWN)}
@@ -554,6 +582,7 @@ def main(argv=None) -> int:
                    f"projections in {dm.compute} with fp32 accumulation",
                    "parallelism": "single GPU"},
         "prompt_prefix": {"tokens": q.n_prefix, "shared": shared} if q.n_prefix else None,
+        "last_layer": "last positions only" if last_rows_only else "every position",
         "prefill_flops": fl["total"],
         "tokens_per_s": round(T / (ms_step * 1e-3), 1),
         "prefill_tokens_per_s": round(T / (prefill_ms * 1e-3), 1) if prefill_ms > 0 else None,

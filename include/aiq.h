@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define AIQ_ABI_VERSION 4
+#define AIQ_ABI_VERSION 5
 
 typedef enum aiq_status {
   AIQ_OK = 0,
@@ -279,6 +279,20 @@ typedef struct aiq_plan_opts {
 #define AIQ_PLAN_MULTIPASS_COMPACT 4
 
 /*
+ * The label head (Figure 2: the logits of the last position only) reads one
+ * row per sequence, and in a causal decoder the last layer's rows after its
+ * q|k|v projection feed no other position.  On 16-bit models (head dim 64 or
+ * 128) aiq_run and aiq_prefill_packed therefore run the last layer's keys and
+ * values for every position but its attention (one query per sequence, over
+ * the sequence's keys), O projection, norm and FFN for the last position of
+ * each sequence only.  The logits are the same function of the inputs; the
+ * last layer's attention then sums in a different order than the full-layer
+ * kernel, so they agree with the full computation to rounding, not bit for
+ * bit.  AIQ_PLAN_FULL_LAST_LAYER: run the last layer on every position.
+ */
+#define AIQ_PLAN_FULL_LAST_LAYER 8
+
+/*
  * Outputs, all device buffers owned by the caller.  Optional buffers may be
  * NULL.  Row ids are probe-table row indices.
  */
@@ -344,7 +358,8 @@ enum {
   AIQ_K_AGG = 10,
   AIQ_K_DECODE = 11,      /* AI_TRANSFORM generation steps: embedding, projections, norms */
   AIQ_K_DECODE_ATTN = 12, /* ... their attention over the kept keys and values */
-  AIQ_K_DECODE_HEAD = 13  /* ... the full-vocabulary head and argmax; the LIKE match */
+  AIQ_K_DECODE_HEAD = 13, /* ... the full-vocabulary head and argmax; the LIKE match */
+  AIQ_K_LAST = 14         /* the last layer after its q|k|v projection, last positions only */
 };
 
 typedef struct aiq_plan aiq_plan;
@@ -374,6 +389,17 @@ aiq_status aiq_workspace_size(const aiq_plan* plan, size_t* bytes);
  * (aiq_trace).  Errors: AIQ_EINVAL (NULL argument, prefill-only plan).
  */
 aiq_status aiq_plan_passes(const aiq_plan* plan, int64_t* chunks, int32_t* prefix_pass);
+
+/*
+ * *last_rows_only = 1 when the plan runs the last layer, after its q|k|v
+ * projection, for the last position of each sequence only (see
+ * AIQ_PLAN_FULL_LAST_LAYER), else 0.  In that case every prefill pass (the
+ * chunks and a shared prefix) launches the gate/up projection of every layer
+ * but the last over all its positions, and the last layer's attention, O
+ * projection, norm and FFN appear in traces as AIQ_K_LAST.
+ * Errors: AIQ_EINVAL (NULL argument).
+ */
+aiq_status aiq_plan_last_layer_rows(const aiq_plan* plan, int32_t* last_rows_only);
 
 /*
  * Enqueues the whole query on `stream`.  The workspace contents on entry do

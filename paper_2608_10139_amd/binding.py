@@ -13,7 +13,7 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libaiq.so")
 
-AIQ_ABI_VERSION = 4   # the struct layouts below
+AIQ_ABI_VERSION = 5   # the struct layouts below
 AIQ_OK, AIQ_EINVAL, AIQ_EUNSUPPORTED, AIQ_ENOSPC, AIQ_EHIP, AIQ_ENOMEM = 0, -1, -2, -3, -4, -5
 AIQ_I8, AIQ_I16, AIQ_I32, AIQ_F32, AIQ_BF16, AIQ_F16 = 1, 2, 3, 4, 5, 6
 AIQ_LT, AIQ_LE, AIQ_GT, AIQ_GE, AIQ_EQ, AIQ_NE, AIQ_IN = range(7)
@@ -24,6 +24,7 @@ AIQ_LOGITS_LABELS, AIQ_LOGITS_FULL_VOCAB = 1, 2
 AIQ_PLAN_RELATIONAL_ONLY = 1
 AIQ_PLAN_UNSHARED_PREFIX = 2
 AIQ_PLAN_MULTIPASS_COMPACT = 4
+AIQ_PLAN_FULL_LAST_LAYER = 8
 
 AIQ_DEV_TOKEN_RANGE, AIQ_DEV_DUP_KEY, AIQ_DEV_HASH_FULL, AIQ_DEV_IDS_CAP = 0x01, 0x02, 0x04, 0x08
 AIQ_DEV_GROUP_RANGE, AIQ_DEV_LIST_LEN, AIQ_DEV_GROUP_CAP, AIQ_DEV_PAIR_CAP = 0x10, 0x20, 0x40, 0x80
@@ -35,7 +36,7 @@ AIQ_MAX_GEN, AIQ_MAX_LIKE = 512, 16
 
 (AIQ_K_REL, AIQ_K_PACK, AIQ_K_EMBED, AIQ_K_NORM, AIQ_K_GEMM_QKV, AIQ_K_ATTN, AIQ_K_GEMM_O,
  AIQ_K_GEMM_UP, AIQ_K_GEMM_DOWN, AIQ_K_HEAD, AIQ_K_AGG, AIQ_K_DECODE, AIQ_K_DECODE_ATTN,
- AIQ_K_DECODE_HEAD) = range(14)
+ AIQ_K_DECODE_HEAD, AIQ_K_LAST) = range(15)
 
 OPS = {"lt": AIQ_LT, "le": AIQ_LE, "gt": AIQ_GT, "ge": AIQ_GE, "eq": AIQ_EQ, "ne": AIQ_NE, "in": AIQ_IN}
 
@@ -100,7 +101,8 @@ class aiq_trace(C.Structure):
                 ("capacity", C.c_int32), ("count", C.c_int32), ("kind_mask", C.c_uint32)]
 
 
-EXPORTS = ("aiq_plan_create", "aiq_workspace_size", "aiq_plan_passes", "aiq_run", "aiq_prefill_workspace_size",
+EXPORTS = ("aiq_plan_create", "aiq_workspace_size", "aiq_plan_passes", "aiq_plan_last_layer_rows", "aiq_run",
+           "aiq_prefill_workspace_size",
            "aiq_prefill_packed", "aiq_plan_destroy", "aiq_status_str", "aiq_abi_version")
 
 
@@ -129,6 +131,8 @@ def load(path: str = LIB_PATH) -> C.CDLL:
     lib.aiq_workspace_size.restype = C.c_int
     lib.aiq_plan_passes.argtypes = [P, C.POINTER(C.c_int64), C.POINTER(C.c_int32)]
     lib.aiq_plan_passes.restype = C.c_int
+    lib.aiq_plan_last_layer_rows.argtypes = [P, C.POINTER(C.c_int32)]
+    lib.aiq_plan_last_layer_rows.restype = C.c_int
     lib.aiq_run.argtypes = [P, P, C.c_size_t, C.POINTER(aiq_out), C.POINTER(aiq_trace), P]
     lib.aiq_run.restype = C.c_int
     lib.aiq_prefill_workspace_size.argtypes = [P, C.c_int64, C.POINTER(C.c_size_t)]
@@ -190,6 +194,13 @@ def aiq_plan_passes(plan) -> tuple:
     pp = C.c_int32()
     check("aiq_plan_passes", load().aiq_plan_passes(plan, C.byref(n), C.byref(pp)))
     return n.value, pp.value
+
+
+def aiq_plan_last_layer_rows(plan) -> bool:
+    """True when the plan runs its last layer for the last positions only."""
+    v = C.c_int32()
+    check("aiq_plan_last_layer_rows", load().aiq_plan_last_layer_rows(plan, C.byref(v)))
+    return bool(v.value)
 
 
 def aiq_prefill_workspace_size(plan, max_tokens: int) -> int:

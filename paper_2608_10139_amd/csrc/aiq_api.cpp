@@ -26,6 +26,10 @@ struct aiq_plan {
   // the prompt prefix is prefilled once per run and its keys / values are
   // shared by every row (16-bit models, unless AIQ_PLAN_UNSHARED_PREFIX)
   bool share_prefix = false;
+  // the last layer runs its rows after the q|k|v projection for the last
+  // position of each sequence only (16-bit models, unless
+  // AIQ_PLAN_FULL_LAST_LAYER)
+  bool prune_last = false;
   int32_t gen = 0;        // AI_TRANSFORM: tokens generated per selected row (0: AI_IF)
   bool pairs = false;     // Q4: the sequences are candidate pairs of selected rows
   int64_t n_seq_ub = 0;   // upper bound on sequences: selected rows, or max_pairs
@@ -149,7 +153,7 @@ struct Layout {
   size_t ctr, mask, blk_cnt, blk_off, sel, payload, lens, label, logits, cu, blk_tok, tok_off, packed, hkeys, hvals,
       bins, desc, rcos, rsin, rrev, x, delta, h, qkv, att, ffn, pos, hf, ssp, rs, pkv, ptok, pcu, pdesc, pxlast,
       kvc, gkv, glog, gtok, gdone, gen, gdesc, gcnt, kcount, koff, prank, psorted, pcnt, poff, pscan, pa, pb,
-      lb, total;
+      lb, xl, ldesc, total;
 };
 
 size_t act_bytes(const aiq_plan* p) { return p->bf16 ? 2 : 4; }
@@ -178,6 +182,24 @@ void take_resid(const aiq_plan* p, Carver& c, Layout& L, size_t T) {
   L.att = c.take(T * p->d_q * ab);
   L.ffn = c.take(T * p->model.d_ff * ab);
   L.pos = c.take((T + 256) * 4);   // GEMM tiles read positions up to the tile edge
+}
+
+// Last positions of a chunk go through the pruned last layer in blocks of at
+// most LAST_ROWS_MAX sequences.
+constexpr int64_t LAST_ROWS_MAX = 65536;
+
+int64_t last_rows(int64_t seq) { return std::max<int64_t>(std::min<int64_t>(seq, LAST_ROWS_MAX), 1); }
+int32_t last_blocks(int64_t seq) {
+  const int64_t R = last_rows(seq);
+  return static_cast<int32_t>(std::max<int64_t>((seq + R - 1) / R, 1));
+}
+
+// the pruned last layer's residual rows and block descriptors, for chunks of
+// at most `seq` sequences
+void take_last(const aiq_plan* p, Carver& c, Layout& L, int64_t seq) {
+  if (!p->prune_last) return;
+  L.xl = c.take(static_cast<size_t>(last_rows(seq)) * p->model.d_model * 4);
+  L.ldesc = c.take(static_cast<size_t>(last_blocks(seq)) * D_STRIDE * 8);
 }
 
 Layout run_layout(const aiq_plan* p) {
@@ -216,6 +238,7 @@ Layout run_layout(const aiq_plan* p) {
   L.rsin = c.take(static_cast<size_t>(p->max_seq) * (p->hd / 2) * 4);
   L.rrev = c.take(static_cast<size_t>(p->hd / 2) * 4);
   take_resid(p, c, L, static_cast<size_t>(p->t_cap));
+  take_last(p, c, L, p->seq_ub);
   L.hf = 0;
   if (p->share_prefix) {   // per-layer q|k|v rows of the prefix, its batch, its last token's final state
     const size_t np = static_cast<size_t>(p->prefix.n);
@@ -268,6 +291,7 @@ Layout prefill_layout(const aiq_plan* p, int64_t max_tokens) {
   L.rsin = c.take(T * (p->hd / 2) * 4);
   L.rrev = c.take(static_cast<size_t>(p->hd / 2) * 4);
   take_resid(p, c, L, T);
+  take_last(p, c, L, static_cast<int64_t>(T));   // sequences <= tokens
   L.hf = c.take(T * d * ab);
   L.total = c.off;
   return L;
@@ -351,12 +375,13 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
   const float* rrev = at<float>(ws, L.rrev);
   const float eps = static_cast<float>(m.norm_eps);
   auto gemm = [&](int epi, const void* A, int64_t lda, int N, int K, const void* B0, const void* B1, const void* B2,
-                  void* C, int64_t ldc, const float* gnext = nullptr) {
+                  void* C, int64_t ldc, const float* gnext = nullptr, const int64_t* rows_ptr = nullptr,
+                  int64_t rows_ub = 0, float* xr = nullptr) {
     GemmArgs g{};
     g.A = A;
     g.lda = lda;
-    g.m_ptr = m_ptr;
-    g.m_ub = t_cap;
+    g.m_ptr = rows_ptr ? rows_ptr : m_ptr;
+    g.m_ub = rows_ptr ? rows_ub : t_cap;
     g.N = N;
     g.K = K;
     g.B0 = B0;
@@ -374,7 +399,7 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
     g.f16 = p->act == 2;
     g.rs = rs;
     if (epi == EPI_RESID) {
-      g.x = x;
+      g.x = xr ? xr : x;
       g.gnext = gnext;
       g.hout = h;
       g.ssp = ssp;
@@ -382,6 +407,28 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
     }
     return p->bf16 ? launch_gemm_bf16(epi, g, s) : launch_gemm_f32(epi, g, s);
   };
+  HeadArgs ha{};
+  ha.desc = desc;
+  ha.cu = cu;
+  ha.x = x;
+  ha.delta = p->n_layers > 0 ? delta : nullptr;   // null on the MFMA path: x is complete
+  ha.g = m.final_norm;
+  ha.eps = eps;
+  ha.d = d;
+  ha.lm_head = m.lm_head;
+  ha.wdtype = m.wdtype;
+  ha.n_labels = (p->has_query && p->gen == 0) ? p->q.n_labels : 0;
+  for (int k = 0; k < ha.n_labels; ++k) ha.labels[k] = p->q.label_ids[k];
+  ha.decision = p->has_query ? p->q.decision : AIQ_DECIDE_BINARY_GT;
+  ha.label_out = ha.n_labels >= 2 ? label_out : nullptr;
+  ha.logits_out = ha.n_labels >= 2 ? logits_out : nullptr;
+  ha.hf_out = hf_out;
+  ha.hf_act = p->act;
+  ha.seq_ub = seq_ub;
+  ha.x_pre = pu.x_pre;
+  // the last layer for the last positions only (the prefix pass, which has
+  // no head, leaves its last position's final residual in row 0 of xl)
+  const bool prune = p->prune_last;
 
   if (p->bf16) {
     // MFMA path: each RMSNorm is split between the producer of its input and
@@ -416,6 +463,52 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
       aa.hd = p->hd;
       aa.seq_ub = seq_ub;
       aa.out_act = p->act;
+      if (last && prune) {
+        // blocks of R sequences: attention of each last position over its
+        // sequence (decode form), then O, norm, FFN and the head on those rows
+        const int64_t R = last_rows(seq_ub);
+        const int32_t nb = last_blocks(seq_ub);
+        int64_t* ldesc = at<int64_t>(ws, L.ldesc);
+        float* xl = at<float>(ws, L.xl);
+        const size_t hf_row = static_cast<size_t>(d) * (p->act ? 2 : 4);
+        TRACED(tr, AIQ_K_LAST, launch_last_desc(desc, ldesc, nb, R, s));
+        for (int32_t b = 0; b < nb; ++b) {
+          const int64_t* bd = ldesc + static_cast<int64_t>(b) * D_STRIDE;
+          GenAttnArgs ga{};
+          ga.kvc = qkv_l;
+          ga.pkv = aa.pkv;
+          ga.npre = aa.npre;
+          ga.ld = p->n_qkv;
+          ga.gen_desc = bd;
+          ga.chunk_desc = desc;
+          ga.cu = cu;
+          ga.out = att;
+          ga.n_heads = m.n_heads;
+          ga.n_kv = m.n_kv_heads;
+          ga.hd = p->hd;
+          ga.out_act = p->act;
+          ga.seq_ub = R;
+          ga.last_row = 1;
+          TRACED(tr, AIQ_K_LAST, launch_attention_gen(ga, s));
+          TRACED(tr, AIQ_K_LAST, launch_last_rows(bd, cu, x, d, xl, R, s));
+          TRACED(tr, AIQ_K_LAST, gemm(EPI_RESID, att, p->d_q, d, p->d_q, W.wo, nullptr, nullptr, nullptr, d,
+                                      W.ffn_norm, bd + D_NTOK, R, xl));
+          TRACED(tr, AIQ_K_LAST, launch_row_scale(bd, ssp, d / 64, d, eps, rs, R, s));
+          TRACED(tr, AIQ_K_LAST, gemm(EPI_SWIGLU, h, d, 2 * m.d_ff, d, W.w_gate, W.w_up, nullptr, ffn, m.d_ff,
+                                      nullptr, bd + D_NTOK, R));
+          TRACED(tr, AIQ_K_LAST, gemm(EPI_RESID, ffn, m.d_ff, d, m.d_ff, W.w_down, nullptr, nullptr, nullptr, d,
+                                      nullptr, bd + D_NTOK, R, xl));
+          if (!pu.head) continue;
+          HeadArgs hb = ha;
+          hb.desc = bd;
+          hb.x = xl;
+          hb.x_compact = 1;
+          hb.seq_ub = R;
+          hb.hf_out = hf_out ? static_cast<char*>(hf_out) + static_cast<size_t>(b) * R * hf_row : nullptr;
+          TRACED(tr, AIQ_K_HEAD, launch_head(hb, s));
+        }
+        break;
+      }
       TRACED(tr, AIQ_K_ATTN, launch_attention_bf16(aa, s));
       TRACED(tr, AIQ_K_GEMM_O, gemm(EPI_RESID, att, p->d_q, d, p->d_q, W.wo, nullptr, nullptr, nullptr, d,
                                     W.ffn_norm));
@@ -457,26 +550,7 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
     TRACED(tr, AIQ_K_GEMM_DOWN, gemm(EPI_STORE_F32, ffn, m.d_ff, d, m.d_ff, W.w_down, nullptr, nullptr, delta, d));
   }
   }
-  if (!pu.head) return AIQ_OK;
-  HeadArgs ha{};
-  ha.desc = desc;
-  ha.cu = cu;
-  ha.x = x;
-  ha.delta = p->n_layers > 0 ? delta : nullptr;   // null on the MFMA path: x is complete
-  ha.g = m.final_norm;
-  ha.eps = eps;
-  ha.d = d;
-  ha.lm_head = m.lm_head;
-  ha.wdtype = m.wdtype;
-  ha.n_labels = (p->has_query && p->gen == 0) ? p->q.n_labels : 0;
-  for (int k = 0; k < ha.n_labels; ++k) ha.labels[k] = p->q.label_ids[k];
-  ha.decision = p->has_query ? p->q.decision : AIQ_DECIDE_BINARY_GT;
-  ha.label_out = ha.n_labels >= 2 ? label_out : nullptr;
-  ha.logits_out = ha.n_labels >= 2 ? logits_out : nullptr;
-  ha.hf_out = hf_out;
-  ha.hf_act = p->act;
-  ha.seq_ub = seq_ub;
-  ha.x_pre = pu.x_pre;
+  if (!pu.head || prune) return AIQ_OK;   // pruned: the head ran per block of last positions
   TRACED(tr, AIQ_K_HEAD, launch_head(ha, s));
   return AIQ_OK;
 }
@@ -648,6 +722,12 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
   p->bf16 = model->wdtype == AIQ_BF16 || model->wdtype == AIQ_F16;
   p->act = model->wdtype == AIQ_F16 ? 2 : model->wdtype == AIQ_BF16 ? 1 : 0;
   p->n_up = p->bf16 ? 2 * model->d_ff : model->d_ff;
+  {
+    const int rep = model->n_kv_heads > 0 ? model->n_heads / model->n_kv_heads : 0;
+    p->prune_last = p->bf16 && p->n_layers > 0 && (p->hd == 64 || p->hd == 128) &&
+                    (rep == 1 || rep == 2 || rep == 3 || rep == 4 || rep == 8) &&
+                    !(opts && (opts->flags & AIQ_PLAN_FULL_LAST_LAYER));
+  }
 
   if (query) {
     p->has_query = true;
@@ -675,7 +755,8 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
     if (!query) return fail(AIQ_EINVAL);
     p->has_probe = true;
     p->rel_only = opts && (opts->flags & AIQ_PLAN_RELATIONAL_ONLY);
-    if (opts && (opts->flags & ~(AIQ_PLAN_RELATIONAL_ONLY | AIQ_PLAN_UNSHARED_PREFIX | AIQ_PLAN_MULTIPASS_COMPACT)))
+    if (opts && (opts->flags & ~(AIQ_PLAN_RELATIONAL_ONLY | AIQ_PLAN_UNSHARED_PREFIX | AIQ_PLAN_MULTIPASS_COMPACT |
+                                 AIQ_PLAN_FULL_LAST_LAYER)))
       return fail(AIQ_EINVAL);
     st = copy_table(probe, &p->probe, &p->probe_cols, p->rel_only ? 1 : 2);
     if (st != AIQ_OK) return fail(st);
@@ -790,6 +871,12 @@ aiq_status aiq_plan_passes(const aiq_plan* plan, int64_t* chunks, int32_t* prefi
   if (!plan || !chunks || !prefix_pass || !plan->has_probe) return AIQ_EINVAL;
   *chunks = plan->rel_only ? 0 : plan->n_chunks;
   *prefix_pass = plan->share_prefix ? 1 : 0;
+  return AIQ_OK;
+}
+
+aiq_status aiq_plan_last_layer_rows(const aiq_plan* plan, int32_t* last_rows_only) {
+  if (!plan || !last_rows_only) return AIQ_EINVAL;
+  *last_rows_only = plan->prune_last ? 1 : 0;
   return AIQ_OK;
 }
 
@@ -942,8 +1029,10 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
                                        s, pre_pu);
     if (e != AIQ_OK) return e;
     float* pxl = at<float>(ws, L.pxlast);
-    HIP_TRY(launch_copy_row_f32(at<float>(ws, L.x) + static_cast<int64_t>(np - 1) * p->model.d_model, pxl,
-                                p->model.d_model, s));
+    // the prefix's last position: row np - 1 of x, or row 0 of the pruned last layer's rows
+    const float* xsrc = p->prune_last ? at<float>(ws, L.xl)
+                                      : at<float>(ws, L.x) + static_cast<int64_t>(np - 1) * p->model.d_model;
+    HIP_TRY(launch_copy_row_f32(xsrc, pxl, p->model.d_model, s));
     rows_pu.pkv_layers = at<void>(ws, L.pkv);
     rows_pu.npre = np;
     rows_pu.x_pre = pxl;

@@ -260,6 +260,7 @@ struct HeadArgs {
   int64_t seq_ub;
   const float* x_pre;        // shared prefix: final residual of its last token, used by
                              // sequences with no own token (null: such sequences get 0 logits)
+  int32_t x_compact;         // 1: x holds one row per sequence of desc (row i), not [T, d]
 };
 hipError_t launch_head(const HeadArgs& a, hipStream_t s);
 
@@ -337,8 +338,20 @@ struct GenAttnArgs {
   void* out;                 // [n, n_heads * hd]
   int32_t n_heads, n_kv, hd, out_act;
   int64_t seq_ub;
+  // 1: the query of sequence i is its own last row in kvc and the keys are
+  // the prefix and its own rows only (no generated tokens; qkv, gkv, step and
+  // gen unused); sequences with no own row are skipped
+  int32_t last_row;
 };
 hipError_t launch_attention_gen(const GenAttnArgs& a, hipStream_t s);
+// Descriptors of the last positions of a chunk's sequences in blocks of R:
+// block b (b < nb) covers local sequences [b R, min(n, (b + 1) R)):
+// ldesc[b] = {chunk's first token, rows, chunk's first sequence + b R, rows}.
+hipError_t launch_last_desc(const int64_t* chunk_desc, int64_t* ldesc, int32_t nb, int64_t R, hipStream_t s);
+// xl[i] = x[last row of sequence i] (fp32 rows of d), i < ldesc[D_NSEQ];
+// sequences with no own row are left as they are.
+hipError_t launch_last_rows(const int64_t* ldesc, const int64_t* cu, const float* x, int32_t d, float* xl,
+                            int64_t R, hipStream_t s);
 // hf[i] = x[i] / rms * g in 16 bits, i < gen_desc[D_NSEQ]
 hipError_t launch_norm_rows(const int64_t* gen_desc, const float* x, const float* g, int32_t d, float eps, void* hf,
                             int32_t act, int64_t seq_ub, hipStream_t s);

@@ -55,6 +55,53 @@ hipError_t launch_gen_desc(const int64_t* chunk_desc, int64_t* gen_desc, int64_t
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ last positions of a chunk
+// The label head needs only each sequence's last position, and in the last
+// layer nothing after the q|k|v projection feeds any other position: that
+// layer's attention (for the last query), O projection, norm and FFN run on
+// one row per sequence, in blocks of R sequences.
+__global__ void k_last_desc(const int64_t* cd, int64_t* ld, int32_t nb, int64_t R) {
+  const int64_t n = cd[D_NSEQ];
+  for (int b = threadIdx.x; b < nb; b += blockDim.x) {
+    int64_t r = n - static_cast<int64_t>(b) * R;
+    r = r < 0 ? 0 : (r > R ? R : r);
+    int64_t* o = ld + static_cast<int64_t>(b) * D_STRIDE;
+    o[D_TOK_BEGIN] = cd[D_TOK_BEGIN];
+    o[D_NTOK] = r;
+    o[D_SEQ_BEGIN] = cd[D_SEQ_BEGIN] + static_cast<int64_t>(b) * R;
+    o[D_NSEQ] = r;
+  }
+}
+
+hipError_t launch_last_desc(const int64_t* chunk_desc, int64_t* ldesc, int32_t nb, int64_t R, hipStream_t s) {
+  if (nb <= 0 || R <= 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_last_desc, dim3(1), dim3(256), 0, s, chunk_desc, ldesc, nb, R);
+  return hipGetLastError();
+}
+
+// Wave per sequence, 16-byte pieces of the row.
+__global__ __launch_bounds__(256) void k_last_rows(const int64_t* ld, const int64_t* cu, const float* x, int32_t d,
+                                                   float* xl) {
+  const int64_t n = ld[D_NSEQ], sb = ld[D_SEQ_BEGIN], tb = ld[D_TOK_BEGIN];
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6;
+  const int64_t n_waves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t i = wave; i < n; i += n_waves) {
+    const int64_t c1 = cu[sb + i + 1];
+    if (c1 == cu[sb + i]) continue;
+    const float4* src = reinterpret_cast<const float4*>(x + (c1 - 1 - tb) * d);
+    float4* dst = reinterpret_cast<float4*>(xl + i * d);
+    for (int c = lane; c < d / 4; c += 64) dst[c] = src[c];
+  }
+}
+
+hipError_t launch_last_rows(const int64_t* ldesc, const int64_t* cu, const float* x, int32_t d, float* xl,
+                            int64_t R, hipStream_t s) {
+  if (d % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_last_rows, dim3(grid_for(R, 4, 8192)), dim3(256), 0, s, ldesc, cu, x, d, xl);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ embedding of the current tokens
 // Wave per sequence: x = E[tok], h = x * g (16-bit), rs = 1 / rms(x), and the
 // position after the prompt (shared prefix included) and the earlier steps.
@@ -140,12 +187,16 @@ __global__ __launch_bounds__(256) void k_attn_gen(GenAttnArgs a) {
     const int64_t i = item / a.n_kv;
     const int kvh = static_cast<int>(item % a.n_kv);
     const int64_t s0 = a.cu[sb + i] - tb;
-    const int P = a.npre + static_cast<int>(a.cu[sb + i + 1] - a.cu[sb + i]);   // prompt positions
-    const int N = P + a.step + 1;   // keys: the prompt, the earlier generated tokens, this token
-    const uint16_t* qrow = qkv + i * ld;
+    const int own = static_cast<int>(a.cu[sb + i + 1] - a.cu[sb + i]);
+    const int P = a.npre + own;   // prompt positions
+    if (a.last_row && own == 0) continue;   // no own row to attend from (same for the whole wave)
+    // keys: the prompt, the earlier generated tokens, this token (last-row
+    // mode: the prompt, whose last row is the query)
+    const int N = a.last_row ? P : P + a.step + 1;
+    const uint16_t* qrow = a.last_row ? kvc + (s0 + own - 1) * ld : qkv + i * ld;
     const int kc = d_q + kvh * HD, vc = d_q + d_kv + kvh * HD;   // key / value columns of a q|k|v row
-    uint16_t* gslot = gkv + (i * a.gen + a.step) * (2 * d_kv);
-    if (lane < 2 * LPK) {
+    uint16_t* gslot = a.last_row ? nullptr : gkv + (i * a.gen + a.step) * (2 * d_kv);
+    if (!a.last_row && lane < 2 * LPK) {
       const bool isv = lane >= LPK;
       const int cc = lane % LPK;
       *reinterpret_cast<uint4*>(gslot + (isv ? d_kv : 0) + kvh * HD + cc * 8) =
@@ -292,8 +343,8 @@ __global__ __launch_bounds__(256) void k_attn_gen(GenAttnArgs a) {
 }
 
 hipError_t launch_attention_gen(const GenAttnArgs& a, hipStream_t s) {
-  if (a.n_kv <= 0 || a.n_heads % a.n_kv || a.npre < 0 || (a.npre > 0 && !a.pkv) || a.step < 0 ||
-      a.step >= a.gen || a.out_act == ACT_F32)
+  if (a.n_kv <= 0 || a.n_heads % a.n_kv || a.npre < 0 || (a.npre > 0 && !a.pkv) || a.out_act == ACT_F32 ||
+      (!a.last_row && (a.step < 0 || a.step >= a.gen || !a.gkv || !a.qkv)))
     return hipErrorInvalidValue;
   const int rep = a.n_heads / a.n_kv;
   const dim3 grid(grid_for(a.seq_ub * a.n_kv, 4, 8192)), block(256);

@@ -121,7 +121,7 @@ __global__ __launch_bounds__(256) void k_head(HeadArgs a) {
     const bool no_own = a.cu[gi + 1] == a.cu[gi];
     const bool empty = no_own && !a.x_pre;
     const bool pre = no_own && a.x_pre;
-    const int64_t last = no_own ? 0 : a.cu[gi + 1] - 1 - tb;
+    const int64_t last = no_own ? 0 : (a.x_compact ? i : a.cu[gi + 1] - 1 - tb);
     const float* xr = pre ? a.x_pre : a.x + last * d;
     const float* dr = (a.delta && !pre) ? a.delta + last * d : nullptr;   // last layer's pending output
     auto xv = [&](int c) { return dr ? xr[c] + dr[c] : xr[c]; };

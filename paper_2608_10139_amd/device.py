@@ -183,7 +183,8 @@ class DeviceQuery:
 
     def __init__(self, tables: dict, model, query, device="cuda", chunk_tokens: int = 0,
                  n_layers: int | None = None, dmodel: DeviceModel | None = None, relational_only: bool = False,
-                 want_sel: bool = True, share_prefix: bool = True, multipass_compact: bool = False):
+                 want_sel: bool = True, share_prefix: bool = True, multipass_compact: bool = False,
+                 full_last_layer: bool = False):
         self.device = torch.device(device)
         self.query = query
         self.dm = dmodel if dmodel is not None else DeviceModel(model, device)
@@ -195,7 +196,8 @@ class DeviceQuery:
         opts.n_layers_override = _layers_opt(n_layers)
         opts.flags = (B.AIQ_PLAN_RELATIONAL_ONLY if relational_only else 0) | \
             (0 if share_prefix else B.AIQ_PLAN_UNSHARED_PREFIX) | \
-            (B.AIQ_PLAN_MULTIPASS_COMPACT if multipass_compact else 0)
+            (B.AIQ_PLAN_MULTIPASS_COMPACT if multipass_compact else 0) | \
+            (B.AIQ_PLAN_FULL_LAST_LAYER if full_last_layer else 0)
         self.plan = B.aiq_plan_create(self.dm.struct, self.probe.struct,
                                       self.build.struct if self.build else None, self.q, opts)
         self.ws_bytes = B.aiq_workspace_size(self.plan)
@@ -288,7 +290,7 @@ class DevicePrefill:
     """Prefill-only plan: runs the transformer on caller-packed sequences."""
 
     def __init__(self, model, labels=(1, 2), max_tokens: int = 4096, device="cuda",
-                 n_layers: int | None = None, dmodel: DeviceModel | None = None):
+                 n_layers: int | None = None, dmodel: DeviceModel | None = None, full_last_layer: bool = False):
         self.device = torch.device(device)
         self.dm = dmodel if dmodel is not None else DeviceModel(model, device)
         q = B.aiq_query()
@@ -301,6 +303,7 @@ class DevicePrefill:
         self.K = len(labels)
         opts = B.aiq_plan_opts()
         opts.n_layers_override = _layers_opt(n_layers)
+        opts.flags = B.AIQ_PLAN_FULL_LAST_LAYER if full_last_layer else 0
         self.plan = B.aiq_plan_create(self.dm.struct, None, None, q, opts)
         self.max_tokens = int(max_tokens)
         self.ws_bytes = B.aiq_prefill_workspace_size(self.plan, self.max_tokens)

@@ -179,9 +179,9 @@ def test_relational_only_plan_validation():
     assert B.aiq_plan_create_status(model(), table(), None, q) == B.AIQ_OK
     assert B.aiq_plan_create_status(model(), table(), None, q, _opts(B.AIQ_PLAN_RELATIONAL_ONLY)) == B.AIQ_EINVAL
     # unknown flag bits
-    assert B.aiq_plan_create_status(model(), table(), None, query(), _opts(8)) == B.AIQ_EINVAL
-    assert B.aiq_plan_create_status(model(), table(), None, query(),
-                                    _opts(B.AIQ_PLAN_MULTIPASS_COMPACT)) == B.AIQ_OK
+    assert B.aiq_plan_create_status(model(), table(), None, query(), _opts(16)) == B.AIQ_EINVAL
+    for flag in (B.AIQ_PLAN_MULTIPASS_COMPACT, B.AIQ_PLAN_FULL_LAST_LAYER):
+        assert B.aiq_plan_create_status(model(), table(), None, query(), _opts(flag)) == B.AIQ_OK
     assert B.aiq_plan_create_status(model(), table(), None, query(), _opts(B.AIQ_PLAN_UNSHARED_PREFIX)) == B.AIQ_OK
 
 
@@ -208,6 +208,29 @@ def test_plan_passes():
         assert B.aiq_plan_passes(chunked) == (10, 0)
     finally:
         for p in (shared, unshared, rel, chunked):
+            B.aiq_plan_destroy(p)
+
+
+def test_last_layer_rows_plan_flag():
+    """16-bit models run the last layer for the last positions only unless
+    AIQ_PLAN_FULL_LAST_LAYER; fp32 models and zero-layer plans never do."""
+    plans = {
+        "default": B.aiq_plan_create(model(), table(), None, query()),
+        "full": B.aiq_plan_create(model(), table(), None, query(), _opts(B.AIQ_PLAN_FULL_LAST_LAYER)),
+        "fp32": B.aiq_plan_create(model(wdtype=B.AIQ_F32, act=B.AIQ_ACT_GELU_ERF), table(), None, query()),
+    }
+    no_layer = B.aiq_plan_opts()
+    no_layer.n_layers_override = -1
+    plans["no_layer"] = B.aiq_plan_create(model(), table(), None, query(), no_layer)
+    try:
+        assert B.aiq_plan_last_layer_rows(plans["default"]) is True
+        assert B.aiq_plan_last_layer_rows(plans["full"]) is False
+        assert B.aiq_plan_last_layer_rows(plans["fp32"]) is False
+        assert B.aiq_plan_last_layer_rows(plans["no_layer"]) is False
+        # the pruned plan needs the compact last-layer rows on top
+        assert B.aiq_workspace_size(plans["default"]) > B.aiq_workspace_size(plans["full"])
+    finally:
+        for p in plans.values():
             B.aiq_plan_destroy(p)
 
 
