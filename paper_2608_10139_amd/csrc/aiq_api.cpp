@@ -376,7 +376,7 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
   const float eps = static_cast<float>(m.norm_eps);
   auto gemm = [&](int epi, const void* A, int64_t lda, int N, int K, const void* B0, const void* B1, const void* B2,
                   void* C, int64_t ldc, const float* gnext = nullptr, const int64_t* rows_ptr = nullptr,
-                  int64_t rows_ub = 0, float* xr = nullptr) {
+                  int64_t rows_ub = 0, float* xr = nullptr, bool x_table = false) {
     GemmArgs g{};
     g.A = A;
     g.lda = lda;
@@ -404,6 +404,13 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
       g.hout = h;
       g.ssp = ssp;
       g.n_part = d / 64;
+      if (x_table) {   // the residual before the first layer is the token's table row
+        epi = EPI_RESID_EMB;
+        g.x_emb = m.emb;
+        g.x_tok = packed;
+        g.x_tok_desc = desc;
+        g.vocab = m.vocab;
+      }
     }
     return p->bf16 ? launch_gemm_bf16(epi, g, s) : launch_gemm_f32(epi, g, s);
   };
@@ -438,7 +445,12 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
     // (x / rms * g) . W^T = ((x * g) . W^T) / rms.
     const float* g0 = p->n_layers > 0 ? p->layers[0].attn_norm : m.final_norm;
     const int32_t pos_base = pu.pkv_layers ? pu.npre : 0;
-    TRACED(tr, AIQ_K_EMBED, launch_embed_norm(desc, cu, packed, m.emb, m.wdtype, d, m.vocab, x, pos, ctr, g0, eps,
+    // x after the embedding is the table row itself: the first layer's O
+    // projection reads it from the table instead (unless that layer is the
+    // pruned last one, which gathers x rows)
+    const bool x_from_table = p->n_layers > 1 || (p->n_layers == 1 && !prune);
+    TRACED(tr, AIQ_K_EMBED, launch_embed_norm(desc, cu, packed, m.emb, m.wdtype, d, m.vocab,
+                                              x_from_table ? nullptr : x, pos, ctr, g0, eps,
                                               h, p->act, rs, t_cap, s, pos_base));
     const size_t pre_layer = static_cast<size_t>(pu.npre) * p->n_qkv * act_bytes(p);   // bytes per layer
     const size_t keep_layer = static_cast<size_t>(pu.qkv_rows) * p->n_qkv * act_bytes(p);
@@ -511,7 +523,7 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
       }
       TRACED(tr, AIQ_K_ATTN, launch_attention_bf16(aa, s));
       TRACED(tr, AIQ_K_GEMM_O, gemm(EPI_RESID, att, p->d_q, d, p->d_q, W.wo, nullptr, nullptr, nullptr, d,
-                                    W.ffn_norm));
+                                    W.ffn_norm, nullptr, 0, nullptr, l == 0 && x_from_table));
       TRACED(tr, AIQ_K_NORM, launch_row_scale(desc, ssp, d / 64, d, eps, rs, t_cap, s));
       TRACED(tr, AIQ_K_GEMM_UP, gemm(EPI_SWIGLU, h, d, 2 * m.d_ff, d, W.w_gate, W.w_up, nullptr, ffn, m.d_ff));
       // the head normalises the last position itself: after the last layer only x is needed

@@ -167,7 +167,8 @@ hipError_t launch_embed(const int64_t* desc, const int64_t* cu, const int32_t* p
 // MFMA path: the embedding also writes the first projection's operand
 // h = x * g (16-bit) and the row scale rs = 1 / sqrt(mean(x^2) + eps).
 // pos_base is added to every position (the row tokens that follow a shared
-// prefix start at the prefix length).
+// prefix start at the prefix length).  x may be null: the residual is then
+// not written (the first layer's O projection reads the embedding rows).
 hipError_t launch_embed_norm(const int64_t* desc, const int64_t* cu, const int32_t* packed, const void* emb,
                              int32_t wdtype, int32_t d, int32_t vocab, float* x, int32_t* pos, int64_t* ctr,
                              const float* g, float eps, void* h, int32_t h_act, float* rs, int64_t t_cap,
@@ -185,7 +186,8 @@ hipError_t launch_rmsnorm(const int64_t* desc, float* x, const float* delta, con
 // (fp32 bits of the maximum, its column) over each 64-column slice of a row,
 // the lowest column among equal maxima.
 enum Epi : int {
-  EPI_STORE_F32 = 0, EPI_QKV_ROPE = 1, EPI_SWIGLU = 3, EPI_GELU = 4, EPI_STORE_ACT = 5, EPI_RESID = 6, EPI_ARGMAX = 7
+  EPI_STORE_F32 = 0, EPI_QKV_ROPE = 1, EPI_SWIGLU = 3, EPI_GELU = 4, EPI_STORE_ACT = 5, EPI_RESID = 6, EPI_ARGMAX = 7,
+  EPI_RESID_EMB = 8   // EPI_RESID reading the residual from the embedding table (x_emb)
 };
 
 struct GemmArgs {
@@ -213,6 +215,14 @@ struct GemmArgs {
   void* hout;                // EPI_RESID: [M, ldc] 16-bit, x * gnext (the next projection's operand)
   float* ssp;                // EPI_RESID: [M, n_part] sums of x^2 over each 64-column slice
   int32_t n_part;            // ldc / 64
+  // EPI_RESID_EMB (first layer): the residual read is the embedding row of
+  // the row's token (16-bit table [vocab, ldc]; token =
+  // x_tok[x_tok_desc[D_TOK_BEGIN] + m], out of range read as 0), not x; x is
+  // still written.
+  const void* x_emb;
+  const int32_t* x_tok;
+  const int64_t* x_tok_desc;
+  int32_t vocab;
 };
 
 hipError_t launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t s);

@@ -96,6 +96,7 @@ template <> struct Op16<false> {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
   }
   static __device__ __forceinline__ uint16_t cvt(float f) { return f2bf(f); }
+  static __device__ __forceinline__ float widen(uint16_t u) { return __uint_as_float(static_cast<uint32_t>(u) << 16); }
 };
 template <> struct Op16<true> {
   typedef half8 V;
@@ -103,6 +104,7 @@ template <> struct Op16<true> {
     return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
   }
   static __device__ __forceinline__ uint16_t cvt(float f) { return f2h(f); }
+  static __device__ __forceinline__ float widen(uint16_t u) { return h2f(u); }
 };
 constexpr int GM = 256, GN = 256, GK = 64, GT = 512;
 
@@ -156,7 +158,7 @@ __device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4
   const int l32 = lane & 31, hi = lane >> 5;
   const int nw = n0 + wn * 64;   // first GEMM column of this wave
   const int64_t mw = m0 + wm * 128;   // first row of this wave's sub-tile
-  if (EPI == EPI_RESID) {
+  if (EPI == EPI_RESID || EPI == EPI_RESID_EMB) {
     // x += acc in place; with a following norm also h = x * g and, per row,
     // the sum of x^2 over this wave's 64 columns.  A slab of 32 rows x 64
     // columns goes through LDS; each lane then owns 4 columns of 8 rows, and
@@ -169,12 +171,26 @@ __device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4
     uint16_t* hout = static_cast<uint16_t*>(a.hout);
     const int part = nw >> 6;
     auto row_of = [&](int i, int k) { return mw + i * 32 + (lane >> 4) + 4 * k; };
+    // the residual before this projection: x, or (first layer) the token's
+    // embedding row widened from 16 bits, which is exactly what x would hold
+    const int64_t tok0 = EPI == EPI_RESID_EMB ? a.x_tok_desc[D_TOK_BEGIN] : 0;
     auto load_x = [&](int i, float4 (&v)[8]) {
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
         int64_t m = row_of(i, k);
         if (m > M - 1) m = M - 1;   // in bounds; the value is not used
-        v[k] = *reinterpret_cast<const float4*>(a.x + m * a.ldc + nw + cg);
+        if (EPI == EPI_RESID_EMB) {
+          int32_t tok = a.x_tok[tok0 + m];
+          if (tok < 0 || tok >= a.vocab) tok = 0;
+          const uint2 e = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(a.x_emb) +
+                                                          static_cast<int64_t>(tok) * a.ldc + nw + cg);
+          v[k] = make_float4(Op16<H>::widen(static_cast<uint16_t>(e.x & 0xFFFFu)),
+                             Op16<H>::widen(static_cast<uint16_t>(e.x >> 16)),
+                             Op16<H>::widen(static_cast<uint16_t>(e.y & 0xFFFFu)),
+                             Op16<H>::widen(static_cast<uint16_t>(e.y >> 16)));
+        } else {
+          v[k] = *reinterpret_cast<const float4*>(a.x + m * a.ldc + nw + cg);
+        }
       }
     };
     float4 xo[8];
@@ -223,7 +239,18 @@ __device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4
         if (i < 3) {   // the same row slot of the next slab
           int64_t mn = row_of(i + 1, k);
           if (mn > M - 1) mn = M - 1;
-          xo[k] = *reinterpret_cast<const float4*>(a.x + mn * a.ldc + nw + cg);
+          if (EPI == EPI_RESID_EMB) {
+            int32_t tok = a.x_tok[tok0 + mn];
+            if (tok < 0 || tok >= a.vocab) tok = 0;
+            const uint2 e = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(a.x_emb) +
+                                                            static_cast<int64_t>(tok) * a.ldc + nw + cg);
+            xo[k] = make_float4(Op16<H>::widen(static_cast<uint16_t>(e.x & 0xFFFFu)),
+                                Op16<H>::widen(static_cast<uint16_t>(e.x >> 16)),
+                                Op16<H>::widen(static_cast<uint16_t>(e.y & 0xFFFFu)),
+                                Op16<H>::widen(static_cast<uint16_t>(e.y >> 16)));
+          } else {
+            xo[k] = *reinterpret_cast<const float4*>(a.x + mn * a.ldc + nw + cg);
+          }
         }
       }
     }
@@ -503,7 +530,7 @@ __global__ __launch_bounds__(GT) void k_gemm_bf16(GemmArgs a) {
     if (w == 0 && (EPI == EPI_QKV_ROPE || EPI == EPI_SWIGLU) && a.rs)
       __builtin_amdgcn_global_load_lds(static_cast<const void*>(a.rs + m0 + lane * 4), (lds_ptr_t)(rbuf + lane * 4),
                                        16, 0, 0);
-    if (w == 0 && EPI == EPI_RESID && a.gnext)   // the following norm's gain for the tile's columns
+    if (w == 0 && (EPI == EPI_RESID || EPI == EPI_RESID_EMB) && a.gnext)   // the following norm's gain for the tile's columns
       __builtin_amdgcn_global_load_lds(static_cast<const void*>(a.gnext + n0 + lane * 4),
                                        (lds_ptr_t)(rbuf + lane * 4), 16, 0, 0);
     if (w == 1 && EPI == EPI_QKV_ROPE)
@@ -561,9 +588,15 @@ hipError_t launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t s) {
     case EPI_SWIGLU: AIQ_LAUNCH_GEMM(EPI_SWIGLU); break;
     case EPI_QKV_ROPE: AIQ_LAUNCH_GEMM(EPI_QKV_ROPE); break;
     case EPI_RESID:
+    case EPI_RESID_EMB:
       if (a.ldc != a.N || a.N % 64 || (a.gnext && (!a.hout || !a.ssp || a.n_part != a.N / 64)))
         return hipErrorInvalidValue;
-      AIQ_LAUNCH_GEMM(EPI_RESID);
+      if (epi == EPI_RESID_EMB) {
+        if (!a.x_emb || !a.x_tok || !a.x_tok_desc || a.vocab <= 0) return hipErrorInvalidValue;
+        AIQ_LAUNCH_GEMM(EPI_RESID_EMB);
+      } else {
+        AIQ_LAUNCH_GEMM(EPI_RESID);
+      }
       break;
     default: return hipErrorInvalidValue;
   }

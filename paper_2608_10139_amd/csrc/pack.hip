@@ -275,7 +275,7 @@ __global__ __launch_bounds__(256) void k_embed(const int64_t* desc, const int64_
     }
     const int64_t sq = seq_of(cu, sb, ns, gt, lane);
     if (lane == 0) pos[t] = pos_base + static_cast<int32_t>(gt - cu[sq]);
-    float* xr = x + t * d;
+    float* xr = x ? x + t * d : nullptr;   // null: x is not written (the first projection reads the table)
     float ssq = 0.f;
     for (int c = lane * 4; c < d; c += 256) {
       float4 o;
@@ -290,7 +290,7 @@ __global__ __launch_bounds__(256) void k_embed(const int64_t* desc, const int64_
       } else {
         o = *reinterpret_cast<const float4*>(static_cast<const float*>(emb) + static_cast<int64_t>(tok) * d + c);
       }
-      *reinterpret_cast<float4*>(xr + c) = o;
+      if (x) *reinterpret_cast<float4*>(xr + c) = o;
       if (NORM) {
         const float4 gv = *reinterpret_cast<const float4*>(g + c);
         uint2 hv;
