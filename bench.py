@@ -153,10 +153,11 @@ def prefill_flops(spec, own: np.ndarray, n_labels: int, npre: int = 0, shared: b
     if last_rows_only and L > 0:
         n_last = n + (1.0 if T_pre else 0.0)   # the prefix pass's own last position
         keys_all = float(np.sum(keys)) + T_pre
-        # keys and values everywhere, the query at the last positions only
-        per["qkv"] += 2 * d * 2 * dkv * (T_rows + T_pre) + 2 * d * dq * n_last
-        # one query over each sequence's keys (QK^T and PV), O, FFN on those rows
-        per["last"] = 4.0 * dq * keys_all + n_last * (2 * dq * d + 2 * d * f * (n_ffn - 1) + 2 * f * d)
+        # keys and values everywhere (traced with the q|k|v projections)
+        per["qkv"] += 2 * d * 2 * dkv * (T_rows + T_pre)
+        # the query projection, one query over each sequence's keys (QK^T and
+        # PV), O and FFN at the last positions
+        per["last"] = 4.0 * dq * keys_all + n_last * (2 * d * dq + 2 * dq * d + 2 * d * f * (n_ffn - 1) + 2 * f * d)
     per["total"] = sum(per.values())
     return per
 

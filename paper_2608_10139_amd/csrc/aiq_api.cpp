@@ -30,6 +30,9 @@ struct aiq_plan {
   // position of each sequence only (16-bit models, unless
   // AIQ_PLAN_FULL_LAST_LAYER)
   bool prune_last = false;
+  // ... and its q|k|v projection computes keys and values for every position
+  // but queries for the last positions only
+  bool q_last_only = false;
   int32_t gen = 0;        // AI_TRANSFORM: tokens generated per selected row (0: AI_IF)
   bool pairs = false;     // Q4: the sequences are candidate pairs of selected rows
   int64_t n_seq_ub = 0;   // upper bound on sequences: selected rows, or max_pairs
@@ -153,7 +156,7 @@ struct Layout {
   size_t ctr, mask, blk_cnt, blk_off, sel, payload, lens, label, logits, cu, blk_tok, tok_off, packed, hkeys, hvals,
       bins, desc, rcos, rsin, rrev, x, delta, h, qkv, att, ffn, pos, hf, ssp, rs, pkv, ptok, pcu, pdesc, pxlast,
       kvc, gkv, glog, gtok, gdone, gen, gdesc, gcnt, kcount, koff, prank, psorted, pcnt, poff, pscan, pa, pb,
-      lb, xl, ldesc, total;
+      lb, xl, ldesc, laux, total;
 };
 
 size_t act_bytes(const aiq_plan* p) { return p->bf16 ? 2 : 4; }
@@ -200,6 +203,8 @@ void take_last(const aiq_plan* p, Carver& c, Layout& L, int64_t seq) {
   if (!p->prune_last) return;
   L.xl = c.take(static_cast<size_t>(last_rows(seq)) * p->model.d_model * 4);
   L.ldesc = c.take(static_cast<size_t>(last_blocks(seq)) * D_STRIDE * 8);
+  // row scales and positions of the last positions (GEMM tiles read 256 rows)
+  if (p->q_last_only) L.laux = c.take(static_cast<size_t>(last_rows(seq) + 256) * 8);
 }
 
 Layout run_layout(const aiq_plan* p) {
@@ -414,6 +419,32 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
     }
     return p->bf16 ? launch_gemm_bf16(epi, g, s) : launch_gemm_f32(epi, g, s);
   };
+  // a section of the q|k|v projection (rotary on q and k columns): n_q query
+  // and n_kv key columns, then values, with its own rows, row scales and positions
+  auto gemm_part = [&](const void* A, const int64_t* rows_ptr, int64_t rows_ub, int N, int n_q, int n_kv,
+                       const void* B0, const void* B1, const void* B2, void* C, int64_t ldc, const float* rsr,
+                       const int32_t* posr) {
+    GemmArgs g{};
+    g.A = A;
+    g.lda = d;
+    g.m_ptr = rows_ptr;
+    g.m_ub = rows_ub;
+    g.N = N;
+    g.K = d;
+    g.B0 = B0;
+    g.B1 = B1;
+    g.B2 = B2;
+    g.n_q = n_q;
+    g.n_kv = n_kv;
+    g.hd = p->hd;
+    g.C = C;
+    g.ldc = ldc;
+    g.pos = posr;
+    g.rope_rev = rrev;
+    g.f16 = p->act == 2;
+    g.rs = rsr;
+    return launch_gemm_bf16(EPI_QKV_ROPE, g, s);
+  };
   HeadArgs ha{};
   ha.desc = desc;
   ha.cu = cu;
@@ -458,7 +489,14 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
       const aiq_layer& W = p->layers[l];
       const bool last = l + 1 == p->n_layers;
       void* qkv_l = pu.qkv_layers ? static_cast<char*>(pu.qkv_layers) + l * keep_layer : qkv;
-      TRACED(tr, AIQ_K_GEMM_QKV, gemm(EPI_QKV_ROPE, h, d, p->n_qkv, d, W.wq, W.wk, W.wv, qkv_l, p->n_qkv));
+      if (last && prune && p->q_last_only) {
+        // keys and values for every position (columns d_q.. of the q|k|v rows)
+        TRACED(tr, AIQ_K_GEMM_QKV, gemm_part(h, m_ptr, t_cap, 2 * p->d_kv, 0, p->d_kv, W.wq, W.wk, W.wv,
+                                             static_cast<char*>(qkv_l) + static_cast<size_t>(p->d_q) * act_bytes(p),
+                                             p->n_qkv, rs, pos));
+      } else {
+        TRACED(tr, AIQ_K_GEMM_QKV, gemm(EPI_QKV_ROPE, h, d, p->n_qkv, d, W.wq, W.wk, W.wv, qkv_l, p->n_qkv));
+      }
       AttnArgs aa{};
       aa.qkv = qkv_l;
       if (pu.pkv_layers) {
@@ -487,6 +525,17 @@ aiq_status enqueue_chunk(const aiq_plan* p, void* ws, const Layout& L, const int
         for (int32_t b = 0; b < nb; ++b) {
           const int64_t* bd = ldesc + static_cast<int64_t>(b) * D_STRIDE;
           GenAttnArgs ga{};
+          if (p->q_last_only) {
+            // queries of the last positions: their h rows, row scales and
+            // positions gathered, then the q projection (rotary) into ffn
+            float* rsl = at<float>(ws, L.laux);
+            int32_t* posl = reinterpret_cast<int32_t*>(rsl + R + 256);
+            TRACED(tr, AIQ_K_LAST, launch_last_h(bd, cu, h, rs, pos, d, att, rsl, posl, R, s));
+            TRACED(tr, AIQ_K_LAST, gemm_part(att, bd + D_NTOK, R, p->d_q, p->d_q, 0, W.wq, W.wk, W.wv, ffn, p->d_q,
+                                             rsl, posl));
+            ga.qkv = ffn;
+            ga.ldq = p->d_q;
+          }
           ga.kvc = qkv_l;
           ga.pkv = aa.pkv;
           ga.npre = aa.npre;
@@ -739,6 +788,9 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
     p->prune_last = p->bf16 && p->n_layers > 0 && (p->hd == 64 || p->hd == 128) &&
                     (rep == 1 || rep == 2 || rep == 3 || rep == 4 || rep == 8) &&
                     !(opts && (opts->flags & AIQ_PLAN_FULL_LAST_LAYER));
+    // separate key/value and query projections need 256-wide sections; the
+    // queries of the last positions go through the FFN buffer
+    p->q_last_only = p->prune_last && (2 * p->d_kv) % 256 == 0 && p->d_q % 256 == 0 && model->d_ff >= p->d_q;
   }
 
   if (query) {

@@ -348,16 +348,23 @@ struct GenAttnArgs {
   void* out;                 // [n, n_heads * hd]
   int32_t n_heads, n_kv, hd, out_act;
   int64_t seq_ub;
-  // 1: the query of sequence i is its own last row in kvc and the keys are
-  // the prefix and its own rows only (no generated tokens; qkv, gkv, step and
-  // gen unused); sequences with no own row are skipped
+  // 1: the query of sequence i is its own last position and the keys are
+  // the prefix and its own rows only (no generated tokens; gkv, step and gen
+  // unused); sequences with no own row are skipped.  The query is row i of
+  // qkv (stride ldq, q columns first) when qkv is set, else the last row in kvc.
   int32_t last_row;
+  int64_t ldq;
 };
 hipError_t launch_attention_gen(const GenAttnArgs& a, hipStream_t s);
 // Descriptors of the last positions of a chunk's sequences in blocks of R:
 // block b (b < nb) covers local sequences [b R, min(n, (b + 1) R)):
 // ldesc[b] = {chunk's first token, rows, chunk's first sequence + b R, rows}.
 hipError_t launch_last_desc(const int64_t* chunk_desc, int64_t* ldesc, int32_t nb, int64_t R, hipStream_t s);
+// The last position of sequence i (i < ldesc[D_NSEQ]): its 16-bit
+// normalised row h (d values), row scale and position, into row i of hl, rsl
+// and posl; sequences with no own row are left as they are.
+hipError_t launch_last_h(const int64_t* ldesc, const int64_t* cu, const void* h, const float* rs, const int32_t* pos,
+                         int32_t d, void* hl, float* rsl, int32_t* posl, int64_t R, hipStream_t s);
 // xl[i] = x[last row of sequence i] (fp32 rows of d), i < ldesc[D_NSEQ];
 // sequences with no own row are left as they are.
 hipError_t launch_last_rows(const int64_t* ldesc, const int64_t* cu, const float* x, int32_t d, float* xl,

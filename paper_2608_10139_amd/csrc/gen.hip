@@ -95,6 +95,36 @@ __global__ __launch_bounds__(256) void k_last_rows(const int64_t* ld, const int6
   }
 }
 
+// Wave per sequence: the row of d 16-bit values in 16-byte pieces.
+__global__ __launch_bounds__(256) void k_last_h(const int64_t* ld, const int64_t* cu, const uint16_t* h,
+                                                const float* rs, const int32_t* pos, int32_t d, uint16_t* hl,
+                                                float* rsl, int32_t* posl) {
+  const int64_t n = ld[D_NSEQ], sb = ld[D_SEQ_BEGIN], tb = ld[D_TOK_BEGIN];
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6;
+  const int64_t n_waves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t i = wave; i < n; i += n_waves) {
+    const int64_t c1 = cu[sb + i + 1];
+    if (c1 == cu[sb + i]) continue;
+    const int64_t r = c1 - 1 - tb;
+    const uint4* src = reinterpret_cast<const uint4*>(h + r * d);
+    uint4* dst = reinterpret_cast<uint4*>(hl + i * d);
+    for (int c = lane; c < d / 8; c += 64) dst[c] = src[c];
+    if (lane == 0) {
+      rsl[i] = rs[r];
+      posl[i] = pos[r];
+    }
+  }
+}
+
+hipError_t launch_last_h(const int64_t* ldesc, const int64_t* cu, const void* h, const float* rs, const int32_t* pos,
+                         int32_t d, void* hl, float* rsl, int32_t* posl, int64_t R, hipStream_t s) {
+  if (d % 8) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_last_h, dim3(grid_for(R, 4, 8192)), dim3(256), 0, s, ldesc, cu,
+                     static_cast<const uint16_t*>(h), rs, pos, d, static_cast<uint16_t*>(hl), rsl, posl);
+  return hipGetLastError();
+}
+
 hipError_t launch_last_rows(const int64_t* ldesc, const int64_t* cu, const float* x, int32_t d, float* xl,
                             int64_t R, hipStream_t s) {
   if (d % 4) return hipErrorInvalidValue;
@@ -193,7 +223,7 @@ __global__ __launch_bounds__(256) void k_attn_gen(GenAttnArgs a) {
     // keys: the prompt, the earlier generated tokens, this token (last-row
     // mode: the prompt, whose last row is the query)
     const int N = a.last_row ? P : P + a.step + 1;
-    const uint16_t* qrow = a.last_row ? kvc + (s0 + own - 1) * ld : qkv + i * ld;
+    const uint16_t* qrow = !a.last_row ? qkv + i * ld : (qkv ? qkv + i * a.ldq : kvc + (s0 + own - 1) * ld);
     const int kc = d_q + kvh * HD, vc = d_q + d_kv + kvh * HD;   // key / value columns of a q|k|v row
     uint16_t* gslot = a.last_row ? nullptr : gkv + (i * a.gen + a.step) * (2 * d_kv);
     if (!a.last_row && lane < 2 * LPK) {
