@@ -87,22 +87,56 @@ hipError_t launch_rmsnorm(const int64_t* desc, float* x, const float* delta, con
 }
 
 // ------------------------------------------------------------------ row scale
-// Thread per token: the RMSNorm scale from the per-slice sums of squares that
-// the residual projection wrote, added in slice order.
+// The RMSNorm scale of each token from the per-slice sums of squares that the
+// residual projection wrote, added in slice order.  A block takes 128 tokens:
+// their rows of sums come in with coalesced 16-byte loads into LDS (rows
+// padded by one float: conflict-free), then one thread per token adds its row
+// (rows wider than RS_MAX_PART: each thread reads its row directly).
+constexpr int RS_TOK = 128, RS_MAX_PART = 64;
+
 __global__ __launch_bounds__(256) void k_row_scale(const int64_t* desc, const float* ssp, int32_t n_part, int32_t d,
                                                    float eps, float* rs) {
+  __shared__ float part[RS_TOK * (RS_MAX_PART + 1)];
   const int64_t nt = desc[D_NTOK];
-  for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < nt; t += (int64_t)gridDim.x * blockDim.x) {
-    const float* p = ssp + t * n_part;
-    float ss = 0.f;
-    for (int k = 0; k < n_part; ++k) ss += p[k];
-    rs[t] = 1.0f / sqrtf(ss / static_cast<float>(d) + eps);
+  if (n_part > RS_MAX_PART || n_part % 4) {   // wide models: thread per token straight from memory
+    for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < nt; t += (int64_t)gridDim.x * blockDim.x) {
+      const float* p = ssp + t * n_part;
+      float ss = 0.f;
+      for (int k = 0; k < n_part; ++k) ss += p[k];
+      rs[t] = 1.0f / sqrtf(ss / static_cast<float>(d) + eps);
+    }
+    return;
+  }
+  const int stride = n_part + 1;
+  const int q4 = n_part / 4;   // 16-byte pieces per token
+  for (int64_t t0 = static_cast<int64_t>(blockIdx.x) * RS_TOK; t0 < nt; t0 += static_cast<int64_t>(gridDim.x) * RS_TOK) {
+    const int ntok = nt - t0 < RS_TOK ? static_cast<int>(nt - t0) : RS_TOK;
+    const float4* src = reinterpret_cast<const float4*>(ssp + t0 * n_part);
+    for (int e = threadIdx.x; e < ntok * q4; e += blockDim.x) {
+      const float4 v = src[e];
+      float* dst = part + (e / q4) * stride + (e % q4) * 4;
+      dst[0] = v.x;
+      dst[1] = v.y;
+      dst[2] = v.z;
+      dst[3] = v.w;
+    }
+    __syncthreads();
+    if (threadIdx.x < ntok) {
+      const float* p = part + threadIdx.x * stride;
+      float ss = 0.f;
+      for (int k = 0; k < n_part; ++k) ss += p[k];
+      rs[t0 + threadIdx.x] = 1.0f / sqrtf(ss / static_cast<float>(d) + eps);
+    }
+    __syncthreads();
   }
 }
 
 hipError_t launch_row_scale(const int64_t* desc, const float* ssp, int32_t n_part, int32_t d, float eps,
                             float* rs, int64_t t_cap, hipStream_t s) {
-  hipLaunchKernelGGL(k_row_scale, dim3(grid_for(t_cap, 256, 4096)), dim3(256), 0, s, desc, ssp, n_part, d, eps, rs);
+  if (n_part <= 0) return hipErrorInvalidValue;
+  const int per_block = (n_part > RS_MAX_PART || n_part % 4) ? 256 : RS_TOK;
+  hipLaunchKernelGGL(k_row_scale, dim3(grid_for(t_cap, per_block, 4096)), dim3(256), 0, s, desc, ssp, n_part, d, eps,
+                     rs);
   return hipGetLastError();
 }
 
