@@ -634,7 +634,7 @@ __global__ __launch_bounds__(256) void k_cu_from_blocks(const int32_t* lens, con
 hipError_t launch_cu_from_blocks(const int32_t* lens, const int64_t* blk_off, const int64_t* tok_off,
                                  int64_t n_ub, int64_t* cu, hipStream_t s) {
   const int64_t nb = (n_ub + REL_ROWS_PER_BLOCK - 1) / REL_ROWS_PER_BLOCK;
-  if (nb == 0) return hipSuccess;
+  if (nb == 0) return launch_fill_i64(cu, 1, 0, s);   // no rows: cu = {0}
   hipLaunchKernelGGL(k_cu_from_blocks, dim3(static_cast<unsigned>(nb)), dim3(256), 0, s, lens, blk_off, tok_off,
                      cu);
   return hipGetLastError();
@@ -914,7 +914,7 @@ hipError_t launch_select_lb(const DPredList& preds, int64_t n_rows, const void* 
                             int64_t out_cap2, int32_t* out_payload, const int64_t* off, int32_t max_len,
                             int32_t n_prefix, int64_t* cu, int64_t* lb, int64_t* ctr, hipStream_t s) {
   const int64_t nb = (n_rows + LB_ROWS - 1) / LB_ROWS;
-  if (nb == 0) return hipSuccess;
+  if (nb == 0) return off ? launch_fill_i64(cu, 1, 0, s) : hipSuccess;   // no rows: cu = {0}
   hipError_t e = launch_fill_i64(lb, 4 * nb, 0, s);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_select_lb, dim3(static_cast<unsigned>(nb)), dim3(LB_THREADS), 0, s, preds, n_rows, nb,
