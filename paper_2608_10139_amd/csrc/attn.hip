@@ -288,7 +288,10 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
 hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s) {
   if (a.npre < 0 || (a.npre > 0 && !a.pkv)) return hipErrorInvalidValue;
   if (a.seq_ub * a.n_heads >= (int64_t(1) << 31)) return hipErrorInvalidValue;   // 32-bit item numbers
-  const int g = grid_cap(a.seq_ub * a.n_heads, 4096);
+  // 32 workgroups per CU: with work items of very unequal length (sequence
+  // lengths spread 16..512) the finer grid balances the tail better than 16
+  // per CU (-3 % on a 1B model with 32 heads; unchanged with 8 heads)
+  const int g = grid_cap(a.seq_ub * a.n_heads, 8192);
   if (a.hd == 64)
     hipLaunchKernelGGL(k_attn_bf16<64>, dim3(g), dim3(256), 0, s, a);
   else if (a.hd == 128)
