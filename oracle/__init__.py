@@ -22,7 +22,7 @@ from .relational import (eval_pred, select, hash_join, sequences, pack, group_av
                          count_by)
 from .transformer import (rmsnorm, rope, causal_attention, gelu_erf, silu, forward_hidden,
                           label_logits, full_logits, Weights64)
-from .query import run_query, decide, aggregate, relational, run_pairs
+from .query import run_query, decide, aggregate, relational
 from .pairs import candidate_pairs, pair_sequences
 from .generate import position_logits, greedy_generate, generated_length, like_tokens
 
@@ -31,5 +31,5 @@ __all__ = [
     "rmsnorm", "rope", "causal_attention", "gelu_erf", "silu", "forward_hidden",
     "label_logits", "full_logits", "Weights64", "run_query", "decide", "aggregate", "relational",
     "position_logits", "greedy_generate", "generated_length", "like_tokens",
-    "run_pairs", "candidate_pairs", "pair_sequences",
+    "candidate_pairs", "pair_sequences",
 ]

@@ -8,7 +8,6 @@ from __future__ import annotations
 
 import numpy as np
 
-from .pairs import candidate_pairs, pair_sequences
 from .relational import select, hash_join, sequences, group_avg_count, count_by, sum_f32
 from .transformer import label_logits
 
@@ -82,20 +81,3 @@ def run_query(tables: dict, model: dict, query, sample=None) -> dict:
         res.update(aggregate(tables, rows, payload, res["labels"], query))
     return res
 
-
-def run_pairs(tables: dict, model: dict, query, sample=None) -> dict:
-    """Q4: pairs of selected rows with equal ``query.pair_key``, classified on
-    their joint text (oracle/pairs.py); kept pairs ascending by (A, B).
-    ``sample`` (indices into the candidate pairs) limits the transformer."""
-    rows, _ = relational(tables, query)
-    a, b = candidate_pairs(tables["probe"], rows, query.pair_key)
-    prefix = tables["prefix"][: query.n_prefix]
-    idx = np.arange(len(a)) if sample is None else np.asarray(sample, dtype=np.int64)
-    seqs = pair_sequences(tables["probe"], a[idx], b[idx], prefix)
-    lg = label_logits(model, seqs, query.labels)
-    res = {"rows": rows, "pair_a": a, "pair_b": b, "sample": idx, "logits": lg, "labels": decide(lg, query),
-           "margin": margin(lg, query), "n_tokens": int(sum(len(s) for s in seqs))}
-    if sample is None:
-        keep = res["labels"] == 1
-        res.update(kept_a=a[keep], kept_b=b[keep], count=int(keep.sum()))
-    return res

@@ -902,18 +902,14 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
     const int64_t def_chunk = std::min<int64_t>((int64_t(48) << 30) / per_tok, int64_t(4) << 20);
     int64_t ct = (opts && opts->chunk_tokens > 0) ? opts->chunk_tokens : def_chunk;
     ct = std::max<int64_t>(ct, max_packed);
-    ct = std::min<int64_t>(ct, std::max<int64_t>(p->t_ub, max_packed));
+    ct = std::min<int64_t>(ct, std::max<int64_t>(p->t_ub + p->n_seq_ub, max_packed));   // one chunk when all fits
     p->chunk_tokens = ct;
     p->t_cap = ct + max_packed;
-    if (p->gen > 0) {
-      // generation keeps per-sequence state: chunks are cut so that each holds
-      // at most ct sequences as well (a sequence counts one unit besides its tokens)
-      p->n_chunks = std::max<int64_t>((p->t_ub + p->n_rows + ct - 1) / ct, 1);
-      p->seq_ub = std::min<int64_t>(p->n_rows, ct);
-    } else {
-      p->n_chunks = std::max<int64_t>((p->t_ub + ct - 1) / ct, 1);
-      p->seq_ub = std::min<int64_t>(p->n_seq_ub, p->t_cap);
-    }
+    // chunks are cut by cu[i] + i (a sequence counts one unit besides its
+    // tokens): a chunk then holds at most ct sequences even where token lists
+    // are empty, and the keys of all sequences stay below n_chunks * ct
+    p->n_chunks = std::max<int64_t>((p->t_ub + p->n_seq_ub + ct - 1) / ct, 1);
+    p->seq_ub = std::min<int64_t>(p->n_seq_ub, ct);
     p->gen_blocks = p->gen > 0 ? static_cast<int32_t>((p->seq_ub + GEN_HEAD_ROWS - 1) / GEN_HEAD_ROWS) : 0;
     p->prefix.n = q.n_prefix;
     for (int k = 0; k < q.n_prefix; ++k) p->prefix.tok[k] = q.prefix[k];
@@ -1072,7 +1068,7 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
   if (!p->pairs)
     HIP_TRY(launch_gather_tokens(sel, ctr + C_SEL, n, p->probe.list_offsets, p->probe.list_tokens, cu, row_prefix,
                                  p->model.vocab, p->t_ub, packed, ctr, s));
-  HIP_TRY(launch_chunk_desc(cu, n_seq, p->chunk_tokens, p->n_chunks, p->t_ub, desc, s, p->gen > 0 ? 1 : 0));
+  HIP_TRY(launch_chunk_desc(cu, n_seq, p->chunk_tokens, p->n_chunks, p->t_ub, desc, s));
   HIP_TRY(launch_rope_table(p->max_seq, p->hd / 2, p->model.rope_theta, p->hd, at<float>(ws, L.rcos),
                             at<float>(ws, L.rsin), at<float>(ws, L.rrev), s));
   tr.end();

@@ -146,10 +146,11 @@ hipError_t launch_gather_tokens(const int32_t* sel, const int64_t* n_ptr, int64_
                                 const int64_t* offsets, const int32_t* tokens, const int64_t* cu,
                                 const Prefix& prefix, int32_t vocab, int64_t t_ub, int32_t* packed,
                                 int64_t* ctr, hipStream_t s);
-// Chunk c: the sequences i with cu[i] + per_seq * i in [c, c + 1) * chunk_tokens
-// (per_seq = 1 also caps the sequences per chunk at chunk_tokens).
+// Chunk c: the sequences i with cu[i] + i in [c, c + 1) * chunk_tokens (at
+// most chunk_tokens sequences per chunk, empty lists included); the last
+// chunk runs to the last sequence.
 hipError_t launch_chunk_desc(const int64_t* cu, const int64_t* n_ptr, int64_t chunk_tokens,
-                             int64_t n_chunks, int64_t t_ub, int64_t* desc, hipStream_t s, int32_t per_seq = 0);
+                             int64_t n_chunks, int64_t t_ub, int64_t* desc, hipStream_t s);
 hipError_t launch_packed_desc(const int32_t* cu32, int32_t n_seq, int64_t n_tok, int64_t* cu64,
                               int64_t* desc, int64_t* ctr, hipStream_t s);
 // The shared prompt prefix as a one-sequence batch: tok[0..n) = prefix,

@@ -158,7 +158,8 @@ __global__ __launch_bounds__(256) void k_head(HeadArgs a) {
     const int64_t last = no_own ? 0 : (a.x_compact ? i : a.cu[gi + 1] - 1 - tb);
     const float* xr = pre ? a.x_pre : a.x + last * d;
     const float* dr = (a.delta && !pre) ? a.delta + last * d : nullptr;   // last layer's pending output
-    auto xv = [&](int c) { return dr ? xr[c] + dr[c] : xr[c]; };
+    // an empty sequence reads no row: its normalised state is 0
+    auto xv = [&](int c) { return empty ? 0.f : dr ? xr[c] + dr[c] : xr[c]; };
     float ss = 0.f;
     for (int c = lane; c < d; c += 64) ss += xv(c) * xv(c);
     ss = wave_sum(ss);

@@ -100,22 +100,24 @@ hipError_t launch_gather_tokens(const int32_t* sel, const int64_t* n_ptr, int64_
 }
 
 // ------------------------------------------------------------------ chunk descriptors
-// Chunk c holds the sequences whose key cu[i] + per_seq * i lies in
-// [c*chunk_tokens, (c+1)*chunk_tokens): with per_seq = 0 the key is the first
-// token index; with per_seq = 1 every sequence also counts as one unit, so a
-// chunk holds at most chunk_tokens sequences even when lists are empty.
-__device__ __forceinline__ int64_t lower_bound_cu(const int64_t* cu, int64_t n, int64_t v, int32_t per_seq) {
+// Chunk c holds the sequences whose key cu[i] + i lies in
+// [c*chunk_tokens, (c+1)*chunk_tokens): every sequence counts as one unit
+// besides its tokens, so a chunk holds at most chunk_tokens sequences even
+// when lists are empty.  The last chunk also takes any sequence beyond the
+// bound (none when n_chunks * chunk_tokens exceeds tokens + sequences, which
+// the plan guarantees).
+__device__ __forceinline__ int64_t lower_bound_cu(const int64_t* cu, int64_t n, int64_t v) {
   int64_t lo = 0, hi = n;  // first i in [0, n) with key(i) >= v, else n
   while (lo < hi) {
     const int64_t mid = (lo + hi) >> 1;
-    if (cu[mid] + per_seq * mid < v) lo = mid + 1;
+    if (cu[mid] + mid < v) lo = mid + 1;
     else hi = mid;
   }
   return lo;
 }
 
 __global__ void k_chunk_desc(const int64_t* cu, const int64_t* n_ptr, int64_t chunk_tokens, int64_t n_chunks,
-                             int64_t t_ub, int64_t* desc, int32_t per_seq) {
+                             int64_t t_ub, int64_t* desc) {
   // only sequences that end inside the packed buffer take part
   int64_t n = *n_ptr;
   {
@@ -128,8 +130,8 @@ __global__ void k_chunk_desc(const int64_t* cu, const int64_t* n_ptr, int64_t ch
     n = lo;
   }
   for (int64_t c = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; c < n_chunks; c += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t sb = lower_bound_cu(cu, n, c * chunk_tokens, per_seq);
-    const int64_t se = lower_bound_cu(cu, n, (c + 1) * chunk_tokens, per_seq);
+    const int64_t sb = lower_bound_cu(cu, n, c * chunk_tokens);
+    const int64_t se = c + 1 == n_chunks ? n : lower_bound_cu(cu, n, (c + 1) * chunk_tokens);
     int64_t* d = desc + c * D_STRIDE;
     d[D_TOK_BEGIN] = cu[sb];
     d[D_NTOK] = cu[se] - cu[sb];
@@ -139,9 +141,9 @@ __global__ void k_chunk_desc(const int64_t* cu, const int64_t* n_ptr, int64_t ch
 }
 
 hipError_t launch_chunk_desc(const int64_t* cu, const int64_t* n_ptr, int64_t chunk_tokens,
-                             int64_t n_chunks, int64_t t_ub, int64_t* desc, hipStream_t s, int32_t per_seq) {
+                             int64_t n_chunks, int64_t t_ub, int64_t* desc, hipStream_t s) {
   hipLaunchKernelGGL(k_chunk_desc, dim3(grid_for(n_chunks, 256)), dim3(256), 0, s, cu, n_ptr,
-                     chunk_tokens, n_chunks, t_ub, desc, per_seq);
+                     chunk_tokens, n_chunks, t_ub, desc);
   return hipGetLastError();
 }
 

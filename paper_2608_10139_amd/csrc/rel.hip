@@ -51,8 +51,10 @@ __device__ __forceinline__ uint32_t hash_slot(int32_t key, int log2cap) {
   return (static_cast<uint32_t>(key) * 0x9E3779B1u) >> (32 - log2cap);
 }
 
-// Returns the slot holding `key`, or -1.
+// Returns the slot holding `key`, or -1.  The empty-slot value is never a
+// stored key (the build refuses it), so a probe with that value matches nothing.
 __device__ __forceinline__ int32_t hash_find(const HashArgs& h, int32_t key) {
+  if (key == HASH_EMPTY) return -1;
   const uint32_t mask = (1u << h.cap_log2) - 1u;
   uint32_t s = hash_slot(key, h.cap_log2);
   for (uint32_t i = 0; i <= mask; ++i) {

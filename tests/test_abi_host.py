@@ -204,8 +204,8 @@ def test_plan_passes():
         assert B.aiq_plan_passes(shared) == (1, 1)
         assert B.aiq_plan_passes(unshared) == (1, 0)
         assert B.aiq_plan_passes(rel) == (0, 0)
-        # 100,000 table tokens in chunks of 10,000
-        assert B.aiq_plan_passes(chunked) == (10, 0)
+        # 100,000 table tokens plus one unit per row (1,000 rows) in chunks of 10,000
+        assert B.aiq_plan_passes(chunked) == (11, 0)
     finally:
         for p in (shared, unshared, rel, chunked):
             B.aiq_plan_destroy(p)

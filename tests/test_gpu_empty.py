@@ -89,3 +89,52 @@ def test_selection_keeps_nothing_on_a_large_table(mname):
     r = run(t, m, dm, q)
     nothing(r)
     assert len(r["groups"][0]) == 0
+
+
+def _trailing_empty_table(n_full, n_empty, seed):
+    """n_full rows with tokens, then n_empty rows whose lists are empty, all
+    selected by c >= 0."""
+    r = np.random.default_rng(seed)
+    lens = np.concatenate([r.integers(1, 40, n_full), np.zeros(n_empty, np.int64)]).astype(np.int32)
+    off = np.zeros(len(lens) + 1, dtype=np.int64)
+    off[1:] = np.cumsum(lens)
+    n = len(lens)
+    probe = {"id": np.arange(n, dtype=np.int32), "c": r.integers(0, 1000, n).astype(np.int32), "len": lens,
+             "offsets": off, "tokens": r.integers(3, 1000, int(off[-1])).astype(np.int32)}
+    return {"probe": probe, "build": None, "prefix": r.integers(3, 1000, 64).astype(np.int32)}
+
+
+@pytest.mark.parametrize("npre", [0, 8])
+@pytest.mark.parametrize("chunk_tokens", [0, 256])
+def test_trailing_empty_rows_are_classified(npre, chunk_tokens):
+    """Rows with empty lists after the last token (every row selected) belong
+    to a chunk: with chunks of 256 units there are more empty rows (700) than
+    one chunk's tokens, and with the default chunk the whole batch is one
+    chunk whose token count equals the table's.  Each empty row's logits are
+    the oracle's: the prompt prefix alone, or all zero without a prefix (the
+    binary decision then rejects it)."""
+    import oracle
+    from oracle.query import decide, margin
+    from tests._parity import TOL_BF16, check_labels
+    say(f"case: trailing empty rows, prefix {npre}, chunk_tokens {chunk_tokens}")
+    m, dm = model("bf16")
+    t = _trailing_empty_table(300, 700, 5 + npre)
+    q = Query(preds=(Pred("c", "ge", 0),), labels=(1, 2), decision="binary_gt", agg="count", n_prefix=npre)
+    r = run(t, m, dm, q, chunk_tokens=chunk_tokens)
+    assert r["status"] == 0, hex(r["status"])
+    n = len(t["probe"]["id"])
+    assert r["n_selected"] == n
+    assert r["n_tokens"] == int(t["probe"]["len"].sum()) + npre * n
+    rows = np.arange(n)
+    sample = np.concatenate([np.arange(0, 300, 37), [299, 300, 301, 650, 998, 999]])
+    seqs = oracle.sequences(t["probe"], rows[sample], t["prefix"][:npre])
+    lg = oracle.label_logits(m, seqs, q.labels)
+    check_labels(r["logits"][sample], r["labels"][sample], lg, decide(lg, q), margin(lg, q), TOL_BF16,
+                 "trailing empty rows")
+    empty = r["logits"][300:]
+    assert np.all(empty == empty[0]), "every empty row carries the same logits"
+    if npre == 0:
+        assert np.all(empty == 0.0) and np.all(r["labels"][300:] == 0)
+    one = run(t, m, dm, q)   # one chunk: bit-identical
+    np.testing.assert_array_equal(r["logits"], one["logits"])
+    np.testing.assert_array_equal(r["kept_ids"], one["kept_ids"])

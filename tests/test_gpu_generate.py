@@ -187,3 +187,73 @@ def test_first_token_is_the_argmax_of_the_full_vocabulary_logits():
     lg = lg.cpu().numpy()
     pf.close()
     np.testing.assert_array_equal(r["gen"][:, 0], lg.argmax(axis=1))
+
+
+# ---------------------------------------------------------------- the benchmarked shapes
+_W = {}
+
+
+def reviews_workload(name):
+    """The reviews table (16,384 rows) and its 4-layer d512 model with the
+    32,000-token vocabulary."""
+    from synth import WORKLOADS
+    from synth.gen import make_tables
+    if name not in _W:
+        w = WORKLOADS[name]
+        m = make_model(w.model)
+        _W.clear()
+        _W[name] = (w, make_tables(w), m, DeviceModel(m))
+    return _W[name]
+
+
+def spread_sample(n, k, seed):
+    """k indices over [0, n): the first and last rows, both sides of every
+    4,096-row block edge of the generation head, and seeded picks."""
+    edges = [0, n - 1] + [e + d for e in range(4096, n, 4096) for d in (-1, 0)]
+    rng = np.random.default_rng(seed)
+    pick = set(i for i in edges if 0 <= i < n)
+    while len(pick) < min(k, n):
+        pick.add(int(rng.integers(0, n)))
+    return np.array(sorted(pick))
+
+
+@pytest.mark.timeout(300)
+def test_q3_generation_at_vocab_32000_over_several_head_blocks():
+    """Q3 at values_a < 50: 8,187 selected rows (two 4,096-row blocks of the
+    full-vocabulary head), 32 new tokens after an 8-token shared prompt."""
+    say("case: Q3 generation, reviews table, values_a < 50, vocab 32,000")
+    w, t, m, dm = reviews_workload("reviews_transform")
+    q = w.queries[2]
+    r = run(t, m, dm, q)
+    assert r["status"] == 0, hex(r["status"])
+    rows, _ = relational(t, q)
+    np.testing.assert_array_equal(r["sel_ids"], rows)
+    assert len(rows) > 4096 and r["gen"].shape == (len(rows), 32)
+    assert r["count"] == len(rows)
+    np.testing.assert_array_equal(r["kept_ids"], rows)
+    sample = spread_sample(len(rows), 128, 7)
+    exact, total = check_valid_tokens(m, t, q, r, sample)
+    say(f"  {exact}/{total} sampled tokens equal the oracle's own argmax")
+    assert exact >= 0.9 * total
+
+
+@pytest.mark.timeout(300)
+def test_q5_long_generation_with_end_token_and_like():
+    """Q5: every row (16,384; four head blocks), 128 new tokens, end token 2,
+    LIKE over the generated tokens; flags, kept ids and COUNT recomputed by the
+    oracle from the device's tokens, and sampled tokens valid."""
+    say("case: Q5 generation + LIKE, reviews table, 128 tokens, vocab 32,000")
+    w, t, m, dm = reviews_workload("reviews_like")
+    q = w.queries[0]
+    r = run(t, m, dm, q)
+    assert r["status"] == 0, hex(r["status"])
+    rows, _ = relational(t, q)
+    np.testing.assert_array_equal(r["sel_ids"], rows)
+    flags = np.array([like_tokens(r["gen"][i], q.like, q.eos_id) for i in range(len(rows))])
+    np.testing.assert_array_equal(r["labels"], flags.astype(np.int64))
+    np.testing.assert_array_equal(r["kept_ids"], rows[flags])
+    assert r["count"] == int(flags.sum())
+    sample = spread_sample(len(rows), 128, 9)
+    exact, total = check_valid_tokens(m, t, q, r, sample)
+    say(f"  {exact}/{total} sampled tokens equal the oracle's own argmax; {int(flags.sum())} rows kept")
+    assert exact >= 0.9 * total

@@ -143,8 +143,7 @@ def test_reviews_full_vocab_head(reviews_prefill):
 def test_reviews_end_to_end(compute):
     say(f"case: reviews end-to-end (16,384 rows, 4-layer d512, {compute} projections)")
     g = load_golden("reviews")
-    if g is None:
-        pytest.skip("golden file for the reviews workload not generated")
+    assert g is not None, "golden file for the reviews workload missing: run python -m tests.golden.make_golden reviews"
     w = workload("reviews")
     q = w["workload"].queries[0]
     r = run_query(w, q, dmodel=DeviceModel(w["model"], compute=compute))

@@ -3,13 +3,19 @@ benchmark uses (default chunking):
 
 * 1B-class 5-way classify + GROUP BY (131,072 rows), reviews JOIN movies with
   a shared 32-token prefix (262,144 reviews), and the 3B-class selectivity
-  sweep at 1 % (1,048,576 rows): selected rows, token counts, kept ids and
-  groups exact; label logits of a seeded sample of rows (shortest and longest
-  included) within the bf16 tolerance of the oracle; every aggregate recomputed
-  by the oracle from the device's per-row labels and compared exactly.
-* All four thresholds of the sweep table with a one-layer fp32 model: the
-  relational result (selection, tokens) exact at every selectivity, sampled
-  labels against the oracle, the COUNT and kept ids exact given the labels.
+  sweep at 1 % and 10 % (1,048,576 rows): selected rows, token counts, kept ids
+  and groups exact; label logits of a sample of at least 128 selected rows
+  (shortest and longest included, every decision outcome present) within the
+  bf16 tolerance of the oracle; every aggregate recomputed by the oracle from
+  the device's per-row labels and compared exactly.
+* The sweep's 50 % and 100 % thresholds with the 3B-class model on the
+  table's first 8,192 rows, to the same bar.
+* All four thresholds on the whole sweep table with a one-layer fp32 model:
+  the relational result (selection, tokens) exact at every selectivity,
+  sampled labels against the oracle, the COUNT and kept ids exact given the
+  labels.
+
+A missing golden file fails the test (tests/golden/make_golden.py writes them).
 """
 import numpy as np
 import pytest
@@ -48,26 +54,68 @@ def run(t, model, q, dm):
     return r
 
 
-@pytest.mark.timeout(600)
-@pytest.mark.parametrize("name", ["groupby1b", "join1b", "sweep3b"])
-def test_full_size_workload(name):
+def golden(name):
     g = load_golden(name)
-    if g is None:
-        pytest.skip(f"golden file for {name} not generated")
-    w = WORKLOADS[name]
-    q = w.queries[0]
-    say(f"case: {name} full size ({w.description}); generating inputs")
-    t = tables(name)
-    model = make_model(w.model)
-    dm = DeviceModel(model)
+    assert g is not None, f"golden file for {name} missing: run python -m tests.golden.make_golden {name}"
+    return g
+
+
+def outcomes(q):
+    return {0, 1} if q.decision == "binary_gt" else set(int(l) for l in q.labels)
+
+
+_MODELS = {}
+
+
+def device_model(w):
+    key = w.model
+    if key not in _MODELS:
+        _MODELS.clear()   # one large model resident at a time
+        m = make_model(w.model)
+        _MODELS[key] = (m, DeviceModel(m))
+    return _MODELS[key]
+
+
+def check_against_golden(gname, t, w, qi):
+    g = golden(gname)
+    q = w.queries[qi]
+    model, dm = device_model(w)
     say("  running on the device")
     r = run(t, model, q, dm)
     say(f"  selected {r['n_selected']} tokens {r['n_tokens']} kept {r['count']} status {r['status']:#x}")
-    rows = g["q0_rows"]
-    payload = g.get("q0_payload")
-    check_query(r, t, q, rows, payload, g["q0_logits"], g["q0_labels"], g["q0_margin"], TOL_BF16,
-                sample=g["q0_sample"])
-    del dm
+    p = f"q{qi}_"
+    sample = g[p + "sample"]
+    assert len(sample) >= min(128, len(g[p + "rows"])), "golden sample smaller than 128 rows"
+    assert outcomes(q) <= set(g[p + "labels"].tolist()), "golden sample misses a decision outcome"
+    check_query(r, t, q, g[p + "rows"], g.get(p + "payload"), g[p + "logits"], g[p + "labels"], g[p + "margin"],
+                TOL_BF16, sample=sample)
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("name,qi", [("groupby1b", 0), ("join1b", 0), ("sweep3b", 0), ("sweep3b", 1)])
+def test_full_size_workload(name, qi):
+    w = WORKLOADS[name]
+    say(f"case: {name} query {qi} full size ({w.description}); generating inputs")
+    check_against_golden(name, tables(name), w, qi)
+
+
+def head_tables(n):
+    """The first n rows of the sweep table (token lists included)."""
+    t = tables("sweep3b")
+    p = t["probe"]
+    off = p["offsets"][: n + 1]
+    probe = {k: v[:n] for k, v in p.items() if k not in ("offsets", "tokens")}
+    probe["offsets"] = off
+    probe["tokens"] = p["tokens"][: int(off[-1])]
+    return {"probe": probe, "build": None, "prefix": t["prefix"]}
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("qi", [2, 3])
+def test_sweep_3b_model_high_selectivity(qi):
+    w = WORKLOADS["sweep3b"]
+    say(f"case: sweep table first 8,192 rows, c < {w.queries[qi].preds[0].k}, 3B-class model")
+    check_against_golden("sweep3b_head", head_tables(8192), w, qi)
 
 
 @pytest.fixture(scope="module")
