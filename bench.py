@@ -1,21 +1,24 @@
 #!/usr/bin/env python3
 """Benchmark of the unified AI-query pipeline on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload reviews]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload sweep3b] [--query 0]
 
 A step is one aiq_run of the whole query over device-resident inputs: WHERE
 + stable selection, varlen pack, decoder prefill, label head + decision,
-kept ids + COUNT, on one HIP stream.  The default workload is the
-reviews-shaped binary filter: 16,384 synthetic rows (seed 1), a 4-layer d512
-bf16 SwiGLU decoder.
+kept ids + COUNT, on one HIP stream.  The default workload is the largest
+configuration: the selectivity sweep's table (1,048,576 synthetic rows, seed
+4) through the 28-layer d3072 3B-class decoder at its 1 % point (c < 10),
+whose whole-table steps take about 15 s each.
 
 Printed (one JSON line): rows/s (table rows / end-to-end step time) as the
 value, tokens/s, a per-stage breakdown, the roofline of the dominant kernel
-(the gate/up SwiGLU GEMM) measured with HIP events around its launches, the
-CPU oracle timed on a bounded sample of the same workload, and a
-split-execution baseline (host selection + pack, H2D copy of survivors in
-micro-batches of 128 rows, the same device prefill with full-vocabulary
-logits copied back, host decision and COUNT).
+(the gate/up SwiGLU GEMM) measured with HIP events around its launches that
+carry tokens, the CPU oracle timed on the same workload (its relational part
+on the whole table, its transformer on a seeded sample of the selected rows,
+projected to all of them by FLOPs), and a split-execution baseline (host
+selection + pack, H2D copy of survivors in micro-batches of 128 rows, the
+same device prefill with full-vocabulary logits copied back, host decision
+and COUNT).
 """
 from __future__ import annotations
 
@@ -37,14 +40,15 @@ PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3
 PEAK_HBM_GBPS = 8000.0
 
-# HBM bytes per launch of the gate/up GEMM on the reviews workload (472,953
-# tokens), from rocprofv3 FETCH_SIZE and WRITE_SIZE runs scaled by a plain
-# 1 GiB copy (x2.000 and x1.000); summary and commands in
-# profiles/reviews_pipeline_hbm_traffic.md.  Valid only for the kernel source
-# it was measured on: reported as null once gemm.hip, dev_util.h or the
-# GemmArgs declaration change.
-GATE_UP_TRAFFIC = {"workload": "reviews", "tokens": 472953, "bytes": 4864697315,
-                   "source_sha256": "f2e7b9aed2e9b69dcb59a4cb3b127233665a51ee634c29375346f530431a7a68"}
+# HBM bytes of gate/up GEMM launches measured by rocprofv3 FETCH_SIZE and
+# WRITE_SIZE runs of the default bench command, scaled by what the same
+# counters read for a plain 1 GiB copy (x2.000 and x1.000), keyed by the
+# launch's token count (profiles/ holds the summaries and commands).  Valid
+# only for the GEMM source they were measured on: reported as null once
+# gemm.hip, dev_util.h or the GemmArgs declaration change, or for launches
+# not listed.
+GATE_UP_TRAFFIC = {"workload": "sweep3b", "query": 0, "bytes_by_tokens": {},
+                   "source_sha256": ""}
 
 
 def gemm_source_sha256() -> str:
@@ -219,9 +223,15 @@ def host_select(cols: dict, preds) -> np.ndarray:
 
 
 # ------------------------------------------------------------------ legs
-def cpu_baseline_leg(tables, model, q, n_rows_sample: int) -> dict:
-    """The CPU oracle (fp64, per sequence) on the first rows of the table."""
+def cpu_baseline_leg(tables, model, q, spec, budget_flop: float = 3.0e12, seed: int = 0) -> dict:
+    """The CPU oracle (fp64, per sequence) on the same workload: its
+    relational part (WHERE, join) on the whole table, then its transformer on
+    a seeded sample of the selected rows of about ``budget_flop`` FLOPs,
+    projected to every selected row: widening the weights to fp64 (timed on
+    its own, done once per run) plus the sample's remaining time scaled by
+    the FLOPs of all selected rows over the sample's."""
     import oracle
+    from oracle.transformer import Weights64
     try:
         from threadpoolctl import threadpool_info
         blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
@@ -229,16 +239,42 @@ def cpu_baseline_leg(tables, model, q, n_rows_sample: int) -> dict:
         blas = 1
     cores = len(os.sched_getaffinity(0))
     probe = tables["probe"]
-    R = min(n_rows_sample, len(probe["id"]))
-    sub = {k: (v[:R + 1] if k == "offsets" else v if k == "tokens" else v[:R]) for k, v in probe.items()}
-    st = {"probe": sub, "build": tables.get("build"), "prefix": tables["prefix"]}
+    n = len(probe["id"])
     t0 = time.perf_counter()
-    res = oracle.run_query(st, model, q)
-    dt = time.perf_counter() - t0
-    return {"value": R / dt, "unit": "rows/s", "cores": int(max(blas, 1)), "host_cores": cores, "kind": "oracle",
-            "sample": f"first {R} of {len(probe['id'])} table rows: full query on them "
-                      f"({len(res['rows'])} selected rows, {res['n_tokens']} tokens, fp64 per-sequence forward)",
-            "seconds": dt}
+    rows, _ = oracle.relational(tables, q)
+    t_rel = time.perf_counter() - t0
+    own = probe["len"][rows].astype(np.float64)
+    npre = q.n_prefix
+    fl_all = prefill_flops(spec, own, len(q.labels), npre)["total"]
+    rng = np.random.default_rng(seed)
+    order = rng.permutation(len(rows))
+    pick, fl_s = [], 0.0
+    for i in order:
+        if fl_s >= budget_flop:
+            break
+        pick.append(int(i))
+        fl_s += prefill_flops(spec, own[[i]], len(q.labels), npre)["total"]
+    pick = np.sort(np.asarray(pick, dtype=np.int64))
+    t0 = time.perf_counter()
+    W = Weights64(model)
+    for l in range(spec.n_layers):
+        W.layer(l)
+    t_widen = time.perf_counter() - t0
+    seqs = oracle.sequences(probe, rows[pick], tables["prefix"][:npre])
+    t0 = time.perf_counter()
+    oracle.label_logits(model, seqs, q.labels)
+    t_sample = time.perf_counter() - t0
+    t_compute = max(t_sample - t_widen, 1e-9)
+    t_model = t_widen + t_compute * (fl_all / max(fl_s, 1.0)) if len(rows) else 0.0
+    total = t_rel + t_model
+    return {"value": round(n / total, 4), "unit": "rows/s", "cores": int(max(blas, 1)), "host_cores": cores,
+            "kind": "oracle",
+            "sample": f"relational part on all {n} table rows (measured {t_rel:.2f} s, {len(rows)} selected); "
+                      f"transformer on {len(pick)} seeded selected rows ({fl_s:.3e} FLOP, measured "
+                      f"{t_sample:.1f} s incl. {t_widen:.1f} s widening the weights to fp64), projected to all "
+                      f"{len(rows)} selected rows ({fl_all:.3e} FLOP): {t_model:.0f} s",
+            "seconds_measured": round(t_rel + t_sample + t_widen, 2), "seconds_projected": round(total, 1),
+            "projected": True}
 
 
 def split_baseline_leg(tables, model, q, dm, B, torch, micro=128) -> dict:
@@ -258,10 +294,11 @@ def split_baseline_leg(tables, model, q, dm, B, torch, micro=128) -> dict:
     labels = list(q.labels)
     prefix = np.asarray(tables["prefix"][:q.n_prefix], dtype=np.int32)
 
-    def one_pass():
+    def one_pass(limit=None):
         rows = host_select(probe, q.preds)
         kept = 0
-        for b0 in range(0, len(rows), micro):
+        end = len(rows) if limit is None else min(len(rows), limit)
+        for b0 in range(0, end, micro):
             rb = rows[b0:b0 + micro]
             seqs = [np.concatenate([prefix, probe["tokens"][probe["offsets"][r]:probe["offsets"][r + 1]]])
                     for r in rb]
@@ -279,7 +316,7 @@ def split_baseline_leg(tables, model, q, dm, B, torch, micro=128) -> dict:
             kept += int(np.sum(full[:, labels[0]] > full[:, labels[1]]))
         return len(rows), kept
 
-    one_pass()   # warm-up
+    one_pass(micro)   # warm-up: one micro-batch
     t0 = time.perf_counter()
     n_sel, kept = one_pass()
     dt = time.perf_counter() - t0
@@ -405,12 +442,13 @@ def pack_config_leg(B, torch, steps: int = 3) -> list:
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="reviews")
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="sweep3b")
     ap.add_argument("--compute", default="f16", choices=["f16", "bf16"],
                     help="projection type for bf16-drawn weights (f16: exact fp16 images of the weights)")
-    ap.add_argument("--cpu-rows", type=int, default=1024)
+    ap.add_argument("--cpu-flop", type=float, default=3.0e12,
+                    help="FLOPs of the oracle's transformer sample in the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-split", action="store_true")
     ap.add_argument("--query", type=int, default=0, help="index of the workload's query to time")
@@ -504,16 +542,28 @@ def main(argv=None) -> int:
     assert T == res["n_tokens"]
 
     # ---- timed region: whole steps; HIP events around the dominant kernel's launches only
-    # every prefill pass (chunk, or the shared prefix) launches the gate/up GEMM once per layer
+    # every prefill pass (the shared prefix, then each chunk) launches the
+    # gate/up GEMM once per layer; with the last layer on the last positions
+    # only, a pass's last gate/up runs on those rows and is traced as part of
+    # that layer.  Passes the selection leaves empty launch and do no work.
     chunks, pre_pass = B.aiq_plan_passes(dq.plan)
     passes = chunks + pre_pass
     last_rows_only = B.aiq_plan_last_layer_rows(dq.plan)
-    # with the last layer on the last positions only, each pass's last gate/up
-    # runs on those rows and is traced as part of that layer
-    launches_per_step = (spec.n_layers - (1 if last_rows_only else 0)) * passes
+    layers_full = spec.n_layers - (1 if last_rows_only else 0)
+    launches_per_step = layers_full * passes
+    # tokens of each pass, from the plan's chunking rule (cu[i] + i over chunk_tokens)
+    ct = B.aiq_plan_chunk_tokens(dq.plan)
+    packed = own + (0 if shared else q.n_prefix)
+    cu = np.concatenate([[0.0], np.cumsum(packed)])
+    cidx = np.minimum(((cu[:-1] + np.arange(len(packed))) // ct).astype(np.int64), chunks - 1)
+    pass_tok = list(np.bincount(cidx, weights=packed, minlength=chunks).astype(np.int64))
+    if pre_pass:
+        pass_tok = [q.n_prefix] + pass_tok
+    launch_tok = np.repeat(np.asarray(pass_tok, dtype=np.int64), layers_full)   # one step, in launch order
     ev = HipEvents(2 * a.steps * launches_per_step)
     trace = make_trace(B, ev, 1 << B.AIQ_K_GEMM_UP)
-    log(f"[bench] timing {a.steps} steps")
+    log(f"[bench] timing {a.steps} steps ({chunks} chunk passes of {ct} units, "
+        f"{int(np.count_nonzero(launch_tok))} of {len(launch_tok)} gate/up launches per step carry tokens)")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     long_steps = step_s > 30.0   # minutes-long queries: report each step as it ends
@@ -527,15 +577,18 @@ def main(argv=None) -> int:
     ms_step = dt / a.steps * 1e3
     if trace.count != a.steps * launches_per_step:
         raise RuntimeError(f"traced {trace.count} gate/up launches, expected {a.steps * launches_per_step}")
-    up = per_kind_ms(B, trace, ev).get(B.AIQ_K_GEMM_UP, [])
+    up = np.asarray(per_kind_ms(B, trace, ev).get(B.AIQ_K_GEMM_UP, []), dtype=np.float64)
     ev.close()
     fl = prefill_flops(spec, own, len(q.labels), q.n_prefix, shared, last_rows_only)
-    # every launch of the gate/up GEMM covers one chunk (or the shared prefix);
-    # chunks the selection leaves empty are launched and do no work
-    n_up = len(up)
-    up_flops_per_launch = fl["up"] * a.steps / max(n_up, 1)
-    up_avg_ms = float(np.mean(up)) if up else float("nan")
-    achieved = up_flops_per_launch / (up_avg_ms * 1e-3) / 1e12
+    tok_all = np.tile(launch_tok, a.steps)
+    real = tok_all > 0
+    n_ffn = 3 if spec.act == "swiglu" else 2
+    up_flops = 2.0 * tok_all[real] * (n_ffn - 1) * spec.d_ff * spec.d_model   # per launch that carries tokens
+    up_ms = up[real]
+    empty_ms = up[~real]
+    up_flops_per_launch = float(np.mean(up_flops)) if len(up_flops) else 0.0
+    up_avg_ms = float(np.mean(up_ms)) if len(up_ms) else float("nan")
+    achieved = float(np.sum(up_flops)) / (float(np.sum(up_ms)) * 1e-3) / 1e12 if len(up_ms) else 0.0
     peak = PEAK_F32_TFLOPS if dm.compute == "f32" else PEAK_BF16_TFLOPS   # fp16 and bf16 MFMA peaks are equal
 
     # ---- one untimed traced step for the stage breakdown
@@ -569,9 +622,12 @@ def main(argv=None) -> int:
     rel_ms = float(np.sum(kinds.get(B.AIQ_K_REL, [0.0])))
 
     traffic = None
-    if (a.workload == GATE_UP_TRAFFIC["workload"] and T == GATE_UP_TRAFFIC["tokens"]
+    by_tok = GATE_UP_TRAFFIC["bytes_by_tokens"]
+    real_tok = [int(t) for t in launch_tok if t > 0]
+    if (a.workload == GATE_UP_TRAFFIC["workload"] and a.query == GATE_UP_TRAFFIC["query"] and real_tok
+            and all(str(t) in by_tok for t in real_tok)
             and gemm_source_sha256() == GATE_UP_TRAFFIC["source_sha256"]):
-        traffic = GATE_UP_TRAFFIC["bytes"]
+        traffic = float(np.mean([by_tok[str(t)] for t in real_tok]))
     result = {
         "metric": METRIC, "value": round(n_rows / (ms_step * 1e-3), 2), "unit": "rows/s",
         "n_gpus": 1, "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_step, 4),
@@ -594,8 +650,11 @@ def main(argv=None) -> int:
         "roofline": {"bound": "mfma", "kernel": "k_gemm_bf16<EPI_SWIGLU> (gate/up projection + SwiGLU)",
                      "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4), "traffic": traffic,
-                     "launches": n_up, "avg_launch_ms": round(up_avg_ms, 5),
-                     "flops_per_launch": up_flops_per_launch},
+                     "launches": int(len(up_ms)), "avg_launch_ms": round(up_avg_ms, 5),
+                     "flops_per_launch": up_flops_per_launch,
+                     "tokens_per_launch": sorted(set(real_tok)),
+                     "empty_launches": int(len(empty_ms)),
+                     "empty_launch_avg_ms": round(float(np.mean(empty_ms)), 5) if len(empty_ms) else None},
     }
     if gen:
         result["generation"] = generation_report(spec, q, tables, sel, kinds, B, ms_step)
@@ -613,7 +672,7 @@ def main(argv=None) -> int:
         result["relational_scale"] = relational_scale_leg(B, torch, [1 << 26], [10, 1000], steps=5)
     if not a.no_cpu_baseline:
         log("[bench] cpu baseline (oracle on a sample)")
-        result["cpu_baseline"] = cpu_baseline_leg(tables, model, q, a.cpu_rows)
+        result["cpu_baseline"] = cpu_baseline_leg(tables, model, q, spec, a.cpu_flop)
     if not a.no_split:
         log("[bench] split-execution baseline")
         result["split_baseline"] = split_baseline_leg(tables, model, q, dm, B, torch)

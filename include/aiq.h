@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define AIQ_ABI_VERSION 5
+#define AIQ_ABI_VERSION 6
 
 typedef enum aiq_status {
   AIQ_OK = 0,
@@ -389,6 +389,18 @@ aiq_status aiq_workspace_size(const aiq_plan* plan, size_t* bytes);
  * (aiq_trace).  Errors: AIQ_EINVAL (NULL argument, prefill-only plan).
  */
 aiq_status aiq_plan_passes(const aiq_plan* plan, int64_t* chunks, int32_t* prefix_pass);
+
+/*
+ * The chunk size of the plan's prefill passes (0 for a relational-only plan):
+ * pass c covers the selected sequences i with cu[i] + i in
+ * [c * chunk_tokens, (c + 1) * chunk_tokens), where cu[i] is the number of
+ * packed tokens before sequence i; a sequence counts one unit besides its
+ * tokens, so a pass never holds more than chunk_tokens sequences.  With
+ * aiq_plan_passes this tells a caller which passes a given selection fills
+ * (a trace's per-pass launches, Section 3.2's scan over micro-batches).
+ * Errors: AIQ_EINVAL (NULL argument, prefill-only plan).
+ */
+aiq_status aiq_plan_chunk_tokens(const aiq_plan* plan, int64_t* chunk_tokens);
 
 /*
  * *last_rows_only = 1 when the plan runs the last layer, after its q|k|v

@@ -13,7 +13,7 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libaiq.so")
 
-AIQ_ABI_VERSION = 5   # the struct layouts below
+AIQ_ABI_VERSION = 6   # the struct layouts below
 AIQ_OK, AIQ_EINVAL, AIQ_EUNSUPPORTED, AIQ_ENOSPC, AIQ_EHIP, AIQ_ENOMEM = 0, -1, -2, -3, -4, -5
 AIQ_I8, AIQ_I16, AIQ_I32, AIQ_F32, AIQ_BF16, AIQ_F16 = 1, 2, 3, 4, 5, 6
 AIQ_LT, AIQ_LE, AIQ_GT, AIQ_GE, AIQ_EQ, AIQ_NE, AIQ_IN = range(7)
@@ -101,7 +101,8 @@ class aiq_trace(C.Structure):
                 ("capacity", C.c_int32), ("count", C.c_int32), ("kind_mask", C.c_uint32)]
 
 
-EXPORTS = ("aiq_plan_create", "aiq_workspace_size", "aiq_plan_passes", "aiq_plan_last_layer_rows", "aiq_run",
+EXPORTS = ("aiq_plan_create", "aiq_workspace_size", "aiq_plan_passes", "aiq_plan_chunk_tokens",
+           "aiq_plan_last_layer_rows", "aiq_run",
            "aiq_prefill_workspace_size",
            "aiq_prefill_packed", "aiq_plan_destroy", "aiq_status_str", "aiq_abi_version")
 
@@ -131,6 +132,8 @@ def load(path: str = LIB_PATH) -> C.CDLL:
     lib.aiq_workspace_size.restype = C.c_int
     lib.aiq_plan_passes.argtypes = [P, C.POINTER(C.c_int64), C.POINTER(C.c_int32)]
     lib.aiq_plan_passes.restype = C.c_int
+    lib.aiq_plan_chunk_tokens.argtypes = [P, C.POINTER(C.c_int64)]
+    lib.aiq_plan_chunk_tokens.restype = C.c_int
     lib.aiq_plan_last_layer_rows.argtypes = [P, C.POINTER(C.c_int32)]
     lib.aiq_plan_last_layer_rows.restype = C.c_int
     lib.aiq_run.argtypes = [P, P, C.c_size_t, C.POINTER(aiq_out), C.POINTER(aiq_trace), P]
@@ -194,6 +197,13 @@ def aiq_plan_passes(plan) -> tuple:
     pp = C.c_int32()
     check("aiq_plan_passes", load().aiq_plan_passes(plan, C.byref(n), C.byref(pp)))
     return n.value, pp.value
+
+
+def aiq_plan_chunk_tokens(plan) -> int:
+    """Units (tokens + sequences) per prefill pass of aiq_run."""
+    v = C.c_int64()
+    check("aiq_plan_chunk_tokens", load().aiq_plan_chunk_tokens(plan, C.byref(v)))
+    return v.value
 
 
 def aiq_plan_last_layer_rows(plan) -> bool:

@@ -934,6 +934,12 @@ aiq_status aiq_plan_passes(const aiq_plan* plan, int64_t* chunks, int32_t* prefi
   return AIQ_OK;
 }
 
+aiq_status aiq_plan_chunk_tokens(const aiq_plan* plan, int64_t* chunk_tokens) {
+  if (!plan || !chunk_tokens || !plan->has_probe) return AIQ_EINVAL;
+  *chunk_tokens = plan->rel_only ? 0 : plan->chunk_tokens;
+  return AIQ_OK;
+}
+
 aiq_status aiq_plan_last_layer_rows(const aiq_plan* plan, int32_t* last_rows_only) {
   if (!plan || !last_rows_only) return AIQ_EINVAL;
   *last_rows_only = plan->prune_last ? 1 : 0;

@@ -109,7 +109,8 @@ def test_join_count_by_payload(rel_model):
     mv = movies(700, 1)
     pr = table(9000, 2)
     r = np.random.default_rng(3)
-    pool = np.concatenate([mv["movie_id"], np.array([-5, 2_000_000], np.int32)])   # dangling keys too
+    # dangling keys too, among them the hash table's empty-slot value (INT32_MIN), which matches no movie
+    pool = np.concatenate([mv["movie_id"], np.array([-5, 2_000_000, np.iinfo(np.int32).min], np.int32)])
     pr["movie_id"] = pool[r.integers(0, len(pool), 9000)]
     t = {"probe": pr, "build": mv, "prefix": np.array([11, 12], np.int32)}
     q = Query(preds=(Pred("a", "lt", 100),), labels=(1, 2), decision="binary_gt", agg="count_by_payload",
