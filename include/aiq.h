@@ -423,6 +423,28 @@ aiq_status aiq_plan_last_layer_rows(const aiq_plan* plan, int32_t* last_rows_onl
 aiq_status aiq_run(const aiq_plan* plan, void* workspace, size_t ws_bytes, const aiq_out* out,
                    aiq_trace* trace, void* stream);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * relational part of aiq_run for a relational-only plan
+ * (AIQ_PLAN_RELATIONAL_ONLY, one-launch compaction), with no workspace
+ * argument.  Its scratch (counters, the compaction's look-back words, the
+ * join's hash table) lives in one fixed device array of 16 MiB inside the
+ * library, which each GPU it runs on holds until the process ends; the call
+ * allocates nothing.  Outputs as aiq_run with that plan: out->ids (and
+ * out->sel_ids when sel_cap > 0) receive the selected row ids ascending,
+ * scalars SELECTED = KEPT = their count, TOKENS = their token total.
+ * Every call on a GPU shares that GPU's array: calls that overlap on one GPU
+ * (on different streams or threads) race and must not be issued.  Each call
+ * clears what must start at zero itself.
+ * Errors: AIQ_EINVAL (NULL plan/out/scalars, a plan that is not
+ * relational-only), AIQ_EUNSUPPORTED (a plan using the multi-launch
+ * compaction), AIQ_ENOSPC (the plan needs more than the 16 MiB scratch:
+ * about 32 B per 4,096 probe rows plus 8 B per hash slot, i.e. 2 x the build
+ * rows rounded up to a power of two; nothing is enqueued), AIQ_EHIP.
+ */
+aiq_status aiq_run_relational_static(const aiq_plan* plan, const aiq_out* out, void* stream);
+
 /* Bytes of workspace aiq_prefill_packed needs for up to max_tokens tokens. */
 aiq_status aiq_prefill_workspace_size(const aiq_plan* plan, int64_t max_tokens, size_t* bytes);
 

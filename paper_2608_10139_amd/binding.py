@@ -102,7 +102,7 @@ class aiq_trace(C.Structure):
 
 
 EXPORTS = ("aiq_plan_create", "aiq_workspace_size", "aiq_plan_passes", "aiq_plan_chunk_tokens",
-           "aiq_plan_last_layer_rows", "aiq_run",
+           "aiq_plan_last_layer_rows", "aiq_run", "aiq_run_relational_static",
            "aiq_prefill_workspace_size",
            "aiq_prefill_packed", "aiq_plan_destroy", "aiq_status_str", "aiq_abi_version")
 
@@ -138,6 +138,8 @@ def load(path: str = LIB_PATH) -> C.CDLL:
     lib.aiq_plan_last_layer_rows.restype = C.c_int
     lib.aiq_run.argtypes = [P, P, C.c_size_t, C.POINTER(aiq_out), C.POINTER(aiq_trace), P]
     lib.aiq_run.restype = C.c_int
+    lib.aiq_run_relational_static.argtypes = [P, C.POINTER(aiq_out), P]
+    lib.aiq_run_relational_static.restype = C.c_int
     lib.aiq_prefill_workspace_size.argtypes = [P, C.c_int64, C.POINTER(C.c_size_t)]
     lib.aiq_prefill_workspace_size.restype = C.c_int
     lib.aiq_prefill_packed.argtypes = [P, P, P, C.c_int32, C.c_int64, C.c_int32, P, P, C.c_size_t, P]
@@ -222,6 +224,15 @@ def aiq_prefill_workspace_size(plan, max_tokens: int) -> int:
 def aiq_run(plan, ws_ptr: int, ws_bytes: int, out: aiq_out, trace=None, stream: int = 0) -> None:
     check("aiq_run", load().aiq_run(plan, ws_ptr, ws_bytes, C.byref(out),
                                     C.byref(trace) if trace is not None else None, stream))
+
+
+def aiq_run_relational_static(plan, out: aiq_out, stream: int = 0) -> None:
+    check("aiq_run_relational_static", load().aiq_run_relational_static(plan, C.byref(out), stream))
+
+
+def aiq_run_relational_static_status(plan, out: aiq_out, stream: int = 0) -> int:
+    """Like aiq_run_relational_static but returns the status (for error-path tests)."""
+    return load().aiq_run_relational_static(plan, C.byref(out), stream)
 
 
 def aiq_prefill_packed(plan, tok_ptr: int, cu_ptr: int, n_seq: int, n_tok: int, mode: int,

@@ -1167,6 +1167,56 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
   return AIQ_OK;
 }
 
+// The relational part of aiq_run (a relational-only plan) with its scratch in
+// the library's fixed device array instead of a caller workspace: counters,
+// the compaction's look-back words and the join's hash table.  The same
+// kernels as aiq_run's one-launch form; the per-row token offsets are not
+// kept (only their total is an output here).
+aiq_status aiq_run_relational_static(const aiq_plan* p, const aiq_out* out, void* stream) {
+  if (!p || !out || !out->scalars) return AIQ_EINVAL;
+  if (!p->has_probe || !p->rel_only) return AIQ_EINVAL;
+  if (out->ids_cap < 0 || (out->ids_cap > 0 && !out->ids) || out->sel_cap < 0) return AIQ_EINVAL;
+  if (!p->lb_compact) return AIQ_EUNSUPPORTED;
+  Carver c;
+  const size_t o_ctr = c.take(C_COUNT * 8);
+  const int64_t nlb = (p->n_rows + LB_MIN_ROWS - 1) / LB_MIN_ROWS + 1;
+  const size_t o_lb = c.take(static_cast<size_t>(nlb) * 4 * 8);
+  const size_t hcap = p->has_build ? (size_t(1) << p->hash_log2) : 0;
+  const size_t o_hk = c.take(hcap * 4);
+  const size_t o_hv = c.take(hcap * 4);
+  if (c.off > STATIC_SCRATCH_BYTES) return AIQ_ENOSPC;   // before any HIP call: nothing enqueued
+  void* base = nullptr;
+  size_t cap = 0;
+  HIP_TRY(static_scratch(&base, &cap));
+  if (c.off > cap) return AIQ_ENOSPC;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const aiq_query& q = p->q;
+  int64_t* ctr = at<int64_t>(base, o_ctr);
+  int64_t* lb = at<int64_t>(base, o_lb);
+  HashArgs h{};
+  if (p->has_build) {
+    h.keys = at<int32_t>(base, o_hk);
+    h.vals = at<int32_t>(base, o_hv);
+    h.cap_log2 = p->hash_log2;
+  }
+  const void* pkey = p->has_build ? p->probe_cols[q.probe_key_col].data : nullptr;
+  const int32_t pkey_dt = p->has_build ? p->probe_cols[q.probe_key_col].dtype : AIQ_I32;
+  HIP_TRY(launch_fill_i64(ctr, C_COUNT, 0, s));
+  if (p->has_build) {
+    HIP_TRY(launch_fill_i32(h.keys, static_cast<int64_t>(hcap), HASH_EMPTY, s));
+    const aiq_col& kc = p->build_cols[q.build_key_col];
+    const aiq_col& pc = p->build_cols[q.build_payload_col];
+    HIP_TRY(launch_hash_build(p->build_preds, kc.data, kc.dtype, pc.data, pc.dtype, p->build.n_rows, h, ctr, s));
+  }
+  int32_t* ids2 = out->sel_cap > 0 ? out->sel_ids : nullptr;
+  HIP_TRY(launch_select_lb(p->probe_preds, p->n_rows, pkey, pkey_dt, h, p->has_build, out->ids, out->ids_cap, ids2,
+                           out->sel_cap, nullptr, p->probe.list_offsets, p->probe.max_list_len, q.n_prefix, nullptr,
+                           lb, ctr, s));
+  HIP_TRY(launch_keep_selected(ctr, out->ids_cap, s));
+  HIP_TRY(launch_finalize(ctr, out->scalars, s));
+  return AIQ_OK;
+}
+
 aiq_status aiq_prefill_packed(const aiq_plan* p, const int32_t* tok, const int32_t* cu_seqlens, int32_t n_seq,
                               int64_t n_tok, int32_t logits_mode, float* logits, void* ws, size_t ws_bytes,
                               void* stream) {

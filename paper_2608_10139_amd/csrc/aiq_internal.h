@@ -104,8 +104,9 @@ hipError_t launch_cu_from_blocks(const int32_t* lens, const int64_t* blk_off, co
 // look-back over `lb`, 4 int64 per block of at least LB_MIN_ROWS rows,
 // cleared here first): out_ids
 // (and out_ids2) as launch_scatter_rows, ctr[C_SEL] = the count; with `off`
-// also cu[0..n_sel] (cu[i] = tokens of the selected rows before i, token
-// count = min(list length, max_len) + n_prefix) and ctr[C_TOK] = the total.
+// also ctr[C_TOK] = the total token count (per row min(list length,
+// max_len) + n_prefix) and, when cu is not NULL, cu[0..n_sel] (cu[i] =
+// tokens of the selected rows before i).
 // A block's token sum must stay below 2^31: REL_ROWS_PER_BLOCK *
 // (max_len + n_prefix) < 2^31.
 hipError_t launch_select_lb(const DPredList& preds, int64_t n_rows, const void* probe_key, int32_t probe_key_dtype,
@@ -391,5 +392,12 @@ hipError_t launch_gen_like(const int32_t* gen, const int64_t* n_ptr, int64_t n_u
 // dst[i * per_row ..] = src[i * per_row ..] for i < min(*n_ptr, cap_rows)
 hipError_t launch_copy_rows_i32(const int32_t* src, const int64_t* n_ptr, int64_t n_ub, int32_t per_row,
                                 int32_t* dst, int64_t cap_rows, hipStream_t s);
+
+// Fixed device scratch of the entry point that allocates nothing
+// (aiq_run_relational_static): STATIC_SCRATCH_BYTES of device memory per GPU,
+// held until the process ends.  Returns its device address on the current
+// device (looked up once per device) and its size.
+constexpr size_t STATIC_SCRATCH_BYTES = size_t(16) << 20;
+hipError_t static_scratch(void** ptr, size_t* bytes);
 
 }  // namespace aiq

@@ -7,11 +7,15 @@
 // row ids so that only survivors reach the transformer (the on-device data
 // skipping named as a roadmap item in Section 5).
 //
-// Compaction is three launches over fixed 2048-row blocks:
+// Compaction runs by default as one launch over 8192-row blocks (k_select_lb:
+// masks, the block's survivor list in LDS, a decoupled look-back for the
+// totals of earlier blocks, outputs written at their final positions).  The
+// three-launch form over blocks of REL_ROWS_PER_BLOCK rows remains:
 //   mask    : 64 rows per wave evaluated into one ballot word, block popcount
 //   scan    : exclusive scan of the block counts (one workgroup)
 //   scatter : popcount prefix inside the block + block offset -> output slot
-// The order of survivors is the row order (stable), independent of timing.
+// In both the order of survivors is the row order (stable), independent of
+// timing.  The join's hash table and the group bins live in global memory.
 #include "aiq_internal.h"
 
 namespace aiq {
@@ -892,7 +896,7 @@ __global__ __launch_bounds__(LB_THREADS) void k_select_lb(
       if (pos < out_cap2) out_ids2[pos] = id;
       else overflow = true;
     }
-    if (off) cu[pos] = tb + tx[lb_pad(i)];
+    if (cu) cu[pos] = tb + tx[lb_pad(i)];
   }
   if (join && out_payload) {   // the build payload of each survivor's match
     for (int i = t; i < cnt; i += LB_THREADS) {
@@ -904,10 +908,8 @@ __global__ __launch_bounds__(LB_THREADS) void k_select_lb(
   if (overflow) set_status(ctr, AIQ_DEV_IDS_CAP);
   if (b == nb - 1 && t == 0) {
     ctr[C_SEL] = cb + cnt;
-    if (off) {
-      ctr[C_TOK] = tb + tok;
-      cu[cb + cnt] = tb + tok;
-    }
+    if (off) ctr[C_TOK] = tb + tok;
+    if (cu) cu[cb + cnt] = tb + tok;
   }
 }
 
@@ -916,7 +918,8 @@ hipError_t launch_select_lb(const DPredList& preds, int64_t n_rows, const void* 
                             int64_t out_cap2, int32_t* out_payload, const int64_t* off, int32_t max_len,
                             int32_t n_prefix, int64_t* cu, int64_t* lb, int64_t* ctr, hipStream_t s) {
   const int64_t nb = (n_rows + LB_ROWS - 1) / LB_ROWS;
-  if (nb == 0) return off ? launch_fill_i64(cu, 1, 0, s) : hipSuccess;   // no rows: cu = {0}
+  if (!off) cu = nullptr;   // no list column: no offsets to write (cu may also be NULL with one: totals only)
+  if (nb == 0) return cu ? launch_fill_i64(cu, 1, 0, s) : hipSuccess;   // no rows: cu = {0}
   hipError_t e = launch_fill_i64(lb, 4 * nb, 0, s);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_select_lb, dim3(static_cast<unsigned>(nb)), dim3(LB_THREADS), 0, s, preds, n_rows, nb,

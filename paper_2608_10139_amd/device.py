@@ -244,6 +244,12 @@ class DeviceQuery:
         s = stream if stream is not None else torch.cuda.current_stream(self.device)
         B.aiq_run(self.plan, self.ws_ptr, self.ws_bytes, self.out, trace, s.cuda_stream)
 
+    def run_static(self, stream=None) -> None:
+        """The relational-only plan through the entry point that allocates
+        nothing (its scratch is the library's fixed device array)."""
+        s = stream if stream is not None else torch.cuda.current_stream(self.device)
+        B.aiq_run_relational_static(self.plan, self.out, s.cuda_stream)
+
     def results(self) -> dict:
         """Copies the outputs to the host (after the stream has been synchronised)."""
         sc = self.scalars.cpu().numpy()

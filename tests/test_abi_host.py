@@ -356,3 +356,30 @@ def test_pairs_workspace_follows_max_pairs():
     finally:
         B.aiq_plan_destroy(small)
         B.aiq_plan_destroy(big)
+
+
+def test_relational_static_refusals():
+    """The entry point without a workspace refuses, before enqueuing
+    anything: a plan that is not relational-only, and a plan whose scratch
+    (here a 2^21-row build table: 2^22 hash slots, 32 MiB) exceeds the fixed
+    16 MiB array."""
+    out = B.aiq_out()
+    sc = (C.c_int64 * B.AIQ_N_SCALARS)()
+    out.scalars = C.cast(sc, C.c_void_p)
+    full = B.aiq_plan_create(model(), table(), None, query())
+    try:
+        assert B.aiq_run_relational_static_status(full, out) == B.AIQ_EINVAL
+    finally:
+        B.aiq_plan_destroy(full)
+    bcols = (B.aiq_col * 2)()
+    bcols[0].data, bcols[0].dtype = FAKE, B.AIQ_I32
+    bcols[1].data, bcols[1].dtype = FAKE, B.AIQ_I8
+    build = B.aiq_table()
+    build.n_rows, build.n_cols, build.cols = 1 << 21, 2, C.cast(bcols, C.POINTER(B.aiq_col))
+    q = query()
+    q.join, q.probe_key_col, q.build_key_col, q.build_payload_col = 1, 1, 0, 1
+    big = B.aiq_plan_create(model(), table(), build, q, _opts(B.AIQ_PLAN_RELATIONAL_ONLY))
+    try:
+        assert B.aiq_run_relational_static_status(big, out) == B.AIQ_ENOSPC
+    finally:
+        B.aiq_plan_destroy(big)
