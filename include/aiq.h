@@ -5,7 +5,8 @@
  * pipeline on one HIP stream:
  *
  *   FROM      columnar table already in device memory            (Table 1, FROM)
- *   WHERE     conjunction of integer predicates -> stable selection (Table 1, WHERE)
+ *   WHERE     conjunction of integer or fp32 column predicates -> stable
+ *             selection (Table 1, WHERE)
  *   JOIN      optional inner PK-FK hash join with a filtered build table
  *             (the reviews-JOIN-movies workload of Section 4)
  *   AI_IF     gather + pack the selected rows' token lists into a variable-
@@ -365,7 +366,11 @@ enum {
 typedef struct aiq_plan aiq_plan;
 
 /*
- * Validates the model, tables and query and builds an immutable plan.
+ * Validates the model, tables and query and builds an immutable plan: the
+ * host-side counterpart of the paper's compile step (Section 3.1, Figure 2:
+ * the SQL clauses of Table 1 mapped to one program of tensor operations),
+ * here a fixed sequence of device kernels whose data-dependent sizes stay on
+ * the device.
  * probe may be NULL for a prefill-only plan (aiq_prefill_packed); build must
  * be non-NULL iff query->join.  query may be NULL for a prefill-only plan
  * that only uses AIQ_LOGITS_FULL_VOCAB.  opts may be NULL.
@@ -376,11 +381,15 @@ typedef struct aiq_plan aiq_plan;
 aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const aiq_table* build,
                            const aiq_query* query, const aiq_plan_opts* opts, aiq_plan** out);
 
-/* Bytes of device workspace aiq_run needs (256-byte aligned base required). */
+/* Bytes of device workspace aiq_run needs (256-byte aligned base required):
+ * the selection, the packed batch and one chunk's activations, sized from the
+ * table and model alone so that nothing is allocated inside the run
+ * (Section 3.3, everything resident on the device). */
 aiq_status aiq_workspace_size(const aiq_plan* plan, size_t* bytes);
 
 /*
- * Prefill passes aiq_run enqueues: the chunks of the packed batch, an upper
+ * Prefill passes aiq_run enqueues (Section 3.2: the scan over micro-batches
+ * of the selected rows): the chunks of the packed batch, an upper
  * bound fixed at plan creation from the table's token total (chunks that
  * the selection leaves empty cost one launch per kernel and no work), plus
  * one pass for a shared prompt prefix.  Each pass launches the embedding,
@@ -404,7 +413,8 @@ aiq_status aiq_plan_chunk_tokens(const aiq_plan* plan, int64_t* chunk_tokens);
 
 /*
  * *last_rows_only = 1 when the plan runs the last layer, after its q|k|v
- * projection, for the last position of each sequence only (see
+ * projection, for the last position of each sequence only (Figure 2 reads
+ * the logits of the last position alone; see
  * AIQ_PLAN_FULL_LAST_LAYER), else 0.  In that case every prefill pass (the
  * chunks and a shared prefix) launches the gate/up projection of every layer
  * but the last over all its positions, and the last layer's attention, O
@@ -414,8 +424,10 @@ aiq_status aiq_plan_chunk_tokens(const aiq_plan* plan, int64_t* chunk_tokens);
 aiq_status aiq_plan_last_layer_rows(const aiq_plan* plan, int32_t* last_rows_only);
 
 /*
- * Enqueues the whole query on `stream`.  The workspace contents on entry do
- * not matter.  Outputs are valid after the caller synchronises the stream.
+ * Enqueues the whole query on `stream` (Section 3.3: the relational part and
+ * the semantic operator as one device program with no host round trip;
+ * Figure 2's filter on the last-position label logits and masked
+ * aggregate).  The workspace contents on entry do not matter.  Outputs are valid after the caller synchronises the stream.
  * Errors: AIQ_EINVAL (NULL plan/out/scalars/ids, prefill-only plan, a
  * group-by without grp_* buffers), AIQ_ENOSPC (ws_bytes too small),
  * AIQ_EHIP.  `trace` may be NULL.
@@ -445,7 +457,8 @@ aiq_status aiq_run(const aiq_plan* plan, void* workspace, size_t ws_bytes, const
  */
 aiq_status aiq_run_relational_static(const aiq_plan* plan, const aiq_out* out, void* stream);
 
-/* Bytes of workspace aiq_prefill_packed needs for up to max_tokens tokens. */
+/* Bytes of workspace aiq_prefill_packed needs for up to max_tokens tokens
+ * (the split-execution baseline's model half, Section 3.3). */
 aiq_status aiq_prefill_workspace_size(const aiq_plan* plan, int64_t max_tokens, size_t* bytes);
 
 /*
@@ -463,9 +476,28 @@ aiq_status aiq_prefill_packed(const aiq_plan* plan, const int32_t* tok, const in
                               int32_t n_seq, int64_t n_tok, int32_t logits_mode, float* logits,
                               void* workspace, size_t ws_bytes, void* stream);
 
+/*
+ * Converts n weight elements in device memory from src_dtype to dst_dtype on
+ * `stream`: AIQ_BF16 -> AIQ_F16 only, each value widened exactly and rounded
+ * to the nearest fp16 (ties to even; magnitudes below 2^-14 become fp16
+ * subnormals, above 65504 infinities).  bf16-stored models run their 16-bit
+ * projections on fp16 images of the weights (10 mantissa bits for the
+ * activations instead of 7 at the same MFMA rate, the precision that keeps a
+ * 16-layer model's label logits within the bf16 tolerance, Figure 2's
+ * last-position comparison); aiq_model.wdtype = AIQ_F16 then points at the
+ * converted arrays.  src and dst are 16-byte aligned, distinct, owned by the
+ * caller.  Errors: AIQ_EINVAL (NULL pointer with n > 0, negative n,
+ * misalignment), AIQ_EUNSUPPORTED (another pair of types), AIQ_EHIP.
+ */
+aiq_status aiq_convert_weights(const void* src, int32_t src_dtype, void* dst, int32_t dst_dtype, int64_t n,
+                               void* stream);
+
+/* Frees a plan (host memory only; NULL is ignored). */
 void aiq_plan_destroy(aiq_plan* plan);
 
+/* A static description of an aiq_status value. */
 const char* aiq_status_str(int32_t status);
+/* AIQ_ABI_VERSION of the library: bindings refuse another layout. */
 int32_t aiq_abi_version(void);
 
 #ifdef __cplusplus

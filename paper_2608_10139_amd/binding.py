@@ -102,7 +102,7 @@ class aiq_trace(C.Structure):
 
 
 EXPORTS = ("aiq_plan_create", "aiq_workspace_size", "aiq_plan_passes", "aiq_plan_chunk_tokens",
-           "aiq_plan_last_layer_rows", "aiq_run", "aiq_run_relational_static",
+           "aiq_plan_last_layer_rows", "aiq_run", "aiq_run_relational_static", "aiq_convert_weights",
            "aiq_prefill_workspace_size",
            "aiq_prefill_packed", "aiq_plan_destroy", "aiq_status_str", "aiq_abi_version")
 
@@ -138,6 +138,8 @@ def load(path: str = LIB_PATH) -> C.CDLL:
     lib.aiq_plan_last_layer_rows.restype = C.c_int
     lib.aiq_run.argtypes = [P, P, C.c_size_t, C.POINTER(aiq_out), C.POINTER(aiq_trace), P]
     lib.aiq_run.restype = C.c_int
+    lib.aiq_convert_weights.argtypes = [P, C.c_int32, P, C.c_int32, C.c_int64, P]
+    lib.aiq_convert_weights.restype = C.c_int
     lib.aiq_run_relational_static.argtypes = [P, C.POINTER(aiq_out), P]
     lib.aiq_run_relational_static.restype = C.c_int
     lib.aiq_prefill_workspace_size.argtypes = [P, C.c_int64, C.POINTER(C.c_size_t)]
@@ -233,6 +235,10 @@ def aiq_run_relational_static(plan, out: aiq_out, stream: int = 0) -> None:
 def aiq_run_relational_static_status(plan, out: aiq_out, stream: int = 0) -> int:
     """Like aiq_run_relational_static but returns the status (for error-path tests)."""
     return load().aiq_run_relational_static(plan, C.byref(out), stream)
+
+
+def aiq_convert_weights(src_ptr: int, src_dtype: int, dst_ptr: int, dst_dtype: int, n: int, stream: int = 0) -> None:
+    check("aiq_convert_weights", load().aiq_convert_weights(src_ptr, src_dtype, dst_ptr, dst_dtype, n, stream))
 
 
 def aiq_prefill_packed(plan, tok_ptr: int, cu_ptr: int, n_seq: int, n_tok: int, mode: int,

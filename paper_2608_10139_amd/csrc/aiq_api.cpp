@@ -892,14 +892,17 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
     p->max_seq = static_cast<int32_t>(max_own + q.n_prefix);   // positions (rotary table rows)
     // longest packed sequence: a chunk must hold one whole
     const int64_t max_packed = p->share_prefix ? std::max<int64_t>(max_own, q.n_prefix) : p->max_seq;
-    // default chunk: about 48 GB of per-token activations (a fraction of one
-    // MI355X's 288 GB), at most 4M tokens
-    // (+ every layer's kept q|k|v rows when the rows go on to generate)
+    // default chunk: about 96 GB of per-token activations (a third of one
+    // MI355X's 288 GB), at most 4M tokens.  The host loops over an upper bound
+    // of chunks fixed by the table's tokens; the passes a selective query
+    // leaves empty each cost one launch per kernel, so larger chunks also mean
+    // fewer of them (+ every layer's kept q|k|v rows when the rows go on to
+    // generate)
     const int64_t per_tok = static_cast<int64_t>(resid_bytes(p)) +
                             static_cast<int64_t>(model->d_model + p->n_qkv + p->d_q + model->d_ff) *
                                 (p->bf16 ? 2 : 4) + 4 +
                             (p->gen > 0 ? static_cast<int64_t>(p->n_layers) * p->n_qkv * 2 : 0);
-    const int64_t def_chunk = std::min<int64_t>((int64_t(48) << 30) / per_tok, int64_t(4) << 20);
+    const int64_t def_chunk = std::min<int64_t>((int64_t(96) << 30) / per_tok, int64_t(4) << 20);
     int64_t ct = (opts && opts->chunk_tokens > 0) ? opts->chunk_tokens : def_chunk;
     ct = std::max<int64_t>(ct, max_packed);
     ct = std::min<int64_t>(ct, std::max<int64_t>(p->t_ub + p->n_seq_ub, max_packed));   // one chunk when all fits
@@ -1214,6 +1217,15 @@ aiq_status aiq_run_relational_static(const aiq_plan* p, const aiq_out* out, void
                            lb, ctr, s));
   HIP_TRY(launch_keep_selected(ctr, out->ids_cap, s));
   HIP_TRY(launch_finalize(ctr, out->scalars, s));
+  return AIQ_OK;
+}
+
+aiq_status aiq_convert_weights(const void* src, int32_t src_dtype, void* dst, int32_t dst_dtype, int64_t n,
+                               void* stream) {
+  if (n < 0 || (n > 0 && (!src || !dst))) return AIQ_EINVAL;
+  if (src_dtype != AIQ_BF16 || dst_dtype != AIQ_F16) return AIQ_EUNSUPPORTED;
+  if (reinterpret_cast<uintptr_t>(src) % 16 || reinterpret_cast<uintptr_t>(dst) % 16) return AIQ_EINVAL;
+  HIP_TRY(launch_bf16_to_f16(src, dst, n, static_cast<hipStream_t>(stream)));
   return AIQ_OK;
 }
 

@@ -157,6 +157,9 @@ hipError_t launch_packed_desc(const int32_t* cu32, int32_t n_seq, int64_t n_tok,
 // The shared prompt prefix as a one-sequence batch: tok[0..n) = prefix,
 // cu = {0, n}, desc = one chunk of n tokens.
 hipError_t launch_prefix_batch(const Prefix& prefix, int32_t* tok, int64_t* cu, int64_t* desc, hipStream_t s);
+// bf16 -> fp16 conversion of n elements (nearest, ties to even); src and dst
+// 16-byte aligned.
+hipError_t launch_bf16_to_f16(const void* src, void* dst, int64_t n, hipStream_t s);
 hipError_t launch_copy_row_f32(const float* src, float* dst, int32_t n, hipStream_t s);
 
 // per-chunk transformer

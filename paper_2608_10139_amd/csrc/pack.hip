@@ -328,4 +328,33 @@ hipError_t launch_embed_norm(const int64_t* desc, const int64_t* cu, const int32
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ weight conversion
+// bf16 -> fp16, element by element: the bf16 value widened exactly to fp32,
+// then rounded to the nearest fp16 (ties to even; values below 2^-14 become
+// fp16 subnormals, above 65504 infinities), 8 elements per thread in 16-byte
+// pieces plus a scalar tail.
+__global__ void k_bf16_to_f16(const uint16_t* src, uint16_t* dst, int64_t n) {
+  const int64_t n8 = n / 8;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n8; i += stride) {
+    const uint4 v = reinterpret_cast<const uint4*>(src)[i];
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    uint32_t o[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      o[k] = f2h(bf2f(static_cast<uint16_t>(w[k] & 0xFFFFu))) |
+             (static_cast<uint32_t>(f2h(bf2f(static_cast<uint16_t>(w[k] >> 16)))) << 16);
+    reinterpret_cast<uint4*>(dst)[i] = make_uint4(o[0], o[1], o[2], o[3]);
+  }
+  for (int64_t i = n8 * 8 + blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += stride)
+    dst[i] = f2h(bf2f(src[i]));
+}
+
+hipError_t launch_bf16_to_f16(const void* src, void* dst, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_bf16_to_f16, dim3(grid_for(n / 8 + 1, 256, 8192)), dim3(256), 0, s,
+                     static_cast<const uint16_t*>(src), static_cast<uint16_t*>(dst), n);
+  return hipGetLastError();
+}
+
 }  // namespace aiq

@@ -65,8 +65,11 @@ class DeviceModel:
 
         def up(a):
             t = _dev(a, device)
-            if t.dtype == torch.bfloat16 and self.compute == "f16":
-                t = t.to(torch.float16)
+            if t.dtype == torch.bfloat16 and self.compute == "f16":   # fp16 images, converted by the library
+                h = torch.empty(t.shape, dtype=torch.float16, device=t.device)
+                B.aiq_convert_weights(t.data_ptr(), B.AIQ_BF16, h.data_ptr(), B.AIQ_F16, t.numel(),
+                                      torch.cuda.current_stream(t.device).cuda_stream)
+                t = h
             self.keep.append(t)
             return t
 

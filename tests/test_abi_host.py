@@ -383,3 +383,12 @@ def test_relational_static_refusals():
         assert B.aiq_run_relational_static_status(big, out) == B.AIQ_ENOSPC
     finally:
         B.aiq_plan_destroy(big)
+
+
+def test_convert_weights_refusals():
+    """Refused before anything is enqueued: another pair of types, a negative
+    count, a NULL pointer with elements, a misaligned pointer."""
+    assert B.load().aiq_convert_weights(FAKE, B.AIQ_F16, FAKE, B.AIQ_BF16, 8, None) == B.AIQ_EUNSUPPORTED
+    assert B.load().aiq_convert_weights(FAKE, B.AIQ_BF16, FAKE, B.AIQ_F16, -1, None) == B.AIQ_EINVAL
+    assert B.load().aiq_convert_weights(None, B.AIQ_BF16, FAKE, B.AIQ_F16, 8, None) == B.AIQ_EINVAL
+    assert B.load().aiq_convert_weights(FAKE + 2, B.AIQ_BF16, FAKE, B.AIQ_F16, 8, None) == B.AIQ_EINVAL
