@@ -86,7 +86,7 @@ typedef enum aiq_logits_mode { AIQ_LOGITS_LABELS = 1, AIQ_LOGITS_FULL_VOCAB = 2 
 /* device status bits (aiq_out.scalars[AIQ_S_STATUS]) */
 #define AIQ_DEV_TOKEN_RANGE 0x01  /* a token id outside [0, vocab): treated as 0   */
 #define AIQ_DEV_DUP_KEY     0x02  /* duplicate key among the passing build rows     */
-#define AIQ_DEV_HASH_FULL   0x04  /* hash table overflow                            */
+#define AIQ_DEV_HASH_FULL   0x04  /* hash table overflow, or an INT32_MIN build key  */
 #define AIQ_DEV_IDS_CAP     0x08  /* more kept rows than aiq_out.ids_cap            */
 #define AIQ_DEV_GROUP_RANGE 0x10  /* group key outside [0, n_group_keys): skipped   */
 #define AIQ_DEV_LIST_LEN    0x20  /* a row's list longer than max_list_len          */
@@ -185,7 +185,12 @@ typedef struct aiq_query {
   aiq_pred preds[AIQ_MAX_PREDS];       /* conjunction over probe columns */
   /* optional inner join probe.cols[probe_key_col] = build.cols[build_key_col]
      with the build rows passing build_preds; the build key must be unique
-     among passing rows.  build_payload_col is carried to each joined row. */
+     among passing rows and must not be INT32_MIN (the empty-slot value; such
+     a build row sets AIQ_DEV_HASH_FULL, a probe key INT32_MIN matches
+     nothing).  build_payload_col is carried to each joined row.  The passing
+     build rows go into a hash table in device memory; when at most 1024 pass,
+     the one-launch compaction probes a copy of it held in each workgroup's
+     LDS (Section 4, reviews JOIN movies on the movie id). */
   int32_t join;                        /* 0 = no join, 1 = inner PK-FK join */
   int32_t probe_key_col, build_key_col, build_payload_col;
   int32_t n_build_pred;
@@ -201,7 +206,14 @@ typedef struct aiq_query {
   int32_t agg;                         /* aiq_agg */
   int32_t group_col;                   /* AVG_LABEL_COUNT_BY: probe key column (integer);
                                           SUM_F32: the summed probe column (AIQ_F32) */
-  int32_t n_group_keys;                /* group keys are codes in [0, n_group_keys) */
+  int32_t n_group_keys;                /* > 0: group keys are codes in [0, n_group_keys),
+                                          aggregated in dense bins (keys outside flag
+                                          AIQ_DEV_GROUP_RANGE); 0: any int32 key
+                                          (INT32_MIN included), aggregated in a hash
+                                          table and emitted in ascending key order;
+                                          out->grp_cap must then cover the distinct keys
+                                          (at most the probe rows, or for COUNT_BY_PAYLOAD
+                                          the build rows) or AIQ_DEV_GROUP_CAP is set */
   /* AI_TRANSFORM (Table 1; Section 4, Q3 and Q5).  gen_tokens > 0 replaces
      the label decision: every selected row's sequence is continued by up
      to gen_tokens tokens, each the argmax of the last position's logits over

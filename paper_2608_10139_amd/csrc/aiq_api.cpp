@@ -49,6 +49,10 @@ struct aiq_plan {
   int64_t n_rows = 0, t_ub = 0, chunk_tokens = 0, n_chunks = 0, t_cap = 0, seq_ub = 0;
   int32_t max_seq = 0;
   int hash_log2 = 0;
+  // GROUP BY over arbitrary keys (n_group_keys == 0): table of 2^hgroup_log2
+  // slots for at most hgroup_max distinct keys
+  int hgroup_log2 = 0;
+  int64_t hgroup_max = 0;
   DPredList probe_preds{}, build_preds{};
   Prefix prefix{};
 };
@@ -156,7 +160,7 @@ struct Layout {
   size_t ctr, mask, blk_cnt, blk_off, sel, payload, lens, label, logits, cu, blk_tok, tok_off, packed, hkeys, hvals,
       bins, desc, rcos, rsin, rrev, x, delta, h, qkv, att, ffn, pos, hf, ssp, rs, pkv, ptok, pcu, pdesc, pxlast,
       kvc, gkv, glog, gtok, gdone, gen, gdesc, gcnt, kcount, koff, prank, psorted, pcnt, poff, pscan, pa, pb,
-      lb, xl, ldesc, laux, total;
+      lb, xl, ldesc, laux, jkeys, jvals, jlog2, gslot, gkey0, gval0, gkey1, gval1, ghist, gn, total;
 };
 
 size_t act_bytes(const aiq_plan* p) { return p->bf16 ? 2 : 4; }
@@ -231,6 +235,11 @@ Layout run_layout(const aiq_plan* p) {
   const size_t hcap = p->hash_log2 ? (size_t(1) << p->hash_log2) : 1;
   L.hkeys = c.take(hcap * 4);
   L.hvals = c.take(hcap * 4);
+  if (p->has_build) {   // the build table rehashed for LDS probes
+    L.jkeys = c.take(JOIN_LDS_SLOTS * 4);
+    L.jvals = c.take(JOIN_LDS_SLOTS * 4);
+    L.jlog2 = c.take(4);
+  }
   if (p->rel_only) {   // no packed batch, model activations or groups
     L.total = c.off;
     return L;
@@ -238,6 +247,16 @@ Layout run_layout(const aiq_plan* p) {
   L.packed = c.take(static_cast<size_t>(p->t_ub + 1) * 4);
   L.bins = c.take(std::max<size_t>(static_cast<size_t>(std::max(p->q.n_group_keys, 1)) * 16,
                                    SUM_BLOCKS * sizeof(double)));   // group bins, or SUM partials
+  if (p->hgroup_log2) {   // hash GROUP BY: slot | count | sum arrays, sort buffers, digit histograms
+    const size_t hs = size_t(1) << p->hgroup_log2, mg = static_cast<size_t>(p->hgroup_max);
+    L.gslot = c.take(hs * 24);
+    L.gkey0 = c.take(mg * 4);
+    L.gval0 = c.take(mg * 4);
+    L.gkey1 = c.take(mg * 4);
+    L.gval1 = c.take(mg * 4);
+    L.ghist = c.take(static_cast<size_t>(256 * hash_group_sort_blocks(p->hgroup_max)) * 8);
+    L.gn = c.take(8);
+  }
   L.desc = c.take(static_cast<size_t>(p->n_chunks) * D_STRIDE * 8);
   L.rcos = c.take(static_cast<size_t>(p->max_seq) * (p->hd / 2) * 4);
   L.rsin = c.take(static_cast<size_t>(p->max_seq) * (p->hd / 2) * 4);
@@ -865,10 +884,10 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
         if (p->gen > 0) return fail(AIQ_EINVAL);   // no label to average
         if (q.group_col < 0 || q.group_col >= static_cast<int>(p->probe_cols.size())) return fail(AIQ_EINVAL);
         if (!int_dtype(p->probe_cols[q.group_col].dtype)) return fail(AIQ_EUNSUPPORTED);
-        if (q.n_group_keys <= 0) return fail(AIQ_EINVAL);
+        if (q.n_group_keys < 0) return fail(AIQ_EINVAL);
         break;
       case AIQ_AGG_COUNT_BY_PAYLOAD:
-        if (!q.join || q.n_group_keys <= 0) return fail(AIQ_EINVAL);
+        if (!q.join || q.n_group_keys < 0) return fail(AIQ_EINVAL);
         break;
       case AIQ_AGG_SUM_F32:
         if (q.group_col < 0 || q.group_col >= static_cast<int>(p->probe_cols.size())) return fail(AIQ_EINVAL);
@@ -916,6 +935,16 @@ aiq_status aiq_plan_create(const aiq_model* model, const aiq_table* probe, const
     p->gen_blocks = p->gen > 0 ? static_cast<int32_t>((p->seq_ub + GEN_HEAD_ROWS - 1) / GEN_HEAD_ROWS) : 0;
     p->prefix.n = q.n_prefix;
     for (int k = 0; k < q.n_prefix; ++k) p->prefix.tok[k] = q.prefix[k];
+    // GROUP BY over any int32 key: at most one group per selected row (by
+    // probe column) or per build row (by the joined payload)
+    if ((q.agg == AIQ_AGG_AVG_LABEL_COUNT_BY || q.agg == AIQ_AGG_COUNT_BY_PAYLOAD) && q.n_group_keys == 0) {
+      p->hgroup_max = std::max<int64_t>(q.agg == AIQ_AGG_COUNT_BY_PAYLOAD ? std::min(p->build.n_rows, p->n_rows)
+                                                                           : p->n_rows, 1);
+      int lg = 6;
+      while ((int64_t(1) << lg) < 2 * p->hgroup_max) ++lg;
+      if (lg > 31) return fail(AIQ_EUNSUPPORTED);
+      p->hgroup_log2 = lg;
+    }
   }
   *out = p;
   return AIQ_OK;
@@ -994,6 +1023,12 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
     h.vals = at<int32_t>(ws, L.hvals);
     h.cap_log2 = p->hash_log2;
   }
+  StagedHash staged{};
+  if (p->has_build) {
+    staged.keys = at<int32_t>(ws, L.jkeys);
+    staged.vals = at<int32_t>(ws, L.jvals);
+    staged.log2_out = at<int32_t>(ws, L.jlog2);
+  }
   const void* pkey = p->has_build ? p->probe_cols[q.probe_key_col].data : nullptr;
   const int32_t pkey_dt = p->has_build ? p->probe_cols[q.probe_key_col].dtype : AIQ_I32;
 
@@ -1005,6 +1040,7 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
     const aiq_col& kc = p->build_cols[q.build_key_col];
     const aiq_col& pc = p->build_cols[q.build_payload_col];
     HIP_TRY(launch_hash_build(p->build_preds, kc.data, kc.dtype, pc.data, pc.dtype, p->build.n_rows, h, ctr, s));
+    if (p->lb_compact) HIP_TRY(launch_hash_stage(h, staged, s));
   }
   const int32_t npre_rows = p->share_prefix ? 0 : q.n_prefix;   // prefix tokens packed into each row
   // selected ids go straight into the caller's ids when nothing else follows
@@ -1014,7 +1050,8 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
   const int64_t cap2 = p->rel_only ? out->sel_cap : 0;
   if (p->lb_compact) {
     // masks, compaction, join payloads and token offsets in one launch
-    HIP_TRY(launch_select_lb(p->probe_preds, n, pkey, pkey_dt, h, p->has_build, ids1, cap1, ids2, cap2, payload,
+    HIP_TRY(launch_select_lb(p->probe_preds, n, pkey, pkey_dt, h, p->has_build, p->has_build ? &staged : nullptr,
+                             ids1, cap1, ids2, cap2, payload,
                              p->pairs ? nullptr : p->probe.list_offsets, p->probe.max_list_len, npre_rows, cu,
                              at<int64_t>(ws, L.lb), ctr, s));
   } else {
@@ -1142,15 +1179,32 @@ aiq_status aiq_run(const aiq_plan* p, void* ws, size_t ws_bytes, const aiq_out* 
     HIP_TRY(launch_copy_ids(sel, ctr + C_SEL, n, out->ids, out->ids_cap, ctr, 1, s));
   }
   if (grouped) {
-    int64_t* bins = at<int64_t>(ws, L.bins);
-    HIP_TRY(launch_fill_i64(bins, 2 * int64_t(q.n_group_keys), 0, s));
     const int mode = q.agg == AIQ_AGG_AVG_LABEL_COUNT_BY ? 1 : 2;
     const void* kcol = mode == 1 ? p->probe_cols[q.group_col].data : nullptr;
     const int32_t kdt = mode == 1 ? p->probe_cols[q.group_col].dtype : AIQ_I32;
-    HIP_TRY(launch_group_accumulate(sel, label, payload, nullptr, ctr + C_SEL, n, kcol, kdt, mode, q.n_group_keys,
-                                    bins, ctr, s));
-    HIP_TRY(launch_group_emit(bins, q.n_group_keys, out->grp_key, out->grp_count, out->grp_sum, out->grp_avg,
-                              out->grp_cap, mode, ctr, s));
+    if (p->hgroup_log2) {   // any int32 key: hash table, then the groups sorted by key
+      HashAggArgs g{};
+      const size_t hs = size_t(1) << p->hgroup_log2;
+      g.slot = at<uint64_t>(ws, L.gslot);
+      g.cnt = at<int64_t>(ws, L.gslot + hs * 8);
+      g.sum = at<int64_t>(ws, L.gslot + hs * 16);
+      g.cap_log2 = p->hgroup_log2;
+      g.key0 = at<uint32_t>(ws, L.gkey0);
+      g.val0 = at<uint32_t>(ws, L.gval0);
+      g.key1 = at<uint32_t>(ws, L.gkey1);
+      g.val1 = at<uint32_t>(ws, L.gval1);
+      g.hist = at<int64_t>(ws, L.ghist);
+      g.n_groups = at<int64_t>(ws, L.gn);
+      HIP_TRY(launch_hash_group(sel, label, payload, ctr + C_SEL, n, kcol, kdt, mode, g, p->hgroup_max,
+                                out->grp_key, out->grp_count, out->grp_sum, out->grp_avg, out->grp_cap, ctr, s));
+    } else {   // keys are codes in [0, n_group_keys): dense bins
+      int64_t* bins = at<int64_t>(ws, L.bins);
+      HIP_TRY(launch_fill_i64(bins, 2 * int64_t(q.n_group_keys), 0, s));
+      HIP_TRY(launch_group_accumulate(sel, label, payload, nullptr, ctr + C_SEL, n, kcol, kdt, mode,
+                                      q.n_group_keys, bins, ctr, s));
+      HIP_TRY(launch_group_emit(bins, q.n_group_keys, out->grp_key, out->grp_count, out->grp_sum, out->grp_avg,
+                                out->grp_cap, mode, ctr, s));
+    }
   }
   if (q.agg == AIQ_AGG_SUM_F32)
     HIP_TRY(launch_sum_f32(sel, label, ctr + C_SEL, static_cast<const float*>(p->probe_cols[q.group_col].data),
@@ -1187,6 +1241,9 @@ aiq_status aiq_run_relational_static(const aiq_plan* p, const aiq_out* out, void
   const size_t hcap = p->has_build ? (size_t(1) << p->hash_log2) : 0;
   const size_t o_hk = c.take(hcap * 4);
   const size_t o_hv = c.take(hcap * 4);
+  const size_t o_jk = c.take(p->has_build ? JOIN_LDS_SLOTS * 4 : 0);
+  const size_t o_jv = c.take(p->has_build ? JOIN_LDS_SLOTS * 4 : 0);
+  const size_t o_jl = c.take(p->has_build ? 4 : 0);
   if (c.off > STATIC_SCRATCH_BYTES) return AIQ_ENOSPC;   // before any HIP call: nothing enqueued
   void* base = nullptr;
   size_t cap = 0;
@@ -1202,6 +1259,7 @@ aiq_status aiq_run_relational_static(const aiq_plan* p, const aiq_out* out, void
     h.vals = at<int32_t>(base, o_hv);
     h.cap_log2 = p->hash_log2;
   }
+  StagedHash staged{at<int32_t>(base, o_jk), at<int32_t>(base, o_jv), at<int32_t>(base, o_jl)};
   const void* pkey = p->has_build ? p->probe_cols[q.probe_key_col].data : nullptr;
   const int32_t pkey_dt = p->has_build ? p->probe_cols[q.probe_key_col].dtype : AIQ_I32;
   HIP_TRY(launch_fill_i64(ctr, C_COUNT, 0, s));
@@ -1210,11 +1268,12 @@ aiq_status aiq_run_relational_static(const aiq_plan* p, const aiq_out* out, void
     const aiq_col& kc = p->build_cols[q.build_key_col];
     const aiq_col& pc = p->build_cols[q.build_payload_col];
     HIP_TRY(launch_hash_build(p->build_preds, kc.data, kc.dtype, pc.data, pc.dtype, p->build.n_rows, h, ctr, s));
+    HIP_TRY(launch_hash_stage(h, staged, s));
   }
   int32_t* ids2 = out->sel_cap > 0 ? out->sel_ids : nullptr;
-  HIP_TRY(launch_select_lb(p->probe_preds, p->n_rows, pkey, pkey_dt, h, p->has_build, out->ids, out->ids_cap, ids2,
-                           out->sel_cap, nullptr, p->probe.list_offsets, p->probe.max_list_len, q.n_prefix, nullptr,
-                           lb, ctr, s));
+  HIP_TRY(launch_select_lb(p->probe_preds, p->n_rows, pkey, pkey_dt, h, p->has_build,
+                           p->has_build ? &staged : nullptr, out->ids, out->ids_cap, ids2, out->sel_cap, nullptr,
+                           p->probe.list_offsets, p->probe.max_list_len, q.n_prefix, nullptr, lb, ctr, s));
   HIP_TRY(launch_keep_selected(ctr, out->ids_cap, s));
   HIP_TRY(launch_finalize(ctr, out->scalars, s));
   return AIQ_OK;

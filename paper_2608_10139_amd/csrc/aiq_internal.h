@@ -48,6 +48,33 @@ struct HashArgs {
 
 constexpr int32_t HASH_EMPTY = INT32_MIN;
 
+// The join's build table rehashed for probing from LDS: 2^(*log2_out) slots
+// (keys, vals) when that is at most JOIN_LDS_SLOTS, else *log2_out = 0 and
+// the probes read the global table.
+constexpr int JOIN_LDS_SLOTS = 2048;
+struct StagedHash {
+  int32_t* keys;      // [JOIN_LDS_SLOTS]
+  int32_t* vals;      // [JOIN_LDS_SLOTS]
+  int32_t* log2_out;  // device word
+};
+
+// GROUP BY over arbitrary int32 keys: an open-addressing table of 2^cap_log2
+// slots in global memory (slot words: key bits | 1 << 32, 0 = empty; slot,
+// cnt and sum are consecutive arrays of 2^cap_log2 entries each, cleared by
+// the launcher), and the buffers of the sort of its occupied slots by key.
+struct HashAggArgs {
+  uint64_t* slot;
+  int64_t* cnt;
+  int64_t* sum;
+  int32_t cap_log2;
+  uint32_t* key0;     // [max_groups] x 4 ping-pong sort buffers
+  uint32_t* val0;
+  uint32_t* key1;
+  uint32_t* val1;
+  int64_t* hist;      // [256 * hash_group_sort_blocks(max_groups)]
+  int64_t* n_groups;  // device word: occupied slots
+};
+
 // relational block geometry: 256 threads x 32 rows
 constexpr int REL_THREADS = 256;
 constexpr int REL_ROWS_PER_THREAD = 32;
@@ -109,16 +136,31 @@ hipError_t launch_cu_from_blocks(const int32_t* lens, const int64_t* blk_off, co
 // tokens of the selected rows before i).
 // A block's token sum must stay below 2^31: REL_ROWS_PER_BLOCK *
 // (max_len + n_prefix) < 2^31.
+// With a join and st non-null, the probes read the LDS-staged table (st,
+// written by launch_hash_stage) when it fits, else h.
 hipError_t launch_select_lb(const DPredList& preds, int64_t n_rows, const void* probe_key, int32_t probe_key_dtype,
-                            HashArgs h, int join, int32_t* out_ids, int64_t out_cap, int32_t* out_ids2,
-                            int64_t out_cap2, int32_t* out_payload, const int64_t* off, int32_t max_len,
-                            int32_t n_prefix, int64_t* cu, int64_t* lb, int64_t* ctr, hipStream_t s);
+                            HashArgs h, int join, const StagedHash* st, int32_t* out_ids, int64_t out_cap,
+                            int32_t* out_ids2, int64_t out_cap2, int32_t* out_payload, const int64_t* off,
+                            int32_t max_len, int32_t n_prefix, int64_t* cu, int64_t* lb, int64_t* ctr,
+                            hipStream_t s);
 // ctr[C_KEPT] = ctr[C_SEL] (every selected row kept), flagged if above cap.
 hipError_t launch_keep_selected(int64_t* ctr, int64_t cap, hipStream_t s);
 hipError_t launch_group_accumulate(const int32_t* sel, const int32_t* label, const int32_t* payload,
                                    const uint8_t* keep_by_label, const int64_t* n_ptr, int64_t n_ub,
                                    const void* key_col, int32_t key_dtype, int mode,
                                    int32_t n_keys, int64_t* bins, int64_t* ctr, hipStream_t s);
+// GROUP BY with a hash table (any int32 key; mode as launch_group_accumulate):
+// groups in ascending key order written to key_out / cnt_out / sum_out /
+// avg_out (at most cap, more flag AIQ_DEV_GROUP_CAP), ctr[C_GROUPS] = the
+// number written.  max_groups bounds the distinct keys; 2^g.cap_log2 >=
+// 2 * max_groups.
+int64_t hash_group_sort_blocks(int64_t max_groups);
+hipError_t launch_hash_group(const int32_t* sel, const int32_t* label, const int32_t* payload, const int64_t* n_ptr,
+                             int64_t n_ub, const void* key_col, int32_t key_dtype, int mode, HashAggArgs g,
+                             int64_t max_groups, int32_t* key_out, int64_t* cnt_out, int64_t* sum_out,
+                             double* avg_out, int64_t cap, int64_t* ctr, hipStream_t s);
+// Rehashes the built join table for LDS probing (see StagedHash).
+hipError_t launch_hash_stage(HashArgs h, StagedHash st, hipStream_t s);
 hipError_t launch_group_emit(const int64_t* bins, int32_t n_keys, int32_t* key_out,
                              int64_t* cnt_out, int64_t* sum_out, double* avg_out, int64_t cap,
                              int mode, int64_t* ctr, hipStream_t s);

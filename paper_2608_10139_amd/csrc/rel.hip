@@ -15,7 +15,10 @@
 //   scan    : exclusive scan of the block counts (one workgroup)
 //   scatter : popcount prefix inside the block + block offset -> output slot
 // In both the order of survivors is the row order (stable), independent of
-// timing.  The join's hash table and the group bins live in global memory.
+// timing.  The join's hash table is built in global memory; the one-launch
+// form probes a copy of it in LDS when it fits (hashagg.hip rehashes it).
+// The dense-key GROUP BY bins live in global memory, privatised in LDS per
+// block; GROUP BY over arbitrary keys is in hashagg.hip.
 #include "aiq_internal.h"
 
 namespace aiq {
@@ -697,10 +700,28 @@ __device__ __forceinline__ int64_t wave_sum64(int64_t v) {
   return v;
 }
 
+// STAGED (joins): the block first copies the rehashed build table into LDS
+// when it fits (st.log2_out > 0) and probes it there.
+template <bool STAGED>
 __global__ __launch_bounds__(LB_THREADS) void k_select_lb(
     DPredList preds, int64_t n_rows, int64_t nb, const void* probe_key, int32_t pk_dt, HashArgs h, int join,
-    int32_t* out_ids, int64_t out_cap, int32_t* out_ids2, int64_t out_cap2, int32_t* out_payload,
+    StagedHash st, int32_t* out_ids, int64_t out_cap, int32_t* out_ids2, int64_t out_cap2, int32_t* out_payload,
     const int64_t* off, int32_t max_len, int32_t n_prefix, int64_t* cu, int64_t* lb, int64_t* ctr) {
+  __shared__ int32_t jk[STAGED ? JOIN_LDS_SLOTS : 1];
+  __shared__ int32_t jv[STAGED ? JOIN_LDS_SLOTS : 1];
+  if (STAGED) {
+    const int lg = *st.log2_out;
+    if (lg > 0) {
+      for (int i = threadIdx.x; i < (1 << lg); i += LB_THREADS) {
+        jk[i] = st.keys[i];
+        jv[i] = st.vals[i];
+      }
+      __syncthreads();
+      h.keys = jk;   // generic pointers into this block's LDS
+      h.vals = jv;
+      h.cap_log2 = lg;
+    }
+  }
   __shared__ uint64_t words[LB_WORDS];
   __shared__ int32_t wpre[LB_WORDS + 1];
   __shared__ int32_t wtot;
@@ -914,17 +935,23 @@ __global__ __launch_bounds__(LB_THREADS) void k_select_lb(
 }
 
 hipError_t launch_select_lb(const DPredList& preds, int64_t n_rows, const void* probe_key, int32_t probe_key_dtype,
-                            HashArgs h, int join, int32_t* out_ids, int64_t out_cap, int32_t* out_ids2,
-                            int64_t out_cap2, int32_t* out_payload, const int64_t* off, int32_t max_len,
-                            int32_t n_prefix, int64_t* cu, int64_t* lb, int64_t* ctr, hipStream_t s) {
+                            HashArgs h, int join, const StagedHash* st, int32_t* out_ids, int64_t out_cap,
+                            int32_t* out_ids2, int64_t out_cap2, int32_t* out_payload, const int64_t* off,
+                            int32_t max_len, int32_t n_prefix, int64_t* cu, int64_t* lb, int64_t* ctr,
+                            hipStream_t s) {
   const int64_t nb = (n_rows + LB_ROWS - 1) / LB_ROWS;
   if (!off) cu = nullptr;   // no list column: no offsets to write (cu may also be NULL with one: totals only)
   if (nb == 0) return cu ? launch_fill_i64(cu, 1, 0, s) : hipSuccess;   // no rows: cu = {0}
   hipError_t e = launch_fill_i64(lb, 4 * nb, 0, s);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_select_lb, dim3(static_cast<unsigned>(nb)), dim3(LB_THREADS), 0, s, preds, n_rows, nb,
-                     probe_key, probe_key_dtype, h, join, out_ids, out_cap, out_ids2, out_cap2, out_payload, off,
-                     max_len, n_prefix, cu, lb, ctr);
+  if (join && st)
+    hipLaunchKernelGGL(k_select_lb<true>, dim3(static_cast<unsigned>(nb)), dim3(LB_THREADS), 0, s, preds, n_rows,
+                       nb, probe_key, probe_key_dtype, h, join, *st, out_ids, out_cap, out_ids2, out_cap2,
+                       out_payload, off, max_len, n_prefix, cu, lb, ctr);
+  else
+    hipLaunchKernelGGL(k_select_lb<false>, dim3(static_cast<unsigned>(nb)), dim3(LB_THREADS), 0, s, preds, n_rows,
+                       nb, probe_key, probe_key_dtype, h, join, StagedHash{}, out_ids, out_cap, out_ids2, out_cap2,
+                       out_payload, off, max_len, n_prefix, cu, lb, ctr);
   return hipGetLastError();
 }
 

@@ -217,7 +217,10 @@ class DeviceQuery:
         self.sel_ids = torch.zeros(max(n, 1), dtype=torch.int32, device=dev)
         self.sel_labels = torch.zeros(max(n, 1), dtype=torch.int32, device=dev)
         self.sel_logits = torch.zeros(max(n, 1) * K, dtype=torch.float32, device=dev)
-        G = max(int(getattr(query, "n_group_keys", 0)), 1)
+        # dense keys: one group per key code; any int32 key (n_group_keys 0):
+        # at most one group per probe row
+        G = int(getattr(query, "n_group_keys", 0)) or n
+        G = max(G, 1)
         self.grp_key = torch.zeros(G, dtype=torch.int32, device=dev)
         self.grp_count = torch.zeros(G, dtype=torch.int64, device=dev)
         self.grp_sum = torch.zeros(G, dtype=torch.int64, device=dev)

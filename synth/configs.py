@@ -133,7 +133,7 @@ class Query:
     join: Optional[Join] = None
     n_prefix: int = 0                 # prefix tokens drawn by the generator (stream 99)
     group_col: Optional[str] = None   # probe column for avg_label_count_by
-    n_group_keys: int = 0             # dense key domain [0, n_group_keys)
+    n_group_keys: int = 0             # dense key domain [0, n_group_keys); 0: any int32 key (hash)
     gen_tokens: int = 0               # AI_TRANSFORM: tokens generated per selected row (0: AI_IF)
     eos_id: int = -1
     pad_id: int = 0

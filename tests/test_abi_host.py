@@ -106,9 +106,11 @@ def test_null_model_and_bad_query():
     # a join without a build table, and a build table without a join
     assert B.aiq_plan_create_status(model(), table(), None, query(join=1)) == B.AIQ_EINVAL
     assert B.aiq_plan_create_status(model(), table(), table(), query()) == B.AIQ_EINVAL
-    # group-by needs a key domain
+    # group-by: a dense key domain (n_group_keys > 0) or any int32 key (0); not negative
     assert B.aiq_plan_create_status(model(), table(), None, query(agg=B.AIQ_AGG_AVG_LABEL_COUNT_BY,
-                                                                  group_col=1)) == B.AIQ_EINVAL
+                                                                  group_col=1, n_group_keys=-1)) == B.AIQ_EINVAL
+    assert B.aiq_plan_create_status(model(), table(), None, query(agg=B.AIQ_AGG_AVG_LABEL_COUNT_BY,
+                                                                  group_col=1)) == B.AIQ_OK
     # count-by-payload needs a join
     assert B.aiq_plan_create_status(model(), table(), None, query(agg=B.AIQ_AGG_COUNT_BY_PAYLOAD,
                                                                   n_group_keys=4)) == B.AIQ_EINVAL

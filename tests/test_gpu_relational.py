@@ -199,3 +199,57 @@ def test_relational_only_join_with_prefix(rel_model):
               join=Join(probe_key="fk", build_key="key", payload="genre",
                         build_preds=(Pred("year", "gt", 1990),)), n_prefix=5)
     check_relational_only(run_relational_only(t, m, dm, q), t, q)
+
+
+# ---- GROUP BY over any int32 key (hash table, groups sorted by key) and the
+# join probed from the LDS-staged build table or, when more build rows pass
+# than LDS holds, from the global one
+
+def sparse_keys(n, seed):
+    """Hot keys (negative, zero, the int32 extremes) mixed with thousands of
+    distinct random keys, so a workgroup's private table fills and merges."""
+    r = np.random.default_rng(seed)
+    hot = np.array([np.iinfo(np.int32).min, -7, -1, 0, 3, 1 << 30, np.iinfo(np.int32).max], np.int64)
+    cold = r.integers(np.iinfo(np.int32).min, np.iinfo(np.int32).max, 6000, dtype=np.int64, endpoint=True)
+    pick = np.where(r.random(n) < 0.5, hot[r.integers(0, len(hot), n)], cold[r.integers(0, len(cold), n)])
+    return pick.astype(np.int32)
+
+
+@pytest.mark.parametrize("n", [1, 3000, 40000])
+def test_hash_group_by_any_int32_key(rel_model, n):
+    say(f"case: hash group by over sparse int32 keys, {n} rows")
+    m, dm = rel_model
+    pr = table(n, 20 + n)
+    pr["g"] = sparse_keys(n, n)
+    t = {"probe": pr, "build": None, "prefix": np.zeros(0, np.int32)}
+    q = Query(preds=(Pred("b", "lt", 40),), labels=(1, 2, 3, 4), decision="argmax", agg="avg_label_count_by",
+              group_col="g", n_group_keys=0)
+    r = full_check(t, m, dm, q)
+    assert len(r["groups"][0]) == len(np.unique(pr["g"][relational(t, q)[0]]))
+
+
+@pytest.mark.parametrize("col", ["a", "b"])
+def test_hash_group_by_narrow_columns(rel_model, col):
+    say(f"case: hash group by over the {col} column (negative int8 / int16 keys)")
+    m, dm = rel_model
+    t = {"probe": table(9000, 31), "build": None, "prefix": np.zeros(0, np.int32)}
+    q = Query(preds=(Pred("c", "lt", 700),), labels=(1, 2), decision="binary_gt", agg="avg_label_count_by",
+              group_col=col, n_group_keys=0)
+    full_check(t, m, dm, q)
+
+
+@pytest.mark.parametrize("n_movies,payload", [(700, "genre"), (700, "movie_id"), (5000, "movie_id")])
+def test_join_hash_groups_and_staging(rel_model, n_movies, payload):
+    say(f"case: join with {n_movies} movies, count by {payload} (hash groups)")
+    m, dm = rel_model
+    mv = movies(n_movies, 40)
+    pr = table(12000, 41)
+    r = np.random.default_rng(42)
+    pool = np.concatenate([mv["movie_id"], np.array([-5, np.iinfo(np.int32).min], np.int32)])
+    pr["movie_id"] = pool[r.integers(0, len(pool), 12000)]
+    t = {"probe": pr, "build": mv, "prefix": np.zeros(0, np.int32)}
+    # 5000 movies with every one passing: more than the LDS table holds
+    bpred = (Pred("year", "gt", 1900),) if n_movies > 1024 else (Pred("genre", "in", values=(2, 5, 11)),)
+    q = Query(preds=(Pred("a", "lt", 90),), labels=(1, 2), decision="binary_gt", agg="count_by_payload",
+              n_group_keys=0, join=Join("movie_id", "movie_id", payload, bpred))
+    full_check(t, m, dm, q)

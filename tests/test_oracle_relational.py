@@ -140,6 +140,19 @@ def test_group_avg_count_matches_dict():
     assert oracle.group_avg_count(np.zeros(0), np.zeros(0))[0].size == 0
 
 
+def test_group_avg_count_any_int32_key():
+    # negative keys, both int32 extremes and sparse keys order like plain integers
+    keys = np.array([2**31 - 1, -2**31, -7, 5, -7, 0, -2**31, 123456789, 5, -1], dtype=np.int32)
+    vals = np.array([3, 1, 2, 4, 5, 1, 2, 3, 3, 2])
+    k, c, s, a = oracle.group_avg_count(keys, vals)
+    assert k.tolist() == [-2**31, -7, -1, 0, 5, 123456789, 2**31 - 1]
+    assert c.tolist() == [2, 2, 1, 1, 2, 1, 1]
+    assert s.tolist() == [3, 7, 2, 1, 7, 3, 3]
+    assert a.tolist() == [1.5, 3.5, 2.0, 1.0, 3.5, 3.0, 3.0]
+    kk, cc = oracle.count_by(keys)
+    assert kk.tolist() == k.tolist() and cc.tolist() == c.tolist()
+
+
 def test_decision_strict_and_argmax_ties():
     qb = Query(preds=(), labels=(1, 2), decision="binary_gt", agg="count")
     lg = np.array([[1.0, 0.5], [0.5, 0.5], [0.1, 0.2]])
