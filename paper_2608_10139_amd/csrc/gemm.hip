@@ -1,13 +1,16 @@
 // Dense projections of the prefill: C[M, N] = A[M, K] . W[N, K]^T with fused
 // epilogues (rotary embedding on q/k, SwiGLU, GELU, residual add).
 //
-// bf16 path (gfx950 MFMA): 256 x 256 output tile per 512-thread workgroup,
-// K stepped by 64 through two LDS stages (2 x 64 KB) filled by 16-byte
-// direct-to-LDS loads, the next stage in flight while the current one feeds
-// the MFMAs.  Eight waves in a 2 x 4 grid each own a 128 x 64 sub-tile =
-// 4 x 2 blocks of v_mfma_f32_32x32x16_bf16 (the 32x32 form sustains about
-// twice the rate of the 16x16x32 form on gfx950).  The next tile's first
-// stage is fetched while the epilogue of the current one runs.
+// bf16 / fp16 path (gfx950 MFMA): 256 x 256 output tile per 256-thread
+// workgroup (one per CU), K stepped by 64 through two LDS stages (2 x 64 KB)
+// filled by 16-byte direct-to-LDS loads.  Four waves, one per SIMD, in a
+// 2 x 2 grid each own a 128 x 128 sub-tile = 4 x 4 blocks of
+// v_mfma_f32_32x32x16 (256 accumulator registers per lane).  The next
+// stage's loads are spread over the MFMAs of the first half of the current
+// one (a burst of them stalls the wave's MFMA issue), and each wave's loads
+// go to 4 KB-contiguous LDS runs so one M0 value serves four of them through
+// the instruction's immediate offset.  The next tile's first stage is
+// fetched while the epilogue of the current one runs.
 //
 // M (tokens in the chunk) is read from device memory; the grid is persistent
 // (one workgroup per CU) and walks the tiles, so an empty chunk costs one
@@ -55,13 +58,11 @@ __device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.0f + e
 // For hd = 128 the two 64-column halves of a head are reordered so that one
 // wave's 64 columns hold 32 complete rotary pairs (i, i + 64).
 __device__ __forceinline__ int qk_row(int c, int hd) {
-  const int head = c / hd, cc = c % hd;
-  int dim = cc;
-  if (hd == 128) {
-    const int hh = cc >> 6, jj = cc & 63;
-    dim = jj < 32 ? hh * 32 + jj : 64 + hh * 32 + (jj - 32);
-  }
-  return head * hd + dim;
+  if (hd != 128) return c;   // 64-dim heads: natural order
+  const int head = c >> 7, cc = c & 127;
+  const int hh = cc >> 6, jj = cc & 63;
+  const int dim = jj < 32 ? hh * 32 + jj : 64 + hh * 32 + (jj - 32);
+  return head * 128 + dim;
 }
 
 template <int EPI, typename T>
@@ -106,281 +107,266 @@ template <> struct Op16<true> {
   static __device__ __forceinline__ uint16_t cvt(float f) { return f2h(f); }
   static __device__ __forceinline__ float widen(uint16_t u) { return h2f(u); }
 };
-constexpr int GM = 256, GN = 256, GK = 64, GT = 512;
+constexpr int GM = 256, GN = 256, GK = 64, GT = 256;
 
 typedef f32x16_t f32x16;
 
-// Accumulator layout (v_mfma_f32_32x32x16_bf16, activations as the first
-// operand): acc[i][j][4g + e] holds C[m][n] with
-//   m = m0 + wm*128 + i*32 + 8g + 4*(lane/32) + e,   n = n0 + wn*64 + j*32 + lane%32.
-// A lane owns one column of each 32-wide block, so the rotary pair (j = 0
-// lower half, j = 1 upper half of a head) and the SwiGLU pair (j = 0 gate,
-// j = 1 up) sit in the same lane.
+// Accumulator layout.  The MFMAs compute the transposed tile, weights as the
+// first operand (v_mfma_f32_32x32x16: D[r][c] with r = 8g + 4*(lane/32) + e
+// in register 4g + e, c = lane % 32): acc[i][j][4g + e] holds C[m][n] with
+//   m = m0 + wm*128 + i*32 + lane%32,   n = n0 + wn*128 + j*32 + 8g + 4*(lane/32) + e,
+// four consecutive columns of one row per (j, g).
+//
+// Epilogue: for each 32-row block i the wave writes its 32 x 128 fp32
+// accumulators to its own 16 KB slice of the idle LDS stage, 16 bytes per
+// (j, g) straight from the accumulator registers, then reads them back as
+// pieces of 8 consecutive columns of one row, 16 consecutive lanes covering
+// one row, so every global access of the epilogue is a contiguous run of
+// 256 or 512 bytes per row.  The SwiGLU pair (columns c and c + 32 of a
+// 64-column half: gate and up) and the rotary pair (lower and upper half of
+// a head's dims, as the q/k weight rows are reordered) are pieces 4 apart.
 //
 // q, k and v (attention operands) are stored in fp16: 10 mantissa bits where
 // bf16 has 7, at the same MFMA rate; their magnitudes are O(1) after RMSNorm.
-//
-// Output goes through LDS: each wave owns an 8 KB slice of the idle LDS stage,
-// writes a slab of its sub-tile there in row-major order, then stores whole
-// 16-byte pieces of rows to global memory (8 store instructions per slab
-// instead of one 2-byte store per value).
 
 __device__ __forceinline__ float silu_fast(float g) {
   return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g));
 }
 
-// Writes a slab of `rows` x `cols` elements of type T from the wave's LDS slice
-// (row-major, `cols` per row) to C[m][col_of(c)] for rows m < M, 16 B per lane.
-template <typename T, typename ColMap>
-__device__ __forceinline__ void flush_slab(const T* slab, int rows, int cols, T* C, int64_t ldc, int64_t m_first,
-                                           int64_t M, int lane, ColMap col_of) {
-  constexpr int PER = 16 / sizeof(T);               // elements per 16-byte piece
-  const int pieces_per_row = cols / PER;
-  const int total = rows * pieces_per_row;
-  for (int p = lane; p < total; p += 64) {
-    const int r = p / pieces_per_row, c = (p % pieces_per_row) * PER;
-    const int64_t m = m_first + r;
-    if (m < M)
-      *reinterpret_cast<uint4*>(C + m * ldc + col_of(c)) = *reinterpret_cast<const uint4*>(slab + r * cols + c);
-  }
+template <bool H>
+__device__ __forceinline__ uint4 pack8(const float (&v)[8]) {
+  uint4 p;
+  p.x = Op16<H>::cvt(v[0]) | (static_cast<uint32_t>(Op16<H>::cvt(v[1])) << 16);
+  p.y = Op16<H>::cvt(v[2]) | (static_cast<uint32_t>(Op16<H>::cvt(v[3])) << 16);
+  p.z = Op16<H>::cvt(v[4]) | (static_cast<uint32_t>(Op16<H>::cvt(v[5])) << 16);
+  p.w = Op16<H>::cvt(v[6]) | (static_cast<uint32_t>(Op16<H>::cvt(v[7])) << 16);
+  return p;
+}
+__device__ __forceinline__ uint4 pack8h(const float (&v)[8]) {
+  uint4 p;
+  p.x = f2h(v[0]) | (static_cast<uint32_t>(f2h(v[1])) << 16);
+  p.y = f2h(v[2]) | (static_cast<uint32_t>(f2h(v[3])) << 16);
+  p.z = f2h(v[4]) | (static_cast<uint32_t>(f2h(v[5])) << 16);
+  p.w = f2h(v[6]) | (static_cast<uint32_t>(f2h(v[7])) << 16);
+  return p;
+}
+
+// The wave's epilogue slice: 32 rows x 128 fp32, 512-byte rows of 32
+// 16-byte chunks; chunk c of row r sits at slot c ^ (r & 15), so 16
+// consecutive rows writing one chunk, and one row read by 16 lanes, each
+// cover all 64 banks.
+__device__ __forceinline__ int eslot(int r, int c) { return r * 32 + (c ^ (r & 15)); }
+
+// Makes this wave's LDS writes visible to its own later reads in other
+// lanes (LDS completes one wave's operations in order; this keeps the
+// compiler from moving them across).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
 // `rl` holds the tile's row scales (QKV, SwiGLU) or the following norm's gain
-// for the tile's columns (residual), `pl` the tile's positions, both in LDS;
-// `rev` the rotary frequencies of this lane's dims (revolutions per position)
-// for the first and second 64-dim half of a head.  `prefetch` issues the next
-// tile's first loads: the residual epilogue calls it after its first loads of
-// x, so that those do not queue behind it; the others call it first.
+// for the tile's columns (residual), `pl` the tile's positions and `rv` the
+// rotary frequencies of a head's lower-half dims (revolutions per position),
+// all in LDS; `slice` is the wave's 16 KB of idle LDS.  `prefetch` issues the
+// next tile's first loads (after the residual epilogue's first loads of x,
+// so that those do not queue behind it; first for the others).
 template <int EPI, bool H, typename Prefetch>
-__device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4][2], int64_t m0, int n0,
-                                              int64_t M, int wm, int wn, int lane, uint16_t* slice,
-                                              const float* rl, const int32_t* pl, float2 rev, Prefetch prefetch) {
+__device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4][4], int64_t m0, int n0,
+                                              int64_t M, int wm, int wn, int lane, float4* slice, const float* rl,
+                                              const int32_t* pl, const float* rv, Prefetch prefetch) {
   const int l32 = lane & 31, hi = lane >> 5;
-  const int nw = n0 + wn * 64;   // first GEMM column of this wave
-  const int64_t mw = m0 + wm * 128;   // first row of this wave's sub-tile
-  if (EPI == EPI_RESID || EPI == EPI_RESID_EMB) {
-    // x += acc in place; with a following norm also h = x * g and, per row,
-    // the sum of x^2 over this wave's 64 columns.  A slab of 32 rows x 64
-    // columns goes through LDS; each lane then owns 4 columns of 8 rows, and
-    // the 16 lanes of a row add their squares in a fixed butterfly order.  A
-    // row's x for the next slab is read as soon as its slot is free, so those
-    // reads are in flight while the rest of the slab is processed.
-    float* slab = reinterpret_cast<float*>(slice);
-    const int cg = (lane & 15) * 4;
-    const bool norm = a.gnext != nullptr;
-    uint16_t* hout = static_cast<uint16_t*>(a.hout);
-    const int part = nw >> 6;
-    auto row_of = [&](int i, int k) { return mw + i * 32 + (lane >> 4) + 4 * k; };
-    // the residual before this projection: x, or (first layer) the token's
-    // embedding row widened from 16 bits, which is exactly what x would hold
-    const int64_t tok0 = EPI == EPI_RESID_EMB ? a.x_tok_desc[D_TOK_BEGIN] : 0;
-    auto load_x = [&](int i, float4 (&v)[8]) {
+  const int nw = n0 + wn * 128;   // first GEMM column of the wave's sub-tile
+  const int pc = lane & 15;       // piece (8 columns) of a row this lane reads back
+  const int pr = lane >> 4;       // its row inside each group of 4 rows
+  constexpr bool RESID = EPI == EPI_RESID || EPI == EPI_RESID_EMB;
+  if (!RESID) prefetch();
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        int64_t m = row_of(i, k);
-        if (m > M - 1) m = M - 1;   // in bounds; the value is not used
-        if (EPI == EPI_RESID_EMB) {
-          int32_t tok = a.x_tok[tok0 + m];
-          if (tok < 0 || tok >= a.vocab) tok = 0;
-          const uint2 e = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(a.x_emb) +
-                                                          static_cast<int64_t>(tok) * a.ldc + nw + cg);
-          v[k] = make_float4(Op16<H>::widen(static_cast<uint16_t>(e.x & 0xFFFFu)),
-                             Op16<H>::widen(static_cast<uint16_t>(e.x >> 16)),
-                             Op16<H>::widen(static_cast<uint16_t>(e.y & 0xFFFFu)),
-                             Op16<H>::widen(static_cast<uint16_t>(e.y >> 16)));
-        } else {
-          v[k] = *reinterpret_cast<const float4*>(a.x + m * a.ldc + nw + cg);
-        }
-      }
-    };
-    float4 xo[8];
-    load_x(0, xo);
-    prefetch();
-    float4 gv = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (norm) gv = *reinterpret_cast<const float4*>(rl + (nw - n0) + cg);
+  for (int i = 0; i < 4; ++i) {
+    // fp32 accumulators of rows 32i .. 32i + 31 to LDS
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int g = 0; g < 4; ++g)
+        slice[eslot(l32, 8 * j + 2 * g + hi)] =
+            make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+    wave_lds_sync();
+    const int row0 = wm * 128 + i * 32;   // tile row of slice row 0
+    if (RESID) {
+      // x += acc in place; with a following norm also h = x * g and, per row,
+      // the sum of x^2 over each 64-column half (pieces 8h .. 8h + 7, eight
+      // neighbouring lanes, added in a fixed butterfly order).  All eight
+      // rows' residuals of this lane are read before any is used.
+      const bool norm = a.gnext != nullptr;
+      uint16_t* hout = static_cast<uint16_t*>(a.hout);
+      const int64_t tok0 = EPI == EPI_RESID_EMB ? a.x_tok_desc[D_TOK_BEGIN] : 0;
+      const int col = nw + 8 * pc;
+      float4 xv[8][2];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = g * 8 + hi * 4 + e;
-          slab[r * 64 + l32] = acc[i][0][4 * g + e];
-          slab[r * 64 + 32 + l32] = acc[i][1][4 * g + e];
+      for (int rr = 0; rr < 8; ++rr) {
+        int64_t m = m0 + row0 + 4 * rr + pr;
+        if (m > M - 1) m = M - 1;   // in bounds; the value is not used
+        if (EPI == EPI_RESID_EMB) {
+          // the residual before this projection is the token's embedding row
+          // widened from 16 bits, which is exactly what x would hold
+          int32_t tok = a.x_tok[tok0 + m];
+          if (tok < 0 || tok >= a.vocab) tok = 0;
+          const uint4 e = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(a.x_emb) +
+                                                          static_cast<int64_t>(tok) * a.ldc + col);
+          xv[rr][0] = make_float4(Op16<H>::widen(static_cast<uint16_t>(e.x & 0xFFFFu)),
+                                  Op16<H>::widen(static_cast<uint16_t>(e.x >> 16)),
+                                  Op16<H>::widen(static_cast<uint16_t>(e.y & 0xFFFFu)),
+                                  Op16<H>::widen(static_cast<uint16_t>(e.y >> 16)));
+          xv[rr][1] = make_float4(Op16<H>::widen(static_cast<uint16_t>(e.z & 0xFFFFu)),
+                                  Op16<H>::widen(static_cast<uint16_t>(e.z >> 16)),
+                                  Op16<H>::widen(static_cast<uint16_t>(e.w & 0xFFFFu)),
+                                  Op16<H>::widen(static_cast<uint16_t>(e.w >> 16)));
+        } else {
+          const float* xr = a.x + m * a.ldc + col;
+          xv[rr][0] = *reinterpret_cast<const float4*>(xr);
+          xv[rr][1] = *reinterpret_cast<const float4*>(xr + 4);
         }
+      }
+      if (i == 0) prefetch();
+      float4 g0 = make_float4(0.f, 0.f, 0.f, 0.f), g1 = g0;
+      if (norm) {
+        g0 = *reinterpret_cast<const float4*>(rl + (col - n0));
+        g1 = *reinterpret_cast<const float4*>(rl + (col - n0) + 4);
+      }
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int r = (lane >> 4) + 4 * k;
-        const int64_t m = row_of(i, k);
+      for (int rr = 0; rr < 8; ++rr) {
+        const int r = 4 * rr + pr;
+        const int64_t m = m0 + row0 + r;
+        const float4 s0 = slice[eslot(r, 2 * pc)], s1 = slice[eslot(r, 2 * pc + 1)];
+        float4 x0 = xv[rr][0], x1 = xv[rr][1];
+        x0.x += s0.x; x0.y += s0.y; x0.z += s0.z; x0.w += s0.w;
+        x1.x += s1.x; x1.y += s1.y; x1.z += s1.z; x1.w += s1.w;
         float ssq = 0.f;
         if (m < M) {
-          const float4 sv = *reinterpret_cast<const float4*>(slab + r * 64 + cg);
-          float4 xn = xo[k];
-          xn.x += sv.x;
-          xn.y += sv.y;
-          xn.z += sv.z;
-          xn.w += sv.w;
-          *reinterpret_cast<float4*>(a.x + m * a.ldc + nw + cg) = xn;
+          float* xr = a.x + m * a.ldc + col;
+          *reinterpret_cast<float4*>(xr) = x0;
+          *reinterpret_cast<float4*>(xr + 4) = x1;
           if (norm) {
-            uint2 hv;
-            hv.x = Op16<H>::cvt(xn.x * gv.x) | (static_cast<uint32_t>(Op16<H>::cvt(xn.y * gv.y)) << 16);
-            hv.y = Op16<H>::cvt(xn.z * gv.z) | (static_cast<uint32_t>(Op16<H>::cvt(xn.w * gv.w)) << 16);
-            *reinterpret_cast<uint2*>(hout + m * a.ldc + nw + cg) = hv;
-            ssq = (xn.x * xn.x + xn.y * xn.y) + (xn.z * xn.z + xn.w * xn.w);
+            const float hv[8] = {x0.x * g0.x, x0.y * g0.y, x0.z * g0.z, x0.w * g0.w,
+                                 x1.x * g1.x, x1.y * g1.y, x1.z * g1.z, x1.w * g1.w};
+            *reinterpret_cast<uint4*>(hout + m * a.ldc + col) = pack8<H>(hv);
           }
+          ssq = ((x0.x * x0.x + x0.y * x0.y) + (x0.z * x0.z + x0.w * x0.w)) +
+                ((x1.x * x1.x + x1.y * x1.y) + (x1.z * x1.z + x1.w * x1.w));
         }
         if (norm) {
           ssq += __shfl_xor(ssq, 1);
           ssq += __shfl_xor(ssq, 2);
           ssq += __shfl_xor(ssq, 4);
-          ssq += __shfl_xor(ssq, 8);
-          if ((lane & 15) == 0 && m < M) a.ssp[m * a.n_part + part] = ssq;
+          if ((pc & 7) == 0 && m < M) a.ssp[m * a.n_part + ((nw >> 6) + (pc >> 3))] = ssq;
         }
-        if (i < 3) {   // the same row slot of the next slab
-          int64_t mn = row_of(i + 1, k);
-          if (mn > M - 1) mn = M - 1;
-          if (EPI == EPI_RESID_EMB) {
-            int32_t tok = a.x_tok[tok0 + mn];
-            if (tok < 0 || tok >= a.vocab) tok = 0;
-            const uint2 e = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(a.x_emb) +
-                                                            static_cast<int64_t>(tok) * a.ldc + nw + cg);
-            xo[k] = make_float4(Op16<H>::widen(static_cast<uint16_t>(e.x & 0xFFFFu)),
-                                Op16<H>::widen(static_cast<uint16_t>(e.x >> 16)),
-                                Op16<H>::widen(static_cast<uint16_t>(e.y & 0xFFFFu)),
-                                Op16<H>::widen(static_cast<uint16_t>(e.y >> 16)));
-          } else {
-            xo[k] = *reinterpret_cast<const float4*>(a.x + mn * a.ldc + nw + cg);
+      }
+    } else if (EPI == EPI_ARGMAX) {
+      // row maxima over each 64-column half: the lane's 8 columns in
+      // increasing order (a strictly greater value replaces), then the eight
+      // lanes of the half in a butterfly that keeps the lower column on ties
+      int2* P = static_cast<int2*>(a.C);
+#pragma unroll
+      for (int rr = 0; rr < 8; ++rr) {
+        const int r = 4 * rr + pr;
+        const int64_t m = m0 + row0 + r;
+        const float4 s0 = slice[eslot(r, 2 * pc)], s1 = slice[eslot(r, 2 * pc + 1)];
+        const float v8[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+        float v = v8[0];
+        int c = nw + 8 * pc;
+#pragma unroll
+        for (int e = 1; e < 8; ++e)
+          if (v8[e] > v) {
+            v = v8[e];
+            c = nw + 8 * pc + e;
           }
+#pragma unroll
+        for (int o = 1; o < 8; o <<= 1) {
+          const float ov = __shfl_xor(v, o);
+          const int oc = __shfl_xor(c, o);
+          if (ov > v || (ov == v && oc < c)) {
+            v = ov;
+            c = oc;
+          }
+        }
+        if ((pc & 7) == 0 && m < M) P[m * a.ldc + ((nw >> 6) + (pc >> 3))] = make_int2(__float_as_int(v), c);
+      }
+    } else if (EPI == EPI_STORE_F32) {
+      float* C = static_cast<float*>(a.C);
+#pragma unroll
+      for (int rr = 0; rr < 8; ++rr) {
+        const int r = 4 * rr + pr;
+        const int64_t m = m0 + row0 + r;
+        if (m < M) {
+          float* cr = C + m * a.ldc + nw + 8 * pc;
+          *reinterpret_cast<float4*>(cr) = slice[eslot(r, 2 * pc)];
+          *reinterpret_cast<float4*>(cr + 4) = slice[eslot(r, 2 * pc + 1)];
+        }
+      }
+    } else if (EPI == EPI_STORE_ACT) {
+      uint16_t* C = static_cast<uint16_t*>(a.C);
+#pragma unroll
+      for (int rr = 0; rr < 8; ++rr) {
+        const int r = 4 * rr + pr;
+        const int64_t m = m0 + row0 + r;
+        const float4 s0 = slice[eslot(r, 2 * pc)], s1 = slice[eslot(r, 2 * pc + 1)];
+        const float v8[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+        if (m < M) *reinterpret_cast<uint4*>(C + m * a.ldc + nw + 8 * pc) = pack8<H>(v8);
+      }
+    } else {
+      // SwiGLU and rotary pairs: pieces q (0..3) and q + 4 of one 64-column
+      // half h; lane piece pc -> (h, q) = (pc / 8, pc % 4) on rows of parity
+      // pc / 4 % 2: 32 rows x 2 halves x 4 pairs = 256 pair-pieces, 4 per lane
+      uint16_t* C = static_cast<uint16_t*>(a.C);
+      const int h = pc >> 3, q = pc & 3, rp = (pc >> 2) & 1;
+      const int nh = nw + 64 * h;
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int r = 8 * rr + 2 * pr + rp;
+        const int tr = row0 + r;
+        const int64_t m = m0 + tr;
+        const float rs = a.rs ? rl[tr] : 1.f;   // RMSNorm row scale
+        const float4 l0 = slice[eslot(r, 16 * h + 2 * q)], l1 = slice[eslot(r, 16 * h + 2 * q + 1)];
+        const float4 u0 = slice[eslot(r, 16 * h + 2 * q + 8)], u1 = slice[eslot(r, 16 * h + 2 * q + 9)];
+        const float lo[8] = {l0.x * rs, l0.y * rs, l0.z * rs, l0.w * rs, l1.x * rs, l1.y * rs, l1.z * rs, l1.w * rs};
+        const float up[8] = {u0.x * rs, u0.y * rs, u0.z * rs, u0.w * rs, u1.x * rs, u1.y * rs, u1.z * rs, u1.w * rs};
+        if (m >= M) continue;
+        uint16_t* crow = C + m * a.ldc;
+        if (EPI == EPI_SWIGLU) {
+          float o[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = silu_fast(lo[e]) * up[e];
+          *reinterpret_cast<uint4*>(crow + (nh >> 1) + 8 * q) = pack8<H>(o);
+        } else if (nh >= a.n_q + a.n_kv) {   // v: natural order
+          *reinterpret_cast<uint4*>(crow + nh + 8 * q) = pack8h(lo);
+          *reinterpret_cast<uint4*>(crow + nh + 32 + 8 * q) = pack8h(up);
+        } else {
+          const int sbase = nh < a.n_q ? 0 : a.n_q;
+          const int cc = nh - sbase;
+          const int head = cc / a.hd, hh = (cc % a.hd) >> 6, half = a.hd >> 1;
+          const float pos = static_cast<float>(pl[tr]);
+          const float4 f0 = *reinterpret_cast<const float4*>(rv + hh * 32 + 8 * q);
+          const float4 f1 = *reinterpret_cast<const float4*>(rv + hh * 32 + 8 * q + 4);
+          const float fr[8] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w};
+          float ol[8], ou[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            // angle pos * theta^(-2i/hd), in revolutions (hardware sin/cos take revolutions)
+            const float rev = pos * fr[e];
+            const float frac = rev - floorf(rev);
+            const float cs = __builtin_amdgcn_cosf(frac), sn = __builtin_amdgcn_sinf(frac);
+            ol[e] = lo[e] * cs - up[e] * sn;   // lower half dim
+            ou[e] = up[e] * cs + lo[e] * sn;   // upper half dim
+          }
+          uint16_t* dst = crow + sbase + head * a.hd + hh * 32 + 8 * q;
+          *reinterpret_cast<uint4*>(dst) = pack8h(ol);
+          *reinterpret_cast<uint4*>(dst + half) = pack8h(ou);
         }
       }
     }
-    return;
+    wave_lds_sync();   // the slice's reads are done before the next block's writes
   }
-  prefetch();
-  if (EPI == EPI_ARGMAX) {
-    // row maxima over this wave's 64 columns: a row's values sit in the 32
-    // lanes of one half-wave (column lane % 32, two 32-column blocks j); the
-    // lanes meet in a butterfly that keeps the lower column on ties
-    int2* P = static_cast<int2*>(a.C);
-    const int chunk = nw >> 6;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int g = 0; g < 4; ++g)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          float v = acc[i][0][4 * g + e];
-          int c = nw + l32;
-          const float v1 = acc[i][1][4 * g + e];
-          if (v1 > v) {   // column + 32 only if strictly greater
-            v = v1;
-            c += 32;
-          }
-#pragma unroll
-          for (int o = 1; o < 32; o <<= 1) {
-            const float ov = __shfl_xor(v, o);
-            const int oc = __shfl_xor(c, o);
-            if (ov > v || (ov == v && oc < c)) {
-              v = ov;
-              c = oc;
-            }
-          }
-          const int64_t m = mw + i * 32 + 8 * g + 4 * hi + e;
-          if (l32 == 0 && m < M) P[m * a.ldc + chunk] = make_int2(__float_as_int(v), c);
-        }
-    return;
-  }
-  if (EPI == EPI_STORE_F32) {
-    // fp32: four slabs of 32 rows x 64 columns (8 KB each)
-    float* slab = reinterpret_cast<float*>(slice);
-    float* C = static_cast<float*>(a.C);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-#pragma unroll
-      for (int g = 0; g < 4; ++g)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = g * 8 + hi * 4 + e;
-          slab[r * 64 + l32] = acc[i][0][4 * g + e];
-          slab[r * 64 + 32 + l32] = acc[i][1][4 * g + e];
-        }
-      flush_slab<float>(slab, 32, 64, C, a.ldc, mw + i * 32, M, lane, [&](int c) { return nw + c; });
-    }
-    return;
-  }
-  // bf16 outputs: slab of 64 rows (two i-blocks) x 64 (or 32 for SwiGLU) columns
-  uint16_t* C = static_cast<uint16_t*>(a.C);
-  const bool is_v = EPI == EPI_QKV_ROPE && nw >= a.n_q + a.n_kv;
-  int sbase = 0, head = 0, hh = 0, half = 0;
-  float rev_per_pos = 0.f;
-  if (EPI == EPI_QKV_ROPE && !is_v) {
-    sbase = nw < a.n_q ? 0 : a.n_q;
-    const int c = nw - sbase;
-    head = c / a.hd;
-    hh = (c % a.hd) >> 6;   // 0 except the second half-wave of a 128-dim head
-    half = a.hd >> 1;
-    // rotary frequency of this lane's lower-half dim, in revolutions per position
-    rev_per_pos = hh ? rev.y : rev.x;
-  }
-  // q / k columns (rotary) or v columns: chosen once per wave (a per-element
-  // choice costs exec-mask branches around every element)
-  auto emit = [&](auto rot_tag) {
-    constexpr bool ROT = decltype(rot_tag)::value;
-#pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2) {
-#pragma unroll
-      for (int ii = 0; ii < 2; ++ii) {
-        const int i = h2 * 2 + ii;
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int tr = wm * 128 + i * 32 + g * 8 + hi * 4;   // tile row of e = 0
-          int4 p4 = make_int4(0, 0, 0, 0);
-          if (EPI == EPI_QKV_ROPE && ROT)   // positions of the 4 rows e = 0..3
-            p4 = *reinterpret_cast<const int4*>(pl + tr);
-          const int pe[4] = {p4.x, p4.y, p4.z, p4.w};
-          float4 r4 = make_float4(1.f, 1.f, 1.f, 1.f);
-          if (a.rs) r4 = *reinterpret_cast<const float4*>(rl + tr);   // RMSNorm row scales
-          const float re[4] = {r4.x, r4.y, r4.z, r4.w};
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int r = ii * 32 + g * 8 + hi * 4 + e;   // row inside the 64-row slab
-            const float v0 = acc[i][0][4 * g + e] * re[e], v1 = acc[i][1][4 * g + e] * re[e];
-            if (EPI == EPI_SWIGLU) {
-              slice[r * 32 + l32] = Op16<H>::cvt(silu_fast(v0) * v1);
-            } else if (EPI == EPI_QKV_ROPE && ROT) {
-              // angle pos * theta^(-2i/hd), in revolutions (hardware sin/cos take revolutions)
-              const float rev = static_cast<float>(pe[e]) * rev_per_pos;
-              const float frac = rev - floorf(rev);
-              const float cs = __builtin_amdgcn_cosf(frac), sn = __builtin_amdgcn_sinf(frac);
-              slice[r * 64 + l32] = f2h(v0 * cs - v1 * sn);        // lower half dims
-              slice[r * 64 + 32 + l32] = f2h(v1 * cs + v0 * sn);   // upper half dims
-            } else if (EPI == EPI_QKV_ROPE && !ROT) {   // v
-              slice[r * 64 + l32] = f2h(v0);
-              slice[r * 64 + 32 + l32] = f2h(v1);
-            } else {
-              slice[r * 64 + l32] = Op16<H>::cvt(v0);
-              slice[r * 64 + 32 + l32] = Op16<H>::cvt(v1);
-            }
-          }
-        }
-      }
-      const int64_t m_first = mw + h2 * 64;
-      if (EPI == EPI_SWIGLU) {
-        flush_slab<uint16_t>(slice, 64, 32, C, a.ldc, m_first, M, lane, [&](int c) { return nw / 2 + c; });
-      } else if (EPI == EPI_QKV_ROPE && ROT) {
-        // slab columns 0..31: lower-half dims hh*32.., 32..63: the matching upper-half dims
-        const int base = sbase + head * a.hd + hh * 32;
-        flush_slab<uint16_t>(slice, 64, 64, C, a.ldc, m_first, M, lane,
-                             [&](int c) { return base + (c < 32 ? c : half + c - 32); });
-      } else {
-        flush_slab<uint16_t>(slice, 64, 64, C, a.ldc, m_first, M, lane, [&](int c) { return nw + c; });
-      }
-    }
-  };
-  if (EPI == EPI_QKV_ROPE && !is_v)
-    emit(std::true_type{});
-  else
-    emit(std::false_type{});
 }
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
@@ -390,76 +376,117 @@ typedef __attribute__((address_space(3))) void* lds_ptr_t;
 // cover all 64 banks once (row parity already picks the bank half).
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
-// One 64-deep k-step of the wave's 128 x 64 sub-tile from one LDS stage.
-// Fragments of the next 16-deep sub-step are read while the MFMAs of the
-// current one run (two register sets), so LDS latency hides behind MFMA work.
+// Fragments of one 16-deep sub-step s of the wave's 128 x 128 sub-tile.
 template <bool H>
 __device__ __forceinline__ void load_frags(const uint16_t* As, const uint16_t* Bs, int s, int wm, int wn, int lane,
-                                           typename Op16<H>::V (&af)[4], typename Op16<H>::V (&bw)[2]) {
+                                           typename Op16<H>::V (&af)[4], typename Op16<H>::V (&bw)[4]) {
   typedef typename Op16<H>::V V;
   const int r32 = lane & 31;
   const int sw = swz(r32, 2 * s + (lane >> 5)) << 3;   // same for every 32-row block
 #pragma unroll
   for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const V*>(As + (wm * 128 + i * 32 + r32) * GK + sw);
 #pragma unroll
-  for (int j = 0; j < 2; ++j) bw[j] = *reinterpret_cast<const V*>(Bs + (wn * 64 + j * 32 + r32) * GK + sw);
+  for (int j = 0; j < 4; ++j) bw[j] = *reinterpret_cast<const V*>(Bs + (wn * 128 + j * 32 + r32) * GK + sw);
 }
 
+// 16-byte direct-to-LDS load whose immediate offset, (i % 4) KB, is added to
+// both the global and the LDS address (the global pointer carries -(i % 4) KB).
+__device__ __forceinline__ void load_lds_imm(const void* g, lds_ptr_t l, int i) {
+  switch (i & 3) {
+    case 0: __builtin_amdgcn_global_load_lds(g, l, 16, 0, 0); break;
+    case 1: __builtin_amdgcn_global_load_lds(g, l, 16, 1024, 0); break;
+    case 2: __builtin_amdgcn_global_load_lds(g, l, 16, 2048, 0); break;
+    default: __builtin_amdgcn_global_load_lds(g, l, 16, 3072, 0); break;
+  }
+}
+
+// Global -> LDS copy of one stage: wave w fills rows 64w .. 64w + 63 of A and
+// of W (eight 1 KB pieces of 8 rows each); in a piece's instruction lane l
+// fetches the global chunk that belongs at row 8c + l/8, slot l%8.  The
+// source pointers advance by one k-step.
+__device__ __forceinline__ void dma_stage(uint16_t* sA, uint16_t* sB, const uint16_t* (&ga)[8],
+                                          const uint16_t* (&gb)[8], int w) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int c = 8 * w + (i & 4);
+    load_lds_imm(static_cast<const void*>(ga[i]), (lds_ptr_t)(sA + c * 512), i);
+    load_lds_imm(static_cast<const void*>(gb[i]), (lds_ptr_t)(sB + c * 512), i);
+    ga[i] += GK;
+    gb[i] += GK;
+  }
+}
+
+// One 64-deep k-step of the wave's sub-tile from one LDS stage (4 sub-steps of
+// 16 MFMAs).  Fragments of the next sub-step are read while the MFMAs of the
+// current one run; with `dma`, the next stage's 16 loads go out during the
+// first two sub-steps, one per MFMA pair.
 template <bool H>
-__device__ __forceinline__ void mma_stage(const uint16_t* As, const uint16_t* Bs, f32x16 (&acc)[4][2], int wm,
-                                          int wn, int lane) {
-  typename Op16<H>::V af[2][4], bw[2][2];
+__device__ __forceinline__ void mma_stage(const uint16_t* As, const uint16_t* Bs, f32x16 (&acc)[4][4], int wm,
+                                          int wn, int lane, uint16_t* nA, uint16_t* nB, const uint16_t* (&ga)[8],
+                                          const uint16_t* (&gb)[8], int w, bool dma) {
+  typename Op16<H>::V af[2][4], bw[2][4];
   load_frags<H>(As, Bs, 0, wm, wn, lane, af[0], bw[0]);
+  __builtin_amdgcn_sched_barrier(0);   // the first sub-step's reads are not interleaved with its own MFMAs
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
     const int cur = s & 1;
     if (s < 3) load_frags<H>(As, Bs, s + 1, wm, wn, lane, af[cur ^ 1], bw[cur ^ 1]);
+    if (s < 2 && dma) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int i = u, c = 8 * w + (i & 4);
+        if (s == 0) {
+          load_lds_imm(static_cast<const void*>(ga[i]), (lds_ptr_t)(nA + c * 512), i);
+          ga[i] += GK;
+        } else {
+          load_lds_imm(static_cast<const void*>(gb[i]), (lds_ptr_t)(nB + c * 512), i);
+          gb[i] += GK;
+        }
+      }
+    }
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-        acc[i][j] = Op16<H>::mma(af[cur][i], bw[cur][j], acc[i][j]);
-    if (s < 3) {
-      // interleave: one MFMA, one LDS read, ... then the remaining MFMAs
-      for (int q = 0; q < 6; ++q) {
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = Op16<H>::mma(bw[cur][j], af[cur][i], acc[i][j]);
+    if (s < 2) {
+      // 16 MFMAs, 8 fragment reads, 8 loads
+      for (int q = 0; q < 8; ++q) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read
       }
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    } else if (s < 3) {
+      for (int q = 0; q < 8; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
     }
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
-// Global -> LDS tile copy with the 16-byte direct-to-LDS load: a wave's
-// instruction fills 1 KB (8 rows) at consecutive lane slots, so lane l
-// fetches the global chunk that belongs at row 8c + l/8, slot l%8.
-__device__ __forceinline__ void dma_stage(uint16_t* sA, uint16_t* sB, const uint16_t* const (&ga)[4],
-                                          const uint16_t* const (&gb)[4], int k0, int w) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c = i * 8 + w;
-    __builtin_amdgcn_global_load_lds(static_cast<const void*>(ga[i] + k0), (lds_ptr_t)(sA + c * 512), 16, 0, 0);
-    __builtin_amdgcn_global_load_lds(static_cast<const void*>(gb[i] + k0), (lds_ptr_t)(sB + c * 512), 16, 0, 0);
-  }
-}
-
+// Source pointers of a tile's first k-step (see dma_stage), each carrying
+// -(i % 4) KB for the loads' immediate offset.
 template <int EPI>
 __device__ __forceinline__ void tile_sources(const GemmArgs& a, const uint16_t* A, int64_t M, int64_t m0, int n0,
-                                             int w, int lane, const uint16_t* (&ga)[4], const uint16_t* (&gb)[4]) {
+                                             int w, int lane, const uint16_t* (&ga)[8], const uint16_t* (&gb)[8]) {
   const int lr = lane >> 3;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = (i * 8 + w) * 8 + lr;
+  for (int i = 0; i < 8; ++i) {
+    const int row = (8 * w + i) * 8 + lr;
     const int lc = swz(row, lane & 7);   // logical chunk stored in this lane's slot
     int64_t mr = m0 + row;
     if (mr > M - 1) mr = M - 1;
-    ga[i] = A + mr * a.lda + lc * 8;
-    gb[i] = b_row<EPI, uint16_t>(a, n0 + row) + lc * 8;
+    ga[i] = A + mr * a.lda + lc * 8 - (i & 3) * 512;
+    gb[i] = b_row<EPI, uint16_t>(a, n0 + row) + lc * 8 - (i & 3) * 512;
   }
 }
 
 template <int EPI, bool H>
-__global__ __launch_bounds__(GT) void k_gemm_bf16(GemmArgs a) {
+__global__ __launch_bounds__(GT, 1) void k_gemm_bf16(GemmArgs a) {
   // two stages in distinct arrays: the compiler can then tell the in-flight
   // loads into one stage from the reads of the other and only waits at the
   // barrier that ends the stage
@@ -469,11 +496,12 @@ __global__ __launch_bounds__(GT) void k_gemm_bf16(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t sB1[GN * GK];
   __shared__ __attribute__((aligned(16))) float rbuf[GM];     // the tile's RMSNorm row scales
   __shared__ __attribute__((aligned(16))) int32_t pbuf[GM];   // the tile's token positions (QKV)
+  __shared__ __attribute__((aligned(16))) float rvbuf[64];    // rotary frequencies of the lower-half dims (QKV)
   const int64_t M = *a.m_ptr;
   if (M <= 0) return;
   const int tiles_n = a.N / GN;
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6, wm = w >> 2, wn = w & 3;
-  const int nk = a.K / GK;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6, wm = w >> 1, wn = w & 1;
+  const int nk = a.K / GK;   // even (the launcher checks K % 128)
   const uint16_t* A = static_cast<const uint16_t*>(a.A);
 
   // XCD-aware order: workgroups are dispatched round-robin over the 8 XCDs,
@@ -483,47 +511,45 @@ __global__ __launch_bounds__(GT) void k_gemm_bf16(GemmArgs a) {
   // one XCD share a few activation row-panels and a few weight column-panels
   // in that XCD's L2 instead of streaming 32 distinct panels.
   constexpr int GROUP_M = 4;
-  const int64_t tiles_m = (M + GM - 1) / GM;
+  const int tiles_m = static_cast<int>((M + GM - 1) / GM);   // < 2^31 (M < 2^39)
   const int xcd = blockIdx.x & 7;
-  const int64_t per_xcd = gridDim.x >> 3;   // grid is a multiple of 8
-  const int64_t rows_x = tiles_m > xcd ? (tiles_m - xcd + 7) / 8 : 0;
-  const int64_t count_x = rows_x * tiles_n;
-  auto tile_mn = [&](int64_t q, int64_t& m0, int& n0) {
-    const int64_t per_group = static_cast<int64_t>(GROUP_M) * tiles_n;
-    const int64_t grp = q / per_group, within = q % per_group;
-    const int64_t rows_here = (rows_x - grp * GROUP_M) < GROUP_M ? (rows_x - grp * GROUP_M) : GROUP_M;
-    const int64_t lr = grp * GROUP_M + within % rows_here;
-    m0 = (lr * 8 + xcd) * GM;
-    n0 = static_cast<int>(within / rows_here) * GN;
+  const int per_xcd = gridDim.x >> 3;   // grid is a multiple of 8
+  const int rows_x = tiles_m > xcd ? (tiles_m - xcd + 7) / 8 : 0;
+  const int count_x = rows_x * tiles_n;
+  const unsigned per_group = static_cast<unsigned>(GROUP_M * tiles_n);
+  auto tile_mn = [&](int q, int64_t& m0, int& n0) {
+    const unsigned grp = static_cast<unsigned>(q) / per_group, within = static_cast<unsigned>(q) - grp * per_group;
+    const int left = rows_x - static_cast<int>(grp) * GROUP_M;
+    const unsigned rows_here = left < GROUP_M ? static_cast<unsigned>(left) : GROUP_M;   // 1 .. 4
+    unsigned col, r;
+    switch (rows_here) {   // within / rows_here without a division
+      case 4: col = within >> 2; r = within & 3; break;
+      case 2: col = within >> 1; r = within & 1; break;
+      case 1: col = within; r = 0; break;
+      default: col = within / 3; r = within - col * 3; break;
+    }
+    const int lr = static_cast<int>(grp) * GROUP_M + static_cast<int>(r);
+    m0 = static_cast<int64_t>(lr * 8 + xcd) * GM;
+    n0 = static_cast<int>(col) * GN;
   };
-  int64_t q = blockIdx.x >> 3;
+  int q = blockIdx.x >> 3;
   if (q >= count_x) return;
-  float2 rev = make_float2(0.f, 0.f);
-  if (EPI == EPI_QKV_ROPE) {
-    const int l32 = lane & 31;
-    rev.x = a.rope_rev[l32];
-    if (a.hd == 128) rev.y = a.rope_rev[32 + l32];
-  }
-  const uint16_t* ga[4];
-  const uint16_t* gb[4];
-  {
-    int64_t m0;
-    int n0;
-    tile_mn(q, m0, n0);
-    tile_sources<EPI>(a, A, M, m0, n0, w, lane, ga, gb);
-  }
-  dma_stage(sA0, sB0, ga, gb, 0, w);
+  if (EPI == EPI_QKV_ROPE && t < (a.hd >> 1)) rvbuf[t] = a.rope_rev[t];   // visible after the first barrier
+  const uint16_t* ga[8];
+  const uint16_t* gb[8];
+  int64_t m0;
+  int n0;
+  tile_mn(q, m0, n0);
+  tile_sources<EPI>(a, A, M, m0, n0, w, lane, ga, gb);
+  dma_stage(sA0, sB0, ga, gb, w);
   for (; q < count_x; q += per_xcd) {
-    int64_t m0;
-    int n0;
-    tile_mn(q, m0, n0);
-    f32x16 acc[4][2];
+    f32x16 acc[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
+        for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
     __syncthreads();   // stage 0 of this tile has landed; the last epilogue is done with rbuf / pbuf
     // the tile's row scales and positions go to LDS now, so that the epilogue
     // reads no global memory behind the next tile's prefetch
@@ -536,35 +562,37 @@ __global__ __launch_bounds__(GT) void k_gemm_bf16(GemmArgs a) {
     if (w == 1 && EPI == EPI_QKV_ROPE)
       __builtin_amdgcn_global_load_lds(static_cast<const void*>(a.pos + m0 + lane * 4), (lds_ptr_t)(pbuf + lane * 4),
                                        16, 0, 0);
+    // nk is even: stages alternate 0, 1 and the loop has no odd tail (a
+    // conditional second stage makes the compiler move the accumulators
+    // between register files every iteration)
     for (int kt = 0; kt < nk; kt += 2) {
-      if (kt + 1 < nk) dma_stage(sA1, sB1, ga, gb, (kt + 1) * GK, w);
-      mma_stage<H>(sA0, sB0, acc, wm, wn, lane);
+      mma_stage<H>(sA0, sB0, acc, wm, wn, lane, sA1, sB1, ga, gb, w, true);
       __syncthreads();
-      if (kt + 1 < nk) {
-        if (kt + 2 < nk) dma_stage(sA0, sB0, ga, gb, (kt + 2) * GK, w);
-        mma_stage<H>(sA1, sB1, acc, wm, wn, lane);
-        __syncthreads();
-      }
+      mma_stage<H>(sA1, sB1, acc, wm, wn, lane, sA0, sB0, ga, gb, w, kt + 2 < nk);
+      __syncthreads();
     }
     // stage 0 is free: the next tile's first k-step loads under the epilogue
     const bool more = q + per_xcd < count_x;
+    int64_t m1 = 0;
+    int n1 = 0;
+    if (more) tile_mn(q + per_xcd, m1, n1);
     auto prefetch = [&]() {
       if (more) {
-        int64_t m1;
-        int n1;
-        tile_mn(q + per_xcd, m1, n1);
         tile_sources<EPI>(a, A, M, m1, n1, w, lane, ga, gb);
-        dma_stage(sA0, sB0, ga, gb, 0, w);
+        dma_stage(sA0, sB0, ga, gb, w);
       }
     };
-    // each wave stages its output in its own 8 KB slice of stage 1, which is
+    // each wave stages its accumulators in its own 16 KB of stage 1, which is
     // idle until the next tile's first barrier
-    uint16_t* slice = (w < 4 ? sA1 : sB1) + (w & 3) * 4096;
-    epilogue_bf16<EPI, H>(a, acc, m0, n0, M, wm, wn, lane, slice, rbuf, pbuf, rev, prefetch);
+    float4* slice = reinterpret_cast<float4*>((w < 2 ? sA1 : sB1) + (w & 1) * 8192);
+    epilogue_bf16<EPI, H>(a, acc, m0, n0, M, wm, wn, lane, slice, rbuf, pbuf, rvbuf, prefetch);
+    m0 = m1;
+    n0 = n1;
   }
 }
 
 hipError_t launch_gemm_bf16(int epi, const GemmArgs& a, hipStream_t s) {
+  if (a.K <= 0 || a.K % (2 * GK) || a.N % GN) return hipErrorInvalidValue;   // whole pairs of k-steps, whole tiles
   // one workgroup per CU, rounded to whole XCD groups; fewer for small problems
   const int64_t tiles = ((a.m_ub + GM - 1) / GM) * (a.N / GN);
   int64_t g = num_cus();
