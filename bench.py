@@ -47,8 +47,9 @@ PEAK_HBM_GBPS = 8000.0
 # only for the GEMM source they were measured on: reported as null once
 # gemm.hip, dev_util.h or the GemmArgs declaration change, or for launches
 # not listed.
-GATE_UP_TRAFFIC = {"workload": "sweep3b", "query": 0, "bytes_by_tokens": {},
-                   "source_sha256": ""}
+GATE_UP_TRAFFIC = {"workload": "sweep3b", "query": 0,
+                   "bytes_by_tokens": {"638426": 146704830377, "1997610": 643944116665},
+                   "source_sha256": "216fa2572f45cbb512ad3d25930692ae5cb9a6eb141d27cdadb9f1f914c8304b"}
 
 
 def gemm_source_sha256() -> str:
