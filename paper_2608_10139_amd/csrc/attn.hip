@@ -1,12 +1,15 @@
 // Causal self-attention over the packed variable-length batch, grouped K/V
 // heads (query head j reads K/V head j / (n_heads / n_kv)).
 //
-// Work items are (sequence, query head) pairs walked by a persistent grid;
-// each item loops over 64-query blocks of its own sequence and, inside, over
-// 64-key blocks from the sequence start up to the diagonal, the next key
-// block's global reads in flight while the current one is consumed.  Key blocks are
-// aligned to the sequence start, so a row's result does not depend on the
-// other rows packed next to it.  Softmax is the usual online form in fp32
+// Work items are (sequence, K/V head, head group) walked by a persistent
+// grid; a workgroup holds REP of the n_heads / n_kv query heads that read one
+// K/V head (all of them when registers allow), four waves per query head, so
+// each staged key block serves all of them (its global reads happen once per
+// group instead of once per query head).  An item loops over 64-query blocks of its own sequence and, inside,
+// over 64-key blocks from the sequence start up to the diagonal, the next key
+// block's global reads in flight while the current one is consumed.  Key
+// blocks are aligned to the sequence start, so a row's result does not depend
+// on the other rows packed next to it.  Softmax is the usual online form in fp32
 // (running max and sum, rescaled output accumulator).
 //
 // MFMA path for bf16 models (hd 64 / 128): q, k, v arrive in fp16 and both
@@ -49,11 +52,12 @@ static int grid_cap(int64_t items, int cap) {
 
 
 // ======================================================================= bf16 MFMA
-template <int HD>
-__global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
+template <int HD, int REP>
+__global__ __launch_bounds__(256 * REP) void k_attn_bf16(AttnArgs a) {
   constexpr int KB = 64;            // keys per block
   constexpr int CH = HD / 8;        // 16-byte chunks per K row
-  constexpr int PER = KB * CH / 256;   // chunks of K (and of V) per thread per block
+  constexpr int NT = 256 * REP;     // threads: four waves per query head of the group
+  constexpr int PER = (KB * CH + NT - 1) / NT;   // chunks of K (and of V) per thread per block (at most)
   // K and V of one key block, row-major, 16-byte chunks XOR-swizzled by row
   // bits (K: rows 2i and 2i+1 share a pattern, so the 16 rows of a fragment
   // read hit distinct banks; V: the rows of a transposed read do)
@@ -62,8 +66,11 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
 
   lds_u16* const vs_lds = (lds_u16*)(Vs);   // LDS address space, for the transposing reads
   const int64_t tb = a.desc[D_TOK_BEGIN], sb = a.desc[D_SEQ_BEGIN], ns = a.desc[D_NSEQ];
-  const int64_t n_items = ns * a.n_heads;
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6, g = lane >> 4, c16 = lane & 15;
+  const int groups = a.n_heads / (a.n_kv * REP);   // head groups per K/V head
+  const int64_t n_items = ns * a.n_kv * groups;
+  const int t = threadIdx.x, lane = t & 63, g = lane >> 4, c16 = lane & 15;
+  const int w = (t >> 6) & 3;      // the wave's 16 queries of a 64-query block
+  const int hq = t >> 8;           // its query head inside the workgroup's group
   const int rep = a.n_heads / a.n_kv;
   const int d_q = a.n_heads * HD, d_kv = a.n_kv * HD;
   const int np = a.npre;
@@ -77,19 +84,21 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   // block of the current one is consumed.
   struct Task {
     int64_t item, s0;   // item, first packed row of the sequence's own rows
-    int L, qb, h;       // positions (prefix + own), query block, query head
+    int L, qb, h0;       // positions (prefix + own), query block, first query head of the group
   };
   // first task of the first item at or after `item` that has own rows
   auto item_task = [&](int64_t item, Task& tk) -> bool {
     for (; item < n_items; item += gridDim.x) {
-      const int64_t si = static_cast<int32_t>(item) / a.n_heads;   // items < 2^31 (checked at launch)
+      const int per_seq = a.n_kv * groups;
+      const int64_t si = static_cast<int32_t>(item) / per_seq;   // items < 2^31 (checked at launch)
       const int64_t c0 = a.cu[sb + si], c1 = a.cu[sb + si + 1];
       if (c1 > c0) {
+        const int r = static_cast<int>(item - si * per_seq);   // K/V head r / groups, group r % groups
         tk.item = item;
         tk.s0 = c0 - tb;
         tk.L = static_cast<int>(c1 - c0) + np;
         tk.qb = np / KB;
-        tk.h = static_cast<int>(item - si * a.n_heads);
+        tk.h0 = r * REP;   // K/V head r / groups owns query heads (r / groups) * rep ..
         return true;
       }
     }
@@ -110,15 +119,15 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   // this thread's K and V chunks of key block kb (zeros past L)
   uint4 kr[PER], vr[PER];
   auto fetch = [&](const Task& tk, int kb) {
-    const int kvh = tk.h / rep;
+    const int kvh = tk.h0 / rep;
     const int kcol = d_q + kvh * HD, vcol = d_q + d_kv + kvh * HD;
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
-      const int id = t + u * 256, r = id / CH, ch = id % CH;
+      const int id = t + u * NT, r = id / CH, ch = id % CH;
       const int kk = kb * KB + r;
       kr[u] = make_uint4(0, 0, 0, 0);
       vr[u] = make_uint4(0, 0, 0, 0);
-      if (kk < tk.L) {
+      if (id < KB * CH && kk < tk.L) {
         const uint16_t* row = row_of(tk, kk);
         kr[u] = *reinterpret_cast<const uint4*>(row + kcol + ch * 8);
         vr[u] = *reinterpret_cast<const uint4*>(row + vcol + ch * 8);
@@ -129,10 +138,11 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   auto load_q = [&](const Task& tk, half8 (&qf)[HD / 32]) {
     const int qi = tk.qb * KB + w * 16 + c16;
     const bool own = qi >= np && qi < tk.L;
+    const int h = tk.h0 + hq;
 #pragma unroll
     for (int kc = 0; kc < HD / 32; ++kc) {
       if (own)
-        qf[kc] = *reinterpret_cast<const half8*>(qkv + (tk.s0 + qi - np) * a.ld + tk.h * HD + kc * 32 + g * 8);
+        qf[kc] = *reinterpret_cast<const half8*>(qkv + (tk.s0 + qi - np) * a.ld + h * HD + kc * 32 + g * 8);
       else
         qf[kc] = half8{};
     }
@@ -165,9 +175,11 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
       __syncthreads();   // previous key block fully consumed
 #pragma unroll
       for (int u = 0; u < PER; ++u) {
-        const int id = t + u * 256, r = id / CH, ch = id % CH;
-        *reinterpret_cast<uint4*>(Ks + r * HD + (kswz(r, ch) << 3)) = kr[u];
-        *reinterpret_cast<uint4*>(Vs + r * HD + (vswz(r, ch) << 3)) = vr[u];
+        const int id = t + u * NT, r = id / CH, ch = id % CH;
+        if (id < KB * CH) {
+          *reinterpret_cast<uint4*>(Ks + r * HD + (kswz(r, ch) << 3)) = kr[u];
+          *reinterpret_cast<uint4*>(Vs + r * HD + (vswz(r, ch) << 3)) = vr[u];
+        }
       }
       __syncthreads();
       if (kb < qb) {
@@ -259,7 +271,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
     }
     if (qi >= np && qi < L) {
       const float inv = 1.0f / ol[0];
-      uint16_t* orow = out + (cur.s0 + qi - np) * a.ldo + cur.h * HD;
+      uint16_t* orow = out + (cur.s0 + qi - np) * a.ldo + (cur.h0 + hq) * HD;
       // output type chosen once, not per element
       auto store = [&](auto f16_tag) {
         constexpr bool F16 = decltype(f16_tag)::value;
@@ -287,17 +299,38 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
 
 hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t s) {
   if (a.npre < 0 || (a.npre > 0 && !a.pkv)) return hipErrorInvalidValue;
-  if (a.seq_ub * a.n_heads >= (int64_t(1) << 31)) return hipErrorInvalidValue;   // 32-bit item numbers
-  // 32 workgroups per CU: with work items of very unequal length (sequence
-  // lengths spread 16..512) the finer grid balances the tail better than 16
-  // per CU (-3 % on a 1B model with 32 heads; unchanged with 8 heads)
-  const int g = grid_cap(a.seq_ub * a.n_heads, 8192);
-  if (a.hd == 64)
-    hipLaunchKernelGGL(k_attn_bf16<64>, dim3(g), dim3(256), 0, s, a);
-  else if (a.hd == 128)
-    hipLaunchKernelGGL(k_attn_bf16<128>, dim3(g), dim3(256), 0, s, a);
-  else
+  if (a.n_kv <= 0 || a.n_heads % a.n_kv) return hipErrorInvalidValue;
+  const int rep = a.n_heads / a.n_kv;
+  // query heads per workgroup: the largest divisor of rep up to 4 (64-dim
+  // heads, 125 registers at 16 waves) or 3 (128-dim heads, 166 registers at 12)
+  const int cap = a.hd == 128 ? 3 : 4;
+  int hpw = 1;
+  for (int d = 1; d <= cap; ++d)
+    if (rep % d == 0) hpw = d;
+  const int64_t items = a.seq_ub * a.n_kv * (rep / hpw);
+  if (items >= (int64_t(1) << 31)) return hipErrorInvalidValue;   // 32-bit item numbers
+  // about 32 query heads' worth of workgroups per CU: with work items of very
+  // unequal length (sequence lengths spread 16..512) a fine grid balances the
+  // tail better
+  const int g = grid_cap(items, 8192 / hpw);
+#define AIQ_ATTN(HD, R) hipLaunchKernelGGL((k_attn_bf16<HD, R>), dim3(g), dim3(256 * R), 0, s, a)
+  if (a.hd == 64) {
+    switch (hpw) {
+      case 1: AIQ_ATTN(64, 1); break;
+      case 2: AIQ_ATTN(64, 2); break;
+      case 3: AIQ_ATTN(64, 3); break;
+      default: AIQ_ATTN(64, 4); break;
+    }
+  } else if (a.hd == 128) {
+    switch (hpw) {
+      case 1: AIQ_ATTN(128, 1); break;
+      case 2: AIQ_ATTN(128, 2); break;
+      default: AIQ_ATTN(128, 3); break;
+    }
+  } else {
     return hipErrorInvalidValue;
+  }
+#undef AIQ_ATTN
   return hipGetLastError();
 }
 
