@@ -253,3 +253,31 @@ def test_join_hash_groups_and_staging(rel_model, n_movies, payload):
     q = Query(preds=(Pred("a", "lt", 90),), labels=(1, 2), decision="binary_gt", agg="count_by_payload",
               n_group_keys=0, join=Join("movie_id", "movie_id", payload, bpred))
     full_check(t, m, dm, q)
+
+
+def test_hash_group_by_group_cap_and_empty(rel_model):
+    say("case: hash group by with more groups than grp_cap, and with no survivors")
+    m, dm = rel_model
+    pr = table(3000, 77)
+    pr["g"] = sparse_keys(3000, 7)
+    t = {"probe": pr, "build": None, "prefix": np.zeros(0, np.int32)}
+    q = Query(preds=(Pred("b", "lt", 40),), labels=(1, 2), decision="binary_gt", agg="avg_label_count_by",
+              group_col="g", n_group_keys=0)
+    full = full_check(t, m, dm, q)
+    assert full["status"] == 0 and len(full["groups"][0]) > 5
+
+    def cap5(dq):
+        dq.out.grp_cap = 5
+
+    capped = run(t, m, dm, q, tweak=cap5)
+    # the groups past the cap are dropped and flagged; the first five (the
+    # smallest keys) are the full run's
+    assert capped["status"] == B.AIQ_DEV_GROUP_CAP
+    assert len(capped["groups"][0]) == 5
+    for a, b in zip(capped["groups"], full["groups"]):
+        np.testing.assert_array_equal(a, b[:5])
+    # nothing passes: no groups, no flag
+    q0 = Query(preds=(Pred("b", "lt", -1000),), labels=(1, 2), decision="binary_gt", agg="avg_label_count_by",
+               group_col="g", n_group_keys=0)
+    r0 = run(t, m, dm, q0)
+    assert r0["status"] == 0 and r0["n_selected"] == 0 and len(r0["groups"][0]) == 0
