@@ -211,9 +211,10 @@ typedef struct aiq_query {
                                           AIQ_DEV_GROUP_RANGE); 0: any int32 key
                                           (INT32_MIN included), aggregated in a hash
                                           table and emitted in ascending key order;
-                                          out->grp_cap must then cover the distinct keys
+                                          out->grp_cap should then cover the distinct keys
                                           (at most the probe rows, or for COUNT_BY_PAYLOAD
-                                          the build rows) or AIQ_DEV_GROUP_CAP is set */
+                                          the build rows); with more, the grp_cap smallest
+                                          keys are written and AIQ_DEV_GROUP_CAP is set */
   /* AI_TRANSFORM (Table 1; Section 4, Q3 and Q5).  gen_tokens > 0 replaces
      the label decision: every selected row's sequence is continued by up
      to gen_tokens tokens, each the argmax of the last position's logits over
