@@ -6,8 +6,8 @@
 // filled by 16-byte direct-to-LDS loads.  Four waves, one per SIMD, in a
 // 2 x 2 grid each own a 128 x 128 sub-tile = 4 x 4 blocks of
 // v_mfma_f32_32x32x16 (256 accumulator registers per lane).  The next
-// stage's loads are spread over the MFMAs of the first half of the current
-// one (a burst of them stalls the wave's MFMA issue), and each wave's loads
+// stage's loads are spread over the MFMAs of the first three quarters of the
+// current one (a burst of them stalls the wave's MFMA issue), and each wave's loads
 // go to 4 KB-contiguous LDS runs so one M0 value serves four of them through
 // the instruction's immediate offset.  The next tile's first stage is
 // fetched while the epilogue of the current one runs.
@@ -418,8 +418,12 @@ __device__ __forceinline__ void dma_stage(uint16_t* sA, uint16_t* sB, const uint
 
 // One 64-deep k-step of the wave's sub-tile from one LDS stage (4 sub-steps of
 // 16 MFMAs).  Fragments of the next sub-step are read while the MFMAs of the
-// current one run; with `dma`, the next stage's 16 loads go out during the
-// first two sub-steps, one per MFMA pair.
+// current one run; with `dma`, the next stage's 16 loads (8 pieces of A,
+// then 8 of W) go out during the first three sub-steps, 5, 5 and 6 of them,
+// each after an MFMA.  Issued over two sub-steps, the loads back up in the
+// memory pipeline and stall MFMA issue on large problems (4 % slower at
+// 2M rows); issued over all four, the last ones are still in flight at the
+// stage's closing barrier.
 template <bool H>
 __device__ __forceinline__ void mma_stage(const uint16_t* As, const uint16_t* Bs, f32x16 (&acc)[4][4], int wm,
                                           int wn, int lane, uint16_t* nA, uint16_t* nB, const uint16_t* (&ga)[8],
@@ -431,11 +435,12 @@ __device__ __forceinline__ void mma_stage(const uint16_t* As, const uint16_t* Bs
   for (int s = 0; s < 4; ++s) {
     const int cur = s & 1;
     if (s < 3) load_frags<H>(As, Bs, s + 1, wm, wn, lane, af[cur ^ 1], bw[cur ^ 1]);
-    if (s < 2 && dma) {
+    const int l0 = (16 * s) / 3, l1 = s < 3 ? (16 * (s + 1)) / 3 : l0;   // this sub-step's loads [l0, l1)
+    if (dma) {
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int i = u, c = 8 * w + (i & 4);
-        if (s == 0) {
+      for (int l = l0; l < l1; ++l) {
+        const int i = l & 7, c = 8 * w + (i & 4);
+        if (l < 8) {
           load_lds_imm(static_cast<const void*>(ga[i]), (lds_ptr_t)(nA + c * 512), i);
           ga[i] += GK;
         } else {
@@ -449,21 +454,14 @@ __device__ __forceinline__ void mma_stage(const uint16_t* As, const uint16_t* Bs
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         acc[i][j] = Op16<H>::mma(bw[cur][j], af[cur][i], acc[i][j]);
-    if (s < 2) {
-      // 16 MFMAs, 8 fragment reads, 8 loads
-      for (int q = 0; q < 8; ++q) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
-        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-    } else if (s < 3) {
-      for (int q = 0; q < 8; ++q) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    // the first 8 MFMAs each followed by one fragment read and (while any
+    // are left) one load, then the other 8
+    for (int q = 0; q < 8; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                  // MFMA
+      if (s < 3) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);       // DS read
+      if (q < l1 - l0) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0); // VMEM read
     }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
     __builtin_amdgcn_sched_barrier(0);
   }
 }

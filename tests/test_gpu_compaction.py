@@ -35,8 +35,11 @@ def table(n, seed, vocab=500, max_len=12, tokens=True):
     lens = r.integers(0, max_len + 1, size=n).astype(np.int32)
     off = np.zeros(n + 1, dtype=np.int64)
     off[1:] = np.cumsum(lens)
-    t = {"id": np.arange(n, dtype=np.int32), "a": r.integers(-128, 128, n).astype(np.int8),
+    ids = np.arange(n, dtype=np.int32)
+    t = {"id": ids, "a": r.integers(-128, 128, n).astype(np.int8),
          "c": r.integers(0, 1000, n).astype(np.int32),
+         # runs of 64 (63) consecutive rows alike: 64 (65 or 66) runs of survivors per block of 8192
+         "g64": ((ids // 64) % 2).astype(np.int32), "g63": ((ids // 63) % 2).astype(np.int32),
          "len": lens, "offsets": off}
     if tokens:
         t["tokens"] = r.integers(0, vocab, int(off[-1])).astype(np.int32)
@@ -60,13 +63,23 @@ def same(r1, r2):
     np.testing.assert_array_equal(r1["logits"].view(np.int32), r2["logits"].view(np.int32))
 
 
-@pytest.mark.parametrize("n", [8191, 8192, 8193, 3 * 8192 + 5, 70001])
-def test_one_launch_vs_multipass_full_pipeline(rel_model, n):
-    say(f"case: one-launch vs multipass compaction, full pipeline, n={n}")
+# Survivor patterns: "mixed" about 30 % at random (thousands of runs of
+# consecutive survivors per block of 8192 rows); "all" one run per block;
+# "sparse" about 0.5 % (some 40 runs); "runs64" exactly 64 runs of 64 rows
+# per block, aligned to the 64-row mask words; "runs63" 65 or 66 runs of 63
+# rows, crossing word and block boundaries.
+PATTERNS = {"mixed": (Pred("c", "lt", 300), Pred("a", "ne", 5)), "all": (Pred("c", "lt", 1000),),
+            "sparse": (Pred("c", "lt", 5),), "runs64": (Pred("g64", "eq", 0),), "runs63": (Pred("g63", "eq", 0),)}
+CASES = [(n, "mixed") for n in (8191, 8192, 8193, 3 * 8192 + 5, 70001)] + \
+    [(n, p) for n in (8193, 70001) for p in ("all", "sparse", "runs64", "runs63")]
+
+
+@pytest.mark.parametrize("n,pattern", CASES)
+def test_one_launch_vs_multipass_full_pipeline(rel_model, n, pattern):
+    say(f"case: one-launch vs multipass compaction, full pipeline, n={n}, {pattern}")
     m, dm = rel_model
     t = {"probe": table(n, 1000 + n), "build": None, "prefix": np.array([7, 8, 9], np.int32)}
-    q = Query(preds=(Pred("c", "lt", 300), Pred("a", "ne", 5)), labels=(1, 2), decision="binary_gt",
-              agg="count", n_prefix=3)
+    q = Query(preds=PATTERNS[pattern], labels=(1, 2), decision="binary_gt", agg="count", n_prefix=3)
     r1 = run(t, m, dm, q)
     r2 = run(t, m, dm, q, multipass_compact=True)
     rows, _ = relational(t, q)
@@ -102,11 +115,11 @@ def test_one_launch_join_several_blocks(rel_model):
         np.testing.assert_array_equal(a, b)
 
 
-@pytest.mark.parametrize("k", [0, 10, 1000])
+@pytest.mark.parametrize("k", [0, 5, 10, 1000])
 def test_one_launch_many_blocks_relational_only(rel_model, k):
     """513 blocks (more than one 64-block look-back window, more blocks than
     fit on the chip at once): selected ids and the token total exact at
-    0 %, 1 % and 100 % selectivity, and equal to the multipass form."""
+    0 %, 0.5 %, 1 % and 100 % selectivity, and equal to the multipass form."""
     n = 512 * 8192 + 4321
     say(f"case: one-launch compaction, relational only, n={n}, c < {k}")
     m, dm = rel_model
