@@ -48,8 +48,8 @@ PEAK_HBM_GBPS = 8000.0
 # gemm.hip, dev_util.h or the GemmArgs declaration change, or for launches
 # not listed.
 GATE_UP_TRAFFIC = {"workload": "sweep3b", "query": 0,
-                   "bytes_by_tokens": {"638426": 146704830377, "1997610": 643944116665},
-                   "source_sha256": "216fa2572f45cbb512ad3d25930692ae5cb9a6eb141d27cdadb9f1f914c8304b"}
+                   "bytes_by_tokens": {"638426": 104782911454, "1997610": 327558568557},
+                   "source_sha256": "3889448b921d1213858839c11f8fb8cabc5537545597932df54c29f92771f185"}
 
 
 def gemm_source_sha256() -> str:
