@@ -192,8 +192,10 @@ void take_resid(const aiq_plan* p, Carver& c, Layout& L, size_t T) {
 }
 
 // Last positions of a chunk go through the pruned last layer in blocks of at
-// most LAST_ROWS_MAX sequences.
-constexpr int64_t LAST_ROWS_MAX = 65536;
+// most LAST_ROWS_MAX sequences (their fp32 residual rows: 3 GB at d 3072).
+// Every block is launched for every chunk pass, also where the selection
+// leaves it empty, so larger blocks mean fewer empty launches.
+constexpr int64_t LAST_ROWS_MAX = 262144;
 
 int64_t last_rows(int64_t seq) { return std::max<int64_t>(std::min<int64_t>(seq, LAST_ROWS_MAX), 1); }
 int32_t last_blocks(int64_t seq) {

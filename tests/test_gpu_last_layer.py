@@ -8,7 +8,7 @@ projection feed no other position).  Pinned against:
 * the oracle (fp64, per sequence) on a sample with the shortest and longest
   rows;
 * itself across chunkings and across more sequences than one block of last
-  positions holds (65,536): bit-identical, since every sequence's last
+  positions holds (262,144): bit-identical, since every sequence's last
   position is computed alone;
 * the prefill-only entry point, labels and full-vocabulary logits.
 """
@@ -114,11 +114,11 @@ def test_last_rows_vs_oracle(mname):
     assert r["count"] == agg["count"]
 
 
-def test_last_rows_chunking_and_blocks_bit_identical():
-    """70,000 selected sequences of 1..4 tokens: two blocks of last positions
-    in one chunk, and one or two per chunk over several chunks, give the same
-    bits; the result stays within tolerance of the full last layer."""
-    say("case: last positions over two blocks and several chunks")
+def test_last_rows_chunking_bit_identical():
+    """70,000 selected sequences of 1..4 tokens: one block of last positions
+    in one chunk, and one per chunk over several chunks, give the same bits;
+    the result stays within tolerance of the full last layer."""
+    say("case: last positions over one and several chunks")
     m, dm = model("mha64")
     t = tables(72000, 13, max_len=4)
     q = Query(preds=(Pred("c", "lt", 980),), labels=(1, 2), decision="binary_gt", agg="count")
@@ -128,7 +128,23 @@ def test_last_rows_chunking_and_blocks_bit_identical():
     for k in ("sel_ids", "labels", "kept_ids"):
         np.testing.assert_array_equal(one[k], chunked[k])
     np.testing.assert_array_equal(one["logits"].view(np.int32), chunked["logits"].view(np.int32))
-    close_to_full(one, run(t, m, dm, q, full_last_layer=True), "two blocks")
+    close_to_full(one, run(t, m, dm, q, full_last_layer=True), "one block")
+
+
+def test_last_rows_two_blocks_bit_identical():
+    """300,000 selected sequences of 1..2 tokens: two blocks of last
+    positions (262,144 per block) in one chunk give the same bits as one
+    block per chunk over several chunks."""
+    say("case: last positions over two blocks")
+    m, dm = model("mha64")
+    t = tables(306000, 19, max_len=2)
+    q = Query(preds=(Pred("c", "lt", 980),), labels=(1, 2), decision="binary_gt", agg="count")
+    one = run(t, m, dm, q)
+    assert one["status"] == 0 and one["n_selected"] > 262144
+    chunked = run(t, m, dm, q, chunk_tokens=200000)
+    for k in ("sel_ids", "labels", "kept_ids"):
+        np.testing.assert_array_equal(one[k], chunked[k])
+    np.testing.assert_array_equal(one["logits"].view(np.int32), chunked["logits"].view(np.int32))
 
 
 def test_last_rows_prefill_entry_point():
