@@ -49,7 +49,7 @@ PEAK_HBM_GBPS = 8000.0
 # not listed.
 GATE_UP_TRAFFIC = {"workload": "sweep3b", "query": 0,
                    "bytes_by_tokens": {"638426": 104782911454, "1997610": 327558568557},
-                   "source_sha256": "3889448b921d1213858839c11f8fb8cabc5537545597932df54c29f92771f185"}
+                   "source_sha256": "05715c2308c6ee1d93927f59414ee1b0f00e6a4038cd04fa3d51f608929013b1"}
 
 
 def gemm_source_sha256() -> str:
