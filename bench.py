@@ -651,6 +651,9 @@ def main(argv=None) -> int:
         "roofline": {"bound": "mfma", "kernel": "k_gemm_bf16<EPI_SWIGLU> (gate/up projection + SwiGLU)",
                      "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4), "traffic": traffic,
+                     "traffic_source": ("rocprofv3 FETCH_SIZE x2.000 + WRITE_SIZE x1.000 per launch of this GEMM "
+                                        "source, separate counter runs (profiles/sweep3b_hbm_traffic.md)")
+                     if traffic is not None else None,
                      "launches": int(len(up_ms)), "avg_launch_ms": round(up_avg_ms, 5),
                      "flops_per_launch": up_flops_per_launch,
                      "tokens_per_launch": sorted(set(real_tok)),
