@@ -48,8 +48,8 @@ PEAK_HBM_GBPS = 8000.0
 # gemm.hip, dev_util.h or the GemmArgs declaration change, or for launches
 # not listed.
 GATE_UP_TRAFFIC = {"workload": "sweep3b", "query": 0,
-                   "bytes_by_tokens": {"638426": 104782911454, "1997610": 327558568557},
-                   "source_sha256": "05715c2308c6ee1d93927f59414ee1b0f00e6a4038cd04fa3d51f608929013b1"}
+                   "bytes_by_tokens": {"638426": 151782041426, "1997610": 474909077312},
+                   "source_sha256": "d5599aac9567f006e273ed5f79cf6b9ca3811f909187b66d317dae12af2b7c26"}
 
 
 def gemm_source_sha256() -> str:
