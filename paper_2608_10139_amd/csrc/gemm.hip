@@ -516,9 +516,9 @@ __global__ __launch_bounds__(GT, 1) void k_gemm_bf16(GemmArgs a) {
   // group_m of its rows, column by column, so the 32 workgroups resident on
   // one XCD share a few activation row-panels and a few weight column-panels
   // in that XCD's L2 instead of streaming 32 distinct panels.  Groups of 2
-  // rows where there are at least 32 column tiles (gate/up: 1-1.8 % faster
-  // than 4; q|k|v with 20 column tiles: 2-3 % slower).
-  const int group_m = tiles_n >= 32 ? 2 : 4;
+  // rows (gate/up 1-1.8 %, O 1-3.6 %, down 0.6-1.8 % faster than 4), 4 for
+  // the q|k|v projection (2 is 2-3 % slower there).
+  constexpr int group_m = EPI == EPI_QKV_ROPE ? 4 : 2;
   const int tiles_m = static_cast<int>((M + GM - 1) / GM);   // < 2^31 (M < 2^39)
   const int xcd = blockIdx.x & 7;
   const int per_xcd = gridDim.x >> 3;   // grid is a multiple of 8
