@@ -48,8 +48,8 @@ PEAK_HBM_GBPS = 8000.0
 # gemm.hip, dev_util.h or the GemmArgs declaration change, or for launches
 # not listed.
 GATE_UP_TRAFFIC = {"workload": "sweep3b", "query": 0,
-                   "bytes_by_tokens": {"638426": 151782041426, "1997610": 474909077312},
-                   "source_sha256": "d5599aac9567f006e273ed5f79cf6b9ca3811f909187b66d317dae12af2b7c26"}
+                   "bytes_by_tokens": {"638426": 151782134473, "1997610": 474908628809},
+                   "source_sha256": "39a9579834657bf68e4c440cfae4d1536bf1406aa94f521daf414d6c12217e0c"}
 
 
 def gemm_source_sha256() -> str:
