@@ -425,13 +425,11 @@ __device__ __forceinline__ void dma_stage(uint16_t* sA, uint16_t* sB, const uint
 // issued over all four, the last ones are still in flight at the stage's
 // closing barrier.  The source pointers point at the k-block after the one
 // being consumed; `dma` is false in the tile's last stage, when they are one
-// past the row's end.  With UNIFORM the loads then re-read the row's last
-// k-block into the idle stage and the pointers stay, so every stage runs the
-// same straight-line schedule (a branch around the loads splits the stage
-// into blocks that the scheduler cannot interleave: 1-2 % slower).  The
-// residual epilogues skip the loads instead (with the re-read the O
-// projection measured 4-9 % slower, the down projection 1 %).
-template <bool H, bool UNIFORM>
+// past the row's end.  The loads then re-read the row's last k-block into the
+// idle stage and the pointers stay, so every stage runs the same
+// straight-line schedule (a branch around the loads splits the stage into
+// blocks that the scheduler cannot interleave: 1-2 % slower).
+template <bool H>
 __device__ __forceinline__ void mma_stage(const uint16_t* As, const uint16_t* Bs, f32x16 (&acc)[4][4], int wm,
                                           int wn, int lane, uint16_t* nA, uint16_t* nB, const uint16_t* (&ga)[8],
                                           const uint16_t* (&gb)[8], int w, bool dma) {
@@ -443,18 +441,16 @@ __device__ __forceinline__ void mma_stage(const uint16_t* As, const uint16_t* Bs
     const int cur = s & 1;
     if (s < 3) load_frags<H>(As, Bs, s + 1, wm, wn, lane, af[cur ^ 1], bw[cur ^ 1]);
     const int l0 = (16 * s) / 3, l1 = s < 3 ? (16 * (s + 1)) / 3 : l0;   // this sub-step's loads [l0, l1)
-    if (UNIFORM || dma) {
-      const int back = dma ? 0 : -GK, adv = dma ? GK : 0;
+    const int back = dma ? 0 : -GK, adv = dma ? GK : 0;
 #pragma unroll
-      for (int l = l0; l < l1; ++l) {
-        const int i = l & 7, c = 8 * w + (i & 4);
-        if (l < 8) {
-          load_lds_imm(static_cast<const void*>(ga[i] + back), (lds_ptr_t)(nA + c * 512), i);
-          ga[i] += adv;
-        } else {
-          load_lds_imm(static_cast<const void*>(gb[i] + back), (lds_ptr_t)(nB + c * 512), i);
-          gb[i] += adv;
-        }
+    for (int l = l0; l < l1; ++l) {
+      const int i = l & 7, c = 8 * w + (i & 4);
+      if (l < 8) {
+        load_lds_imm(static_cast<const void*>(ga[i] + back), (lds_ptr_t)(nA + c * 512), i);
+        ga[i] += adv;
+      } else {
+        load_lds_imm(static_cast<const void*>(gb[i] + back), (lds_ptr_t)(nB + c * 512), i);
+        gb[i] += adv;
       }
     }
 #pragma unroll
@@ -573,11 +569,10 @@ __global__ __launch_bounds__(GT, 1) void k_gemm_bf16(GemmArgs a) {
     // nk is even: stages alternate 0, 1 and the loop has no odd tail (a
     // conditional second stage makes the compiler move the accumulators
     // between register files every iteration)
-    constexpr bool UNIFORM = EPI != EPI_RESID && EPI != EPI_RESID_EMB;
     for (int kt = 0; kt < nk; kt += 2) {
-      mma_stage<H, UNIFORM>(sA0, sB0, acc, wm, wn, lane, sA1, sB1, ga, gb, w, true);
+      mma_stage<H>(sA0, sB0, acc, wm, wn, lane, sA1, sB1, ga, gb, w, true);
       __syncthreads();
-      mma_stage<H, UNIFORM>(sA1, sB1, acc, wm, wn, lane, sA0, sB0, ga, gb, w, kt + 2 < nk);
+      mma_stage<H>(sA1, sB1, acc, wm, wn, lane, sA0, sB0, ga, gb, w, kt + 2 < nk);
       __syncthreads();
     }
     // stage 0 is free: the next tile's first k-step loads under the epilogue
