@@ -48,8 +48,8 @@ PEAK_HBM_GBPS = 8000.0
 # gemm.hip, dev_util.h or the GemmArgs declaration change, or for launches
 # not listed.
 GATE_UP_TRAFFIC = {"workload": "sweep3b", "query": 0,
-                   "bytes_by_tokens": {"638426": 151782134473, "1997610": 474908628809},
-                   "source_sha256": "39a9579834657bf68e4c440cfae4d1536bf1406aa94f521daf414d6c12217e0c"}
+                   "bytes_by_tokens": {"638426": 151782014897, "1997610": 474910304578},
+                   "source_sha256": "137ed84b5acce862216939a61b7f3e78872639b642de8f6e9e2b16100157c9ae"}
 
 
 def gemm_source_sha256() -> str:
