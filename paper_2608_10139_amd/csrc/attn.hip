@@ -220,8 +220,17 @@ __global__ __launch_bounds__(256 * REP) void k_attn_bf16(AttnArgs a) {
       for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int e = 0; e < 4; ++e) mx = fmaxf(mx, sacc[j][e]);
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      // across the four 16-lane rows: v_permlane16_swap with both operands
+      // the same value leaves rows (x0, x0, x2, x2) in one result and
+      // (x1, x1, x3, x3) in the other; v_permlane32_swap then pairs the two
+      // halves of the wave.  Plain VALU ops, not LDS round trips (2 % faster
+      // than two lane shuffles through the LDS crossbar).
+      {
+        const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+        mx = fmaxf(__uint_as_float(r16[0]), __uint_as_float(r16[1]));
+        const auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+        mx = fmaxf(__uint_as_float(r32[0]), __uint_as_float(r32[1]));
+      }
       // scale > 0, so the maximum of the scaled scores is the scaled maximum;
       // it is finite: each block holds a key at or before every query
       const float m_new = fmaxf(m_run, mx * scale);
