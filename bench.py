@@ -673,7 +673,7 @@ def main(argv=None) -> int:
         a.no_cpu_baseline = a.no_split = True   # both classify single rows
         result["cpu_baseline"] = None
     if not a.no_relational_scale and not gen and not pairs:
-        result["relational_scale"] = relational_scale_leg(B, torch, [1 << 26], [10, 1000], steps=5)
+        result["relational_scale"] = relational_scale_leg(B, torch, [1 << 26, 1 << 28], [10, 1000], steps=5)
     if not a.no_cpu_baseline:
         log("[bench] cpu baseline (oracle on a sample)")
         result["cpu_baseline"] = cpu_baseline_leg(tables, model, q, spec, a.cpu_flop)
