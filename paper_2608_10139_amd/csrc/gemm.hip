@@ -129,6 +129,16 @@ typedef f32x16_t f32x16;
 // q, k and v (attention operands) are stored in fp16: 10 mantissa bits where
 // bf16 has 7, at the same MFMA rate; their magnitudes are O(1) after RMSNorm.
 
+// Lane exchange through a DPP move (a VALU op; a lane shuffle goes through
+// the LDS crossbar).  The residual epilogue's butterfly takes the same
+// partners and adds in the same order as lane ^ 1, ^ 2, ^ 4 shuffles: after
+// the first two steps the four lanes of a quad hold equal sums, so the
+// mirrored quad is the ^ 4 partner's.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
 __device__ __forceinline__ float silu_fast(float g) {
   return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g));
 }
@@ -256,9 +266,9 @@ __device__ __forceinline__ void epilogue_bf16(const GemmArgs& a, f32x16 (&acc)[4
                 ((x1.x * x1.x + x1.y * x1.y) + (x1.z * x1.z + x1.w * x1.w));
         }
         if (norm) {
-          ssq += __shfl_xor(ssq, 1);
-          ssq += __shfl_xor(ssq, 2);
-          ssq += __shfl_xor(ssq, 4);
+          ssq += dpp_f32<0xB1>(ssq);    // quad_perm [1,0,3,2]: lane ^ 1
+          ssq += dpp_f32<0x4E>(ssq);    // quad_perm [2,3,0,1]: lane ^ 2
+          ssq += dpp_f32<0x141>(ssq);   // row_half_mirror: the other quad of the eight, whose lanes agree
           if ((pc & 7) == 0 && m < M) a.ssp[m * a.n_part + ((nw >> 6) + (pc >> 3))] = ssq;
         }
       }
